@@ -1,0 +1,263 @@
+"""Pins for the fp64 TTM oracle against things other than itself.
+
+* explicit index sums (brute force) on tiny shapes, masks included;
+* d = 1 is a plain matrix product; all ranks 1 is a Kronecker product;
+* central finite differences for dX and every dG_k;
+* zeroing rank-mask entries equals deleting those bond slices;
+* inner-product identities <dG_k, G_k> = <dX, X> = <Y, dY> at workload size;
+* the paper's large-batch path (Alg. path; eq. path-T1 .. path-gGi<d) on the
+  unit-mode TT layout of Sec. 4.2.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+from oracle import ttm
+from paper_2405_14377_amd import workloads as wl
+
+pytestmark = pytest.mark.filterwarnings("ignore")
+
+
+def _rand_problem(seed, d, b=3, max_factor=3, max_rank=3, masks="real"):
+    rng = np.random.default_rng(seed)
+    shape = wl.random_ttm_shape(rng, d, max_factor=max_factor, max_rank=max_rank)
+    cores = wl.random_cores(rng, shape)
+    if masks == "real":
+        D = [rng.standard_normal(shape.r[k + 1]) for k in range(d - 1)]
+        for Dk in D:                       # plant an exact zero where possible
+            if Dk.size > 1:
+                Dk[rng.integers(Dk.size)] = 0.0
+    else:
+        D = None
+    X = rng.standard_normal((b, shape.n_in))
+    dY = rng.standard_normal((b, shape.n_out))
+    return shape, cores, D, X, dY
+
+
+def _brute(shape, cores, D, X, dY):
+    """Y, dX, dG by explicit sums over every index of the definition."""
+    d = shape.d
+    G = [np.asarray(c, np.float64) for c in cores]
+    Dm = [np.ones(shape.r[k + 1]) if D is None else np.asarray(D[k], np.float64) for k in range(d - 1)]
+    b = X.shape[0]
+    Y = np.zeros((b, shape.n_out))
+    dX = np.zeros((b, shape.n_in))
+    dG = [np.zeros(g.shape) for g in G]
+    XtdY = X.T @ dY                           # only used as sum_b X[b,i] dY[b,j]; a plain product
+    iranges = [range(x) for x in shape.n]
+    jranges = [range(x) for x in shape.m]
+    aranges = [range(shape.r[k]) for k in range(1, d)]
+    for it in itertools.product(*iranges):
+        i = 0
+        for k in range(d):
+            i = i * shape.n[k] + it[k]
+        for jt in itertools.product(*jranges):
+            j = 0
+            for k in range(d):
+                j = j * shape.m[k] + jt[k]
+            w = 0.0
+            for at in itertools.product(*aranges):
+                a = (0,) + at + (0,)
+                fac = [G[k][a[k], jt[k], it[k], a[k + 1]] for k in range(d)]
+                msk = [Dm[k][a[k + 1]] for k in range(d - 1)]
+                term = np.prod(fac) * np.prod(msk)
+                w += term
+                for k in range(d):
+                    rest = np.prod([fac[l] for l in range(d) if l != k]) * np.prod(msk)
+                    dG[k][a[k], jt[k], it[k], a[k + 1]] += XtdY[i, j] * rest
+            Y[:, j] += X[:, i] * w
+            dX[:, i] += dY[:, j] * w
+    return Y, dX, dG
+
+
+@pytest.mark.parametrize("seed,d", [(s, d) for d in (1, 2, 3) for s in range(4)] + [(11, 4), (12, 4)])
+def test_brute_force(seed, d):
+    shape, cores, D, X, dY = _rand_problem(seed, d, max_factor=3 if d < 4 else 2,
+                                            max_rank=3 if d < 4 else 2)
+    Yb, dXb, dGb = _brute(shape, cores, D, X, dY)
+    for route_f, route_b in ((ttm.forward_dense, ttm.backward_dense), (ttm.forward_direct, ttm.backward_direct)):
+        Y = route_f(X, cores, D)
+        dX, dG = route_b(X, dY, cores, D)
+        np.testing.assert_allclose(Y, Yb, rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(dX, dXb, rtol=1e-12, atol=1e-12)
+        for k in range(d):
+            np.testing.assert_allclose(dG[k], dGb[k], rtol=1e-12, atol=1e-12)
+
+
+def test_d1_is_matmul():
+    rng = np.random.default_rng(5)
+    G = rng.standard_normal((1, 7, 5, 1))
+    X = rng.standard_normal((4, 5))
+    dY = rng.standard_normal((4, 7))
+    A = G[0, :, :, 0]                      # [m, n]
+    np.testing.assert_allclose(ttm.forward_dense(X, [G]), X @ A.T, rtol=1e-13)
+    np.testing.assert_allclose(ttm.forward_direct(X, [G]), X @ A.T, rtol=1e-13)
+    dX, dG = ttm.backward_direct(X, dY, [G])
+    np.testing.assert_allclose(dX, dY @ A, rtol=1e-13)
+    np.testing.assert_allclose(dG[0][0, :, :, 0], dY.T @ X, rtol=1e-13)
+
+
+@pytest.mark.parametrize("n,m", [((2, 3, 4), (5, 2, 3)), ((3, 1, 2, 2), (1, 4, 2, 3))])
+def test_rank_one_is_kronecker(n, m):
+    rng = np.random.default_rng(7)
+    d = len(n)
+    cores = [rng.standard_normal((1, m[k], n[k], 1)) for k in range(d)]
+    A = [cores[k][0, :, :, 0].T for k in range(d)]          # [n_k, m_k]
+    K = A[0]
+    for k in range(1, d):
+        K = np.kron(K, A[k])
+    np.testing.assert_allclose(ttm.dense_weight(cores), K, rtol=1e-13)
+    X = rng.standard_normal((3, int(np.prod(n))))
+    np.testing.assert_allclose(ttm.forward_direct(X, cores), X @ K, rtol=1e-12)
+
+
+@pytest.mark.parametrize("seed,d", [(21, 2), (22, 3), (23, 3)])
+def test_finite_differences(seed, d):
+    shape, cores, D, X, dY = _rand_problem(seed, d, b=2)
+    h = 1e-6
+
+    def loss(Xv, cs):
+        return float(np.sum(ttm.forward_direct(Xv, cs, D) * dY))
+
+    for route in (ttm.backward_dense, ttm.backward_direct):
+        dX, dG = route(X, dY, cores, D)
+        for idx in np.ndindex(*X.shape):
+            Xp = X.copy(); Xp[idx] += h
+            Xm = X.copy(); Xm[idx] -= h
+            fd = (loss(Xp, cores) - loss(Xm, cores)) / (2 * h)
+            assert abs(fd - dX[idx]) < 1e-6 * max(1.0, abs(fd))
+        for k in range(d):
+            Gk = np.asarray(cores[k], np.float64)
+            for idx in np.ndindex(*Gk.shape):
+                cp = [np.asarray(c, np.float64) for c in cores]
+                cm = [np.asarray(c, np.float64) for c in cores]
+                cp[k] = Gk.copy(); cp[k][idx] += h
+                cm[k] = Gk.copy(); cm[k][idx] -= h
+                fd = (loss(X, cp) - loss(X, cm)) / (2 * h)
+                assert abs(fd - dG[k][idx]) < 1e-6 * max(1.0, abs(fd)), (k, idx, fd, dG[k][idx])
+
+
+def _delete_slice(cores, k, a):
+    """Remove entry a of bond k (between core k and k+1)."""
+    out = [np.asarray(c, np.float64).copy() for c in cores]
+    out[k] = np.delete(out[k], a, axis=3)
+    out[k + 1] = np.delete(out[k + 1], a, axis=0)
+    return out
+
+
+@pytest.mark.parametrize("seed", [31, 32, 33])
+def test_rank_mask_deletion_invariant(seed):
+    rng = np.random.default_rng(seed)
+    shape = wl.TTMLayerShape("t", (2, 3, 2), (3, 2, 2), (1, 4, 3, 1))
+    cores = wl.random_cores(rng, shape)
+    X = rng.standard_normal((5, shape.n_in))
+    dY = rng.standard_normal((5, shape.n_out))
+    k, a = int(rng.integers(2)), None
+    a = int(rng.integers(shape.r[k + 1]))
+    D = [np.ones(shape.r[1]), np.ones(shape.r[2])]
+    D[k][a] = 0.0
+    red = _delete_slice(cores, k, a)
+    for fwd, bwd in ((ttm.forward_dense, ttm.backward_dense), (ttm.forward_direct, ttm.backward_direct)):
+        np.testing.assert_allclose(fwd(X, cores, D), fwd(X, red), rtol=1e-12, atol=1e-13)
+        dX, dG = bwd(X, dY, cores, D)
+        dXr, dGr = bwd(X, dY, red)
+        np.testing.assert_allclose(dX, dXr, rtol=1e-12, atol=1e-13)
+        keep = [i for i in range(shape.r[k + 1]) if i != a]
+        for l in range(3):
+            g = dG[l]
+            if l == k:
+                assert np.all(g[..., a] == 0.0)
+                g = g[..., keep]
+            if l == k + 1:
+                assert np.all(g[a] == 0.0)
+                g = g[keep]
+            np.testing.assert_allclose(g, dGr[l], rtol=1e-12, atol=1e-13)
+    # a fully masked bond makes the layer identically zero
+    Dz = [np.ones(shape.r[1]), np.zeros(shape.r[2])]
+    assert np.all(ttm.forward_direct(X, cores, Dz) == 0.0)
+    dX, dG = ttm.backward_direct(X, dY, cores, Dz)
+    assert np.all(dX == 0.0) and all(np.all(g == 0.0) for g in dG)
+
+
+@pytest.mark.parametrize("wid,rows", [(0, 32), (1, 256)])
+def test_inner_product_identities_and_routes(wid, rows):
+    w = wl.WORKLOADS[wid]
+    sh = w.layers[0]
+    li = wl.ttm_layer_inputs(wid, 0, sh, w.mask)
+    X = wl.activations(wid, w.batch, sh.n_in, 0, "f32", rows=rows)
+    dY = wl.activations(wid, w.batch, sh.n_out, 1, "f32", rows=rows)
+    Y = ttm.forward_dense(X, li.cores, li.masks)
+    Yd = ttm.forward_direct(X, li.cores, li.masks)
+    np.testing.assert_allclose(Yd, Y, rtol=1e-10, atol=1e-10 * np.abs(Y).max())
+    dX, dG = ttm.backward_dense(X, dY, li.cores, li.masks)
+    dXd, dGd = ttm.backward_direct(X, dY, li.cores, li.masks)
+    ref = float(np.sum(Y * dY))
+    assert abs(float(np.sum(dX * X)) - ref) < 1e-9 * abs(ref) + 1e-9
+    for k in range(sh.d):
+        assert abs(float(np.sum(dG[k] * li.cores[k])) - ref) < 1e-9 * abs(ref) + 1e-9
+        np.testing.assert_allclose(dGd[k], dG[k], rtol=1e-9, atol=1e-10 * np.abs(dG[k]).max())
+    np.testing.assert_allclose(dXd, dX, rtol=1e-10, atol=1e-10 * np.abs(dX).max())
+    # the core scale targets Var(Y) ~ 1
+    assert 0.5 < float(Y.std()) < 2.0
+
+
+# --------------------------------------------------------------------------- paper's TT path
+def _tt_to_ttm_unit(tt_cores, d):
+    """Sec. 4.2 TT layout: 2d three-way cores, inputs first then outputs -> TTM with unit modes."""
+    out = []
+    for k, G in enumerate(tt_cores):
+        if k < d:
+            out.append(G[:, None, :, :])        # m = 1, n = n_k
+        else:
+            out.append(G[:, :, None, :])        # m = n_k, n = 1
+    return out
+
+
+def _chain3(cores):
+    P = cores[0]
+    for G in cores[1:]:
+        P = np.tensordot(P, G, axes=([-1], [0]))
+    return P
+
+
+@pytest.mark.parametrize("seed,d", [(41, 2), (42, 3)])
+def test_paper_tt_path(seed, d):
+    rng = np.random.default_rng(seed)
+    ns = [int(x) for x in rng.integers(2, 4, 2 * d)]
+    rs = [1] + [int(x) for x in rng.integers(2, 5, 2 * d - 1)] + [1]
+    G = [rng.standard_normal((rs[i], ns[i], rs[i + 1])) for i in range(2 * d)]
+    b = 4
+    N1 = int(np.prod(ns[:d])); N2 = int(np.prod(ns[d:]))
+    X = rng.standard_normal((b, N1))
+    gY = rng.standard_normal((b, N2))
+    rd = rs[d]
+    # A_d = G_1 x ... x G_d -> [N1, r_d]; B_d = G_{d+1} x ... x G_{2d} -> [r_d, N2]
+    A = _chain3(G[:d]).reshape(N1, rd)
+    B = _chain3(G[d:]).reshape(rd, N2)
+    T1 = X @ A                         # eq. path-T1
+    Y = T1 @ B                         # eq. path-Y
+    U1 = gY @ B.T                      # eq. path-U1
+    gX = U1 @ A.T                      # eq. path-gX
+    T2 = T1.T @ gY                     # eq. path-T2: [r_d, N2]
+    U2 = U1.T @ X                      # eq. path-U2: [r_d, N1]
+    gG = []
+    for i in range(d):                 # eq. path-gGi<d: contract U2 with A_{i-1} and A_{-(d-i)}
+        left = _chain3(G[:i]).reshape(-1, rs[i]) if i > 0 else np.ones((1, 1))
+        right = _chain3(G[i + 1:d]).reshape(rs[i + 1], -1, rd) if i < d - 1 else np.eye(rd).reshape(rd, 1, rd)
+        U2r = U2.reshape(rd, left.shape[0], ns[i], right.shape[1])
+        gG.append(np.einsum("cLnR,La,bRc->anb", U2r, left, right))
+    for i in range(d, 2 * d):          # eq. path-gGi>d: contract T2 with B_{i-1-d} and B_{-(2d-i)}
+        left = _chain3(G[d:i]).reshape(rd, -1, rs[i]) if i > d else np.eye(rd).reshape(rd, 1, rd)
+        right = _chain3(G[i + 1:]).reshape(rs[i + 1], -1) if i < 2 * d - 1 else np.ones((1, 1))
+        T2r = T2.reshape(rd, left.shape[1], ns[i], right.shape[1])
+        gG.append(np.einsum("cLnR,cLa,bR->anb", T2r, left, right))
+    ttm_cores = _tt_to_ttm_unit(G, d)
+    np.testing.assert_allclose(ttm.forward_direct(X, ttm_cores), Y, rtol=1e-11)
+    np.testing.assert_allclose(ttm.forward_dense(X, ttm_cores), Y, rtol=1e-11)
+    for route in (ttm.backward_direct, ttm.backward_dense):
+        dX, dG = route(X, gY, ttm_cores)
+        np.testing.assert_allclose(dX, gX, rtol=1e-11)
+        for i in range(2 * d):
+            got = dG[i][:, 0, :, :] if i < d else dG[i][:, :, 0, :]
+            np.testing.assert_allclose(got, gG[i], rtol=1e-10, atol=1e-12)
