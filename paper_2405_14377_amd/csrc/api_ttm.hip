@@ -1,0 +1,255 @@
+// extern "C" entry points for one TTM linear layer: comera_ttm_forward and
+// comera_ttm_backward.  Every step runs as a kernel on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+
+#include "internal.h"
+
+using namespace comera;
+
+namespace {
+
+inline char *at(void *ws, size_t off) { return reinterpret_cast<char *>(ws) + off; }
+
+struct DenseBuild {
+    float *gc[kMaxCores];
+    float *P[kMaxCores + 1];  // P[k] = product of cores 0..k-1, k = 1..d-1
+};
+
+// Steps shared by forward and backward: fold the masks into compacted core
+// copies, then build the left chains P_1..P_{d-1} and W (eq. TTM / Wcompress).
+int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *const *D, void *ws, void *stream,
+                DenseBuild &bd) {
+    const DenseLayout &L = p->dense;
+    const int d = p->d;
+    FoldArgs fa;
+    std::memset(&fa, 0, sizeof(fa));
+    fa.d = d;
+    fa.nfold = d;
+    fa.compacted = p->compacted ? 1 : 0;
+    for (int k = 0; k < d; ++k) {
+        fa.G[k] = G[k];
+        fa.D[k] = (D && k < d - 1) ? D[k] : nullptr;
+        bd.gc[k] = reinterpret_cast<float *>(at(ws, L.gc[k]));
+        fa.Gc[k] = bd.gc[k];
+        fa.m[k] = int(p->s.m[k]);
+        fa.n[k] = int(p->s.n[k]);
+    }
+    for (int k = 0; k <= d; ++k) {
+        fa.r[k] = int(p->s.r[k]);
+        fa.rc[k] = int(p->rho[k]);
+        fa.act[k] = p->act[k];
+    }
+    int e = launch_fold(fa, stream);
+    if (e) return e;
+    const bool bf = p->s.act == COMERA_BF16;
+    int64_t Il = 1, Jl = 1;
+    const float *prev = nullptr;
+    for (int k = 0; k < d; ++k) {
+        const bool last = k == d - 1;
+        float *out = last ? (bf ? nullptr : reinterpret_cast<float *>(at(ws, L.w)))
+                          : reinterpret_cast<float *>(at(ws, L.p[k + 1]));
+        uint16_t *outb = (last && bf) ? reinterpret_cast<uint16_t *>(at(ws, L.w)) : nullptr;
+        e = launch_chain(prev, bd.gc[k], out, outb, Il, Jl, int(p->rho[k]), int(p->s.m[k]), int(p->s.n[k]),
+                         int(p->rho[k + 1]), 2, stream);
+        if (e) return e;
+        if (!last) {
+            bd.P[k + 1] = out;
+            prev = out;
+        }
+        Il *= p->s.n[k];
+        Jl *= p->s.m[k];
+    }
+    return 0;
+}
+
+comera_status hip_status(int e) { return e ? COMERA_ERR_HIP : COMERA_OK; }
+
+}  // namespace
+
+namespace comera {
+
+void timing_begin(comera_ttm_plan_s *p, int kernel, void *stream, void **ev0) {
+    *ev0 = nullptr;
+    if (!p->timing.on) return;
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return;
+    hipEventRecord(e, hipStream_t(stream));
+    *ev0 = e;
+    (void)kernel;
+}
+
+void timing_end(comera_ttm_plan_s *p, int kernel, void *stream, void *ev0) {
+    if (!p->timing.on || !ev0) return;
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) {
+        hipEventDestroy(hipEvent_t(ev0));
+        return;
+    }
+    hipEventRecord(e, hipStream_t(stream));
+    p->timing.ev[kernel].push_back({ev0, e});
+}
+
+void timing_clear(comera_ttm_plan_s *p) {
+    for (auto &v : p->timing.ev) {
+        for (auto &pr : v) {
+            hipEventDestroy(hipEvent_t(pr.first));
+            hipEventDestroy(hipEvent_t(pr.second));
+        }
+        v.clear();
+    }
+}
+
+}  // namespace comera
+
+extern "C" {
+
+comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, const float *const *G,
+                                 const float *const *D, void *Y, void *ws, size_t ws_bytes, void *stream) {
+    if (!p || b < 0 || b > p->batch) return COMERA_ERR_INVALID_ARG;
+    if (b == 0) return COMERA_OK;
+    if (!X || !Y) return COMERA_ERR_INVALID_ARG;
+    const size_t esz = p->s.act == COMERA_BF16 ? 2 : 4;
+    if (p->zero) return hip_status(launch_fill_zero(Y, size_t(b) * size_t(p->N_out) * esz, stream));
+    if (!G) return COMERA_ERR_INVALID_ARG;
+    for (int k = 0; k < p->d; ++k)
+        if (!G[k]) return COMERA_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < p->ws_bytes) return COMERA_ERR_WORKSPACE;
+    DenseBuild bd;
+    int e = build_dense(p, G, D, ws, stream, bd);
+    if (e) return COMERA_ERR_HIP;
+    void *ev;
+    timing_begin(p, COMERA_KERNEL_FWD, stream, &ev);
+    e = launch_gemm(p->s.act, true, false, p->s.act == COMERA_BF16, X, at(ws, p->dense.w), Y, b, p->N_out, p->N_in,
+                    p->N_in, p->N_out, p->N_out, 1, p->N_in, stream);
+    timing_end(p, COMERA_KERNEL_FWD, stream, ev);
+    return hip_status(e);
+}
+
+comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X, const void *dY,
+                                  const float *const *G, const float *const *D, void *dX, float *const *dG,
+                                  void *ws, size_t ws_bytes, void *stream) {
+    if (!p || b < 0 || b > p->batch) return COMERA_ERR_INVALID_ARG;
+    const int d = p->d;
+    const size_t esz = p->s.act == COMERA_BF16 ? 2 : 4;
+    bool want_dg = false;
+    if (dG)
+        for (int k = 0; k < d; ++k) want_dg = want_dg || dG[k];
+    // nothing flows when the batch is empty or a bond is fully masked
+    if (b == 0 || p->zero) {
+        int e = 0;
+        if (dX && b > 0) e = launch_fill_zero(dX, size_t(b) * size_t(p->N_in) * esz, stream);
+        for (int k = 0; want_dg && k < d && !e; ++k)
+            if (dG[k])
+                e = launch_fill_zero(dG[k], sizeof(float) * size_t(p->s.r[k] * p->s.m[k] * p->s.n[k] * p->s.r[k + 1]),
+                                     stream);
+        return hip_status(e);
+    }
+    if (!dY || !G || (want_dg && !X)) return COMERA_ERR_INVALID_ARG;
+    for (int k = 0; k < d; ++k)
+        if (!G[k]) return COMERA_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < p->ws_bytes) return COMERA_ERR_WORKSPACE;
+    const DenseLayout &L = p->dense;
+    DenseBuild bd;
+    int e = build_dense(p, G, D, ws, stream, bd);
+    if (e) return COMERA_ERR_HIP;
+    if (dX) {
+        // dX[b, N_in] = dY[b, N_out] W^T  (eq. back X)
+        void *ev;
+        timing_begin(p, COMERA_KERNEL_DX, stream, &ev);
+        e = launch_gemm(p->s.act, true, true, p->s.act == COMERA_BF16, dY, at(ws, L.w), dX, b, p->N_in, p->N_out,
+                        p->N_out, p->N_out, p->N_in, 1, p->N_out, stream);
+        timing_end(p, COMERA_KERNEL_DX, stream, ev);
+        if (e) return COMERA_ERR_HIP;
+    }
+    if (!want_dg) return COMERA_OK;
+    // dW[N_in, N_out] = X^T dY, split over tokens, fixed-order split sum
+    const int splits = int((b + L.dw_kchunk - 1) / L.dw_kchunk);
+    float *dw = reinterpret_cast<float *>(at(ws, L.dw));
+    float *dwp = splits > 1 ? reinterpret_cast<float *>(at(ws, L.dw_part)) : dw;
+    void *ev;
+    timing_begin(p, COMERA_KERNEL_DW, stream, &ev);
+    e = launch_gemm(p->s.act, false, false, false, X, dY, dwp, p->N_in, p->N_out, b, p->N_in, p->N_out, p->N_out,
+                    splits, L.dw_kchunk, stream);
+    timing_end(p, COMERA_KERNEL_DW, stream, ev);
+    if (e) return COMERA_ERR_HIP;
+    if (splits > 1) {
+        e = launch_sum_splits(dwp, dw, p->N_in * p->N_out, splits, stream);
+        if (e) return COMERA_ERR_HIP;
+    }
+    // right environments E_k = dW contracted with cores k..d-1
+    float *E[kMaxCores + 1];
+    E[d] = dw;
+    int64_t Il = p->N_in, Jl = p->N_out;
+    for (int k = d - 1; k >= 1; --k) {
+        Il /= p->s.n[k];
+        Jl /= p->s.m[k];
+        E[k] = reinterpret_cast<float *>(at(ws, L.e[k]));
+        e = launch_adjoint(E[k + 1], bd.gc[k], E[k], Il, Jl, int(p->rho[k]), int(p->s.m[k]), int(p->s.n[k]),
+                           int(p->rho[k + 1]), 2, stream);
+        if (e) return COMERA_ERR_HIP;
+    }
+    // core gradients: meet of P_k and E_{k+1} (eq. back Gi), then expand
+    ExpandArgs xa;
+    std::memset(&xa, 0, sizeof(xa));
+    xa.d = d;
+    xa.compacted = p->compacted ? 1 : 0;
+    Il = 1;
+    Jl = 1;
+    for (int k = 0; k < d; ++k) {
+        float *part = reinterpret_cast<float *>(at(ws, L.gpart[k]));
+        if (dG[k]) {
+            e = launch_meet(k == 0 ? nullptr : bd.P[k], E[k + 1], part, Il, Jl, int(p->rho[k]), int(p->s.m[k]),
+                            int(p->s.n[k]), int(p->rho[k + 1]), 2, L.meet_splits[k], stream);
+            if (e) return COMERA_ERR_HIP;
+        }
+        xa.part[k] = part;
+        xa.D[k] = (D && k < d - 1) ? D[k] : nullptr;
+        xa.dG[k] = dG[k];
+        xa.m[k] = int(p->s.m[k]);
+        xa.n[k] = int(p->s.n[k]);
+        xa.splits[k] = L.meet_splits[k];
+        Il *= p->s.n[k];
+        Jl *= p->s.m[k];
+    }
+    for (int k = 0; k <= d; ++k) {
+        xa.r[k] = int(p->s.r[k]);
+        xa.rc[k] = int(p->rho[k]);
+        xa.act[k] = p->act[k];
+    }
+    return hip_status(launch_expand(xa, stream));
+}
+
+comera_status comera_ttm_plan_set_timing(comera_ttm_plan_t p, int32_t enable) {
+    if (!p) return COMERA_ERR_INVALID_ARG;
+    p->timing.on = enable != 0;
+    if (!p->timing.on) timing_clear(p);
+    return COMERA_OK;
+}
+
+comera_status comera_ttm_plan_kernel_time(comera_ttm_plan_t p, int32_t kernel, double *avg_ms, int32_t *count) {
+    if (!p || kernel < 0 || kernel > 2) return COMERA_ERR_INVALID_ARG;
+    auto &v = p->timing.ev[kernel];
+    double tot = 0;
+    int n = 0;
+    comera_status st = COMERA_OK;
+    for (auto &pr : v) {
+        float ms = 0.f;
+        if (hipEventSynchronize(hipEvent_t(pr.second)) != hipSuccess ||
+            hipEventElapsedTime(&ms, hipEvent_t(pr.first), hipEvent_t(pr.second)) != hipSuccess) {
+            st = COMERA_ERR_HIP;
+        } else {
+            tot += ms;
+            ++n;
+        }
+        hipEventDestroy(hipEvent_t(pr.first));
+        hipEventDestroy(hipEvent_t(pr.second));
+    }
+    v.clear();
+    if (avg_ms) *avg_ms = n ? tot / n : 0.0;
+    if (count) *count = n;
+    return st;
+}
+
+}  // extern "C"

@@ -1,0 +1,178 @@
+"""C-ABI boundary checks that need no GPU.
+
+* the library loads and exports every function include/comera.h declares;
+* the planner: order enumeration (Prop. 4.1 family: 2^d - 1 orders), its
+  flop model against independent closed forms (the dense GEMM count, the
+  per-order sweep counts worked out by hand for the 768 -> 3072 layer at
+  effective rank 24, and the paper's estimate b (N_1 + N_2) r_d multiply-adds
+  for its TT layout, Sec. 4.2 Analysis), mask compaction and zero bonds;
+* host-side argument checks return their status before any launch.
+"""
+import os
+import re
+
+import pytest
+
+from paper_2405_14377_amd import comera as C
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_functions():
+    txt = open(os.path.join(ROOT, "include", "comera.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(comera_\w+)\s*\(", txt)))
+
+
+def test_exports_every_header_function():
+    lib = C.load()
+    names = _header_functions()
+    assert names, "no declarations parsed"
+    assert sorted(C.EXPORTS) == names
+    for nm in names:
+        assert hasattr(lib, nm), nm
+
+
+def test_status_strings():
+    assert C.comera_status_string(C.OK) == "ok"
+    assert "workspace" in C.comera_status_string(C.ERR_WORKSPACE)
+    assert C.comera_status_string(12345) == "unknown status"
+
+
+@pytest.mark.parametrize("d", [1, 2, 3, 4, 5])
+def test_order_count(d):
+    p = C.TTMPlan([2] * d, [3] * d, [1] + [2] * (d - 1) + [1], batch=8)
+    assert p.num_orders == 2 ** d - 1
+    assert p.order_info(0)["kind"] == C.ORDER_DENSE
+    kinds = [p.order_info(i)["kind"] for i in range(1, p.num_orders)]
+    assert kinds == [C.ORDER_SWEEP_RL, C.ORDER_SWEEP_LR] * (2 ** (d - 1) - 1)
+    assert p.chosen == 0
+
+
+def test_order_descriptions_d3():
+    p = C.TTMPlan((8, 8, 12), (12, 8, 8), (1, 8, 8, 1), batch=32)
+    descs = [p.order_info(i)["desc"] for i in range(7)]
+    assert descs == ["dense [0,1,2]", "sweep-rl [0][1,2]", "sweep-lr [0][1,2]", "sweep-rl [0,1][2]",
+                     "sweep-lr [0,1][2]", "sweep-rl [0][1][2]", "sweep-lr [0][1][2]"]
+
+
+def _rank24_masks():
+    act = [1] * 24 + [0] * 6
+    return act + act
+
+
+def test_flops_ffn_up_rank24():
+    """768 -> 3072, n = (8,8,12), m = (16,16,12), ranks 30 with 24 active
+    entries per bond, b = 4096: forward flops per order, counted by hand."""
+    b = 4096
+    p = C.TTMPlan((8, 8, 12), (16, 16, 12), (1, 30, 30, 1), batch=b, mask_active=_rank24_masks())
+    info = {p.order_info(i)["desc"]: p.order_info(i) for i in range(p.num_orders)}
+    # dense: W build = 2*8*8*16*16*24*24 + 2*64*12*256*12*24, GEMM = 2*b*768*3072
+    build = 2 * 8 * 8 * 16 * 16 * 24 * 24 + 2 * 64 * 12 * 256 * 12 * 24
+    assert info["dense [0,1,2]"]["flops_fwd"] == pytest.approx(build + 2 * b * 768 * 3072, rel=1e-12)
+    # singles, right to left: cores 2, 1, 0
+    s2 = 2 * b * 64 * (12 * 1) * (24 * 12)
+    s1 = 2 * b * (8 * 12) * (8 * 24) * (24 * 16)
+    s0 = 2 * b * (1 * 192) * (8 * 24) * (1 * 16)
+    assert info["sweep-rl [0][1][2]"]["flops_fwd"] == pytest.approx(s2 + s1 + s0, rel=1e-12)
+    # rounded values
+    assert info["dense [0,1,2]"]["flops_fwd"] / 1e9 == pytest.approx(19.46, abs=0.01)
+    assert info["sweep-rl [0][1][2]"]["flops_fwd"] / 1e9 == pytest.approx(64.63, abs=0.01)
+    assert info["sweep-lr [0][1][2]"]["flops_fwd"] / 1e9 == pytest.approx(125.6, abs=0.1)
+    assert info["sweep-rl [0][1,2]"]["flops_fwd"] / 1e9 == pytest.approx(33.84, abs=0.01)
+    assert info["sweep-rl [0,1][2]"]["flops_fwd"] / 1e9 == pytest.approx(40.49, abs=0.01)
+    # the dense order is the cheapest forward here
+    assert min(info.values(), key=lambda o: o["flops_fwd"])["desc"] == "dense [0,1,2]"
+
+
+@pytest.mark.parametrize("ns,r", [((4, 4, 4, 2, 2, 4), 5), ((16, 8, 8, 8, 8, 16), 32)])
+def test_flops_paper_tt_layout(ns, r):
+    """Paper's TT layout as TTM with unit modes: the left-to-right sweep over
+    the groups [inputs][outputs] does 2 b (N_1 + N_2) r_d flops in its batch
+    steps (Sec. 4.2 Analysis: about b (N_1 + N_2) r_d multiply-adds)."""
+    d = len(ns) // 2
+    n = list(ns[:d]) + [1] * d
+    m = [1] * d + list(ns[d:])
+    ranks = [1] + [r] * (2 * d - 1) + [1]
+    b = 1000
+    p = C.TTMPlan(n, m, ranks, batch=b)
+    cut_mask = 1 << (d - 1)
+    descs = [p.order_info(i)["desc"] for i in range(p.num_orders)]
+    want = "sweep-lr [" + ",".join(str(k) for k in range(d)) + "][" + ",".join(str(k) for k in range(d, 2 * d)) + "]"
+    i = descs.index(want)
+    N1 = 1
+    for x in ns[:d]:
+        N1 *= x
+    N2 = 1
+    for x in ns[d:]:
+        N2 *= x
+    # group builds are batch free: recompute them at b = 0 and subtract
+    p0 = C.TTMPlan(n, m, ranks, batch=0)
+    build = p0.order_info(i)["flops_fwd"]
+    assert p.order_info(i)["flops_fwd"] - build == pytest.approx(2 * b * (N1 + N2) * r, rel=1e-12)
+    assert cut_mask > 0
+
+
+def test_mask_compaction_and_zero_bond():
+    p = C.TTMPlan((2, 3), (3, 2), (1, 4, 1), batch=4, mask_active=[1, 0, 1, 0])
+    # rank 4 with 2 active: the dense build flops use rank 2
+    assert p.order_info(0)["flops_fwd"] == pytest.approx(2 * 2 * 3 * 3 * 2 * 1 * 2 + 2 * 4 * 6 * 6, rel=1e-12)
+    z = C.TTMPlan((2, 3), (3, 2), (1, 4, 1), batch=4, mask_active=[0, 0, 0, 0])
+    assert z.order_info(0)["kind"] == C.ORDER_ZERO
+    assert z.workspace_bytes == 0
+
+
+def test_plan_errors():
+    st, h = C.comera_ttm_plan(C.ttm_shape((2, 2), (2, 2), (2, 2, 1)), 4, raise_on_error=False)
+    assert st == C.ERR_INVALID_ARG and h is None
+    st, _ = C.comera_ttm_plan(C.ttm_shape((2, 0), (2, 2), (1, 2, 1)), 4, raise_on_error=False)
+    assert st == C.ERR_INVALID_ARG
+    st, _ = C.comera_ttm_plan(C.ttm_shape((2, 2), (2, 2), (1, 2, 1), act=7), 4, raise_on_error=False)
+    assert st == C.ERR_INVALID_ARG
+    st, _ = C.comera_ttm_plan(C.ttm_shape((2, 2), (2, 2), (1, 2, 1)), 4, force_order=3, raise_on_error=False)
+    assert st == C.ERR_INVALID_ARG
+    st, _ = C.comera_ttm_plan(C.ttm_shape((2, 2), (2, 2), (1, 2, 1)), -1, raise_on_error=False)
+    assert st == C.ERR_INVALID_ARG
+
+
+def test_call_errors_before_launch():
+    """Argument errors are reported on the host, before any device work."""
+    lib = C.load()
+    p = C.TTMPlan((2, 3), (3, 2), (1, 2, 1), batch=16)
+    fake = 1 << 40          # never dereferenced: every call below fails its host checks first
+    G = C._ptr_array([fake, fake])
+    # NULL plan
+    assert lib.comera_ttm_forward(None, 4, fake, G, None, fake, fake, 1 << 20, None) == C.ERR_INVALID_ARG
+    # batch above the planned batch
+    assert lib.comera_ttm_forward(p.handle, 17, fake, G, None, fake, fake, 1 << 20, None) == C.ERR_INVALID_ARG
+    # workspace too small / missing
+    assert lib.comera_ttm_forward(p.handle, 4, fake, G, None, fake, fake, 1, None) == C.ERR_WORKSPACE
+    assert lib.comera_ttm_forward(p.handle, 4, fake, G, None, fake, None, 0, None) == C.ERR_WORKSPACE
+    # missing core pointer
+    G1 = C._ptr_array([fake, None])
+    assert lib.comera_ttm_forward(p.handle, 4, fake, G1, None, fake, fake, 1 << 20, None) == C.ERR_INVALID_ARG
+    assert lib.comera_ttm_backward(p.handle, 4, fake, None, G, None, fake, None, fake, 1 << 20,
+                                   None) == C.ERR_INVALID_ARG
+    assert lib.comera_ttm_backward(p.handle, 4, fake, fake, G, None, fake, None, fake, 1, None) == C.ERR_WORKSPACE
+    # empty batch is a no-op that needs nothing
+    assert lib.comera_ttm_forward(p.handle, 0, None, None, None, None, None, 0, None) == C.OK
+
+
+def test_embed_workspace_and_errors():
+    s = C.tt_embed_shape((32, 32, 32), (8, 8, 12), (1, 30, 30, 1))
+    ws = C.comera_tt_embed_workspace_bytes(s, 16384)
+    assert ws > 2 * 16384 * 768 * 4
+    bad = C.tt_embed_shape((32, 32), (8, 8), (2, 3, 1))
+    assert C.comera_tt_embed_workspace_bytes(bad, 10) == 0
+    lib = C.load()
+    fake = 1 << 40
+    G = C._ptr_array([fake, fake, fake])
+    assert lib.comera_tt_embed_forward(bad, fake, 4, G, None, fake, fake, 1 << 30, None, None) == C.ERR_INVALID_ARG
+    assert lib.comera_tt_embed_forward(s, fake, 4, G, None, fake, fake, 1, None, None) == C.ERR_WORKSPACE
+    dG = C._ptr_array([fake, None, fake])
+    assert lib.comera_tt_embed_backward(s, fake, 4, fake, G, None, dG, 1, fake, 1 << 30, None,
+                                        None) == C.ERR_INVALID_ARG
+    # too large for the kernels' LDS staging: refused, not run
+    big = C.tt_embed_shape((4, 4), (4096, 64), (1, 64, 1))
+    assert lib.comera_tt_embed_forward(big, fake, 4, C._ptr_array([fake, fake]), None, fake, fake, 1 << 40, None,
+                                       None) == C.ERR_UNSUPPORTED
