@@ -1,0 +1,340 @@
+#!/usr/bin/env python3
+"""Throughput of the TTM-layer hot path on one MI355X.
+
+A step is one pass of the whole path over one batch: forward Y = X W and
+backward dX = dY W^T plus every dG_k, through the C ABI, for the TTM FFN
+up-projection 768 -> 3072 (n = (8, 8, 12), m = (16, 16, 12), ranks
+(1, 30, 30, 1), Bernoulli(0.8) rank masks, 32 x 128 = 4096 tokens).  The
+plan is made once, outside the timed region.  The line reports the fp32
+run as `value`; the bf16 run (fp32 accumulation), the dense GEMM baseline,
+the roofline of the dominant kernel, the CPU oracle and the other workloads
+are reported beside it.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "TT-layer fwd+bwd tokens/s; % of MFMA or HBM roofline; speedup vs dense GEMM"
+PEAK = {"f32": 157.3e12, "bf16": 2.5e15}
+HBM_PEAK = 8.0e12
+PROFILES = os.path.join(ROOT, "profiles")
+GEMM_SRC = os.path.join(ROOT, "paper_2405_14377_amd", "csrc", "ttm_kernels.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------------ inputs
+def layer_inputs(wid, li, act, gen_seed):
+    """Cores/masks from the seeded workload recipe; activations drawn on the device."""
+    import numpy as np
+    import torch
+    from paper_2405_14377_amd import workloads as wl
+    w = wl.WORKLOADS[wid]
+    sh = w.layers[li]
+    inp = wl.ttm_layer_inputs(wid, li, sh, w.mask)
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(gen_seed)
+    tdt = torch.bfloat16 if act == "bf16" else torch.float32
+    X = torch.randn((w.batch, sh.n_in), generator=g, device=dev, dtype=torch.float32).to(tdt)
+    dY = torch.randn((w.batch, sh.n_out), generator=g, device=dev, dtype=torch.float32).to(tdt)
+    G = [torch.from_numpy(c).to(dev) for c in inp.cores]
+    D = [torch.from_numpy(mk).to(dev) for mk in inp.masks]
+    mask_active = [int(x != 0) for mk in inp.masks for x in mk]
+    return sh, inp, X, dY, G, D, mask_active, w.batch
+
+
+class Layer:
+    def __init__(self, sh, X, dY, G, D, mask_active, b, act):
+        import torch
+        from paper_2405_14377_amd import comera as C
+        self.C = C
+        self.sh, self.X, self.dY, self.G, self.D, self.b, self.act = sh, X, dY, G, D, b, act
+        self.plan = C.TTMPlan(sh.n, sh.m, sh.r, C.BF16 if act == "bf16" else C.F32, batch=b,
+                              mask_active=mask_active)
+        dev = X.device
+        self.ws = torch.empty(self.plan.workspace_bytes, dtype=torch.uint8, device=dev)
+        self.Y = torch.empty((b, sh.n_out), dtype=X.dtype, device=dev)
+        self.dX = torch.empty((b, sh.n_in), dtype=X.dtype, device=dev)
+        self.dG = [torch.empty_like(g) for g in G]
+        self.stream = torch.cuda.current_stream().cuda_stream
+
+    def step(self):
+        C = self.C
+        C.comera_ttm_forward(self.plan.handle, self.b, self.X, self.G, self.D, self.Y, self.ws, self.stream)
+        C.comera_ttm_backward(self.plan.handle, self.b, self.X, self.dY, self.G, self.D, self.dX, self.dG, self.ws,
+                              self.stream)
+
+
+def time_loop(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return e0.elapsed_time(e1) / steps, wall
+
+
+def dense_step_fn(sh, X, dY):
+    """Three plain GEMMs of the same shapes (W materialised): Y = X W,
+    dX = dY W^T, dW = X^T dY; all operands contiguous."""
+    import torch
+    dev = X.device
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    W = (torch.randn((sh.n_in, sh.n_out), generator=g, device=dev) / sh.n_in ** 0.5).to(X.dtype)
+    Wt = W.t().contiguous()
+    Xt = X.t().contiguous()
+
+    def fn():
+        torch.matmul(X, W)
+        torch.matmul(dY, Wt)
+        torch.matmul(Xt, dY)
+    return fn
+
+
+# ------------------------------------------------------------------ roofline
+def source_sha():
+    return hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()[:16]
+
+
+def traffic_from_profile(kernel_tag, act):
+    """HBM bytes per launch from a committed counter summary, if it was taken
+    on the current kernel source; else None."""
+    path = os.path.join(PROFILES, f"traffic_{kernel_tag}_{act}.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    m_sha = re.search(r"source_sha256_16:\s*([0-9a-f]+)", txt)
+    m_b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not m_sha or not m_b or m_sha.group(1) != source_sha():
+        return None
+    return float(m_b.group(1))
+
+
+def kernel_roofline(layer, steps, act):
+    """Mean duration of each batch-product kernel from HIP events recorded by
+    the library on its launch stream, over `steps` instrumented steps."""
+    import torch
+    C = layer.C
+    C.comera_ttm_plan_set_timing(layer.plan.handle, True)
+    for _ in range(steps):
+        layer.step()
+    torch.cuda.synchronize()
+    sh, b = layer.sh, layer.b
+    flops = 2.0 * b * sh.n_in * sh.n_out        # per launch of each of the three products
+    out = {}
+    for tag, kid in (("fwd", C.KERNEL_FWD), ("dx", C.KERNEL_DX), ("dw", C.KERNEL_DW)):
+        ms, cnt = C.comera_ttm_plan_kernel_time(layer.plan.handle, kid)
+        out[tag] = {"avg_ms": ms, "launches": cnt, "tflops": flops / (ms * 1e-3) / 1e12 if ms > 0 else 0.0}
+    C.comera_ttm_plan_set_timing(layer.plan.handle, False)
+    dom = max(out, key=lambda t: out[t]["avg_ms"])
+    ach = out[dom]["tflops"]
+    peak = PEAK[act] / 1e12
+    traffic = traffic_from_profile(dom, act)
+    roof = {"bound": "mfma", "achieved": round(ach, 3), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(ach / peak, 4), "traffic": traffic, "kernel": f"gemm {dom} ({act})",
+            "flops_per_launch": flops, "avg_ms": round(out[dom]["avg_ms"], 5)}
+    return roof, out
+
+
+# ------------------------------------------------------------------ CPU oracle
+def cpu_baseline(min_seconds=10.0):
+    import numpy as np
+    from oracle import ttm as OT
+    from paper_2405_14377_amd import workloads as wl
+    w = wl.WORKLOADS[1]
+    sh = w.layers[0]
+    inp = wl.ttm_layer_inputs(1, 0, sh, w.mask)
+    b = w.batch
+    X = wl.activations(1, b, sh.n_in, 0, "f32")
+    dY = wl.activations(1, b, sh.n_out, 1, "f32")
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 0) for i in threadpool_info()), default=None)
+    except Exception:
+        pass
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        OT.forward_dense(X, inp.cores, inp.masks)
+        OT.backward_dense(X, dY, inp.cores, inp.masks)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds or reps >= 50:
+            break
+    tok_s = reps * b / el
+    return {"value": round(tok_s, 1), "unit": "tokens/s", "cores": threads or len(os.sched_getaffinity(0)),
+            "kind": "oracle",
+            "sample": f"{reps} full steps (4096 tokens each) of the 768->3072 fp32 layer, fp64 dense-W route "
+                      f"(forward_dense + backward_dense), {el:.1f} s"}
+
+
+# ------------------------------------------------------------------ other workloads
+def other_workloads(steps, warmup):
+    import numpy as np
+    import torch
+    from paper_2405_14377_amd import comera as C
+    from paper_2405_14377_amd import workloads as wl
+    res = {}
+    # TTM layer workloads
+    for wid, act in ((0, "f32"), (1, "bf16"), (2, "bf16"), (4, "bf16")):
+        w = wl.WORKLOADS[wid]
+        layers, dense = [], []
+        for li in range(len(w.layers)):
+            sh, inp, X, dY, G, D, ma, b = layer_inputs(wid, li, act, 1000 * wid + li)
+            layers.append(Layer(sh, X, dY, G, D, ma, b, act))
+            dense.append(dense_step_fn(sh, X, dY))
+        k = steps if wid != 4 else max(3, steps // 4)
+        ms, _ = time_loop(lambda: [l.step() for l in layers], k, warmup)
+        dms, _ = time_loop(lambda: [f() for f in dense], k, warmup)
+        fl = sum(6.0 * l.b * l.sh.n_in * l.sh.n_out for l in layers)
+        entry = {"workload": w.name, "dtype": act, "tokens": w.batch, "layers": len(layers),
+                 "ms_per_step": round(ms, 4), "tokens_per_s": round(w.batch / (ms * 1e-3), 1),
+                 "tflops_gemm_equiv": round(fl / (ms * 1e-3) / 1e12, 2),
+                 "dense_ms_per_step": round(dms, 4), "speedup_vs_dense": round(dms / ms, 3)}
+        if wid in (1, 2, 4):
+            roofs = [kernel_roofline(l, max(2, k // 2), act)[1] for l in layers]
+            entry["kernels_ms"] = [{t: round(v["avg_ms"], 4) for t, v in r.items()} for r in roofs]
+        res[f"w{wid}_{act}"] = entry
+        del layers, dense
+        torch.cuda.empty_cache()
+    # embedding
+    w = wl.WORKLOADS[3]
+    dev = torch.device("cuda", 0)
+    cores = [torch.from_numpy(c).to(dev) for c in wl.embed_cores(w)]
+    shape = C.tt_embed_shape(w.v, w.e, w.r)
+    V, E, n = int(np.prod(w.v)), int(np.prod(w.e)), w.n_tokens
+    ws = torch.empty(C.comera_tt_embed_workspace_bytes(shape, n), dtype=torch.uint8, device=dev)
+    Y = torch.empty((n, E), device=dev)
+    dG = [torch.empty_like(c) for c in cores]
+    g = torch.Generator(device=dev)
+    g.manual_seed(3000)
+    dYe = torch.randn((n, E), generator=g, device=dev)
+    table = torch.randn((V, E), generator=g, device=dev) * 0.1
+    table.requires_grad_(True)
+    for dist in ("zipf1.1", "uniform"):
+        ids = torch.from_numpy(wl.token_ids(n, V, dist, wl.seed_of(3, 20))).to(dev)
+        stream = torch.cuda.current_stream().cuda_stream
+
+        def step():
+            C.comera_tt_embed_forward(shape, ids, n, cores, None, Y, ws, None, stream)
+            C.comera_tt_embed_backward(shape, ids, n, dYe, cores, None, dG, 1, ws, None, stream)
+
+        def fstep():
+            C.comera_tt_embed_forward(shape, ids, n, cores, None, Y, ws, None, stream)
+
+        def dense():
+            out = torch.nn.functional.embedding(ids, table)
+            out.backward(dYe)
+            table.grad = None
+
+        ms, _ = time_loop(step, steps, warmup)
+        fms, _ = time_loop(fstep, steps, warmup)
+        dms, _ = time_loop(dense, steps, warmup)
+        byt = 2.0 * n * E * 4            # output write + dY read (algorithmic floor)
+        res[f"w3_{dist}"] = {"workload": w.name, "dtype": "f32", "tokens": n, "ms_per_step": round(ms, 4),
+                             "fwd_ms": round(fms, 4), "tokens_per_s": round(n / (ms * 1e-3), 1),
+                             "gbps_floor_bytes": round(byt / (ms * 1e-3) / 1e9, 1),
+                             "hbm_frac": round(byt / (ms * 1e-3) / HBM_PEAK, 4),
+                             "dense_ms_per_step": round(dms, 4), "speedup_vs_dense": round(dms / ms, 3)}
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
+    ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"], help="dtype of the reported value")
+    args = ap.parse_args()
+    ws = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or ws != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path (the layer shards by tokens with "
+              "one all-reduce of the core gradients; see the design notes). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    from paper_2405_14377_amd import comera as C
+    C.load()
+    runs = {}
+    for act in ("f32", "bf16"):
+        sh, inp, X, dY, G, D, ma, b = layer_inputs(1, 0, act, 1000 + (act == "bf16"))
+        layer = Layer(sh, X, dY, G, D, ma, b, act)
+        log(f"[bench] ttm 768x3072 {act}: warmup {args.warmup}, timing {args.steps} steps")
+        torch.cuda.synchronize()
+        ms, wall = time_loop(layer.step, args.steps, args.warmup)
+        dms, _ = time_loop(dense_step_fn(sh, X, dY), args.steps, args.warmup)
+        roof, kern = kernel_roofline(layer, args.steps, act)
+        runs[act] = {"ms_per_step": ms, "wall_s": wall, "tokens_per_s": b / (ms * 1e-3), "dense_ms": dms,
+                     "speedup_vs_dense": dms / ms, "roofline": roof,
+                     "kernels_ms": {t: round(v["avg_ms"], 5) for t, v in kern.items()}}
+        log(f"[bench]   {ms:.4f} ms/step, dense {dms:.4f} ms, dominant {roof['kernel']} {roof['achieved']} TF/s")
+        del layer
+        torch.cuda.empty_cache()
+    main_run = runs[args.dtype]
+    sh = None
+    out = {
+        "metric": METRIC,
+        "value": round(main_run["tokens_per_s"], 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(main_run["ms_per_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.dtype,
+        "data": "synthetic (seeded N(0,1) activations, cores scaled for unit output variance)",
+        "config": {"workload": "ttm_ffn_up_768x3072_n8x8x12_m16x16x12_r30_mask0.8_b4096",
+                   "global_batch": 4096, "parallelism": "none (1 GPU)"},
+        "roofline": main_run["roofline"],
+        "speedup_vs_dense_gemm": round(main_run["speedup_vs_dense"], 3),
+        "dense_gemm_ms_per_step": round(main_run["dense_ms"], 5),
+        "kernels_ms": main_run["kernels_ms"],
+    }
+    other = "bf16" if args.dtype == "f32" else "f32"
+    r = runs[other]
+    out[f"{other}_run"] = {"value": round(r["tokens_per_s"], 1), "ms_per_step": round(r["ms_per_step"], 5),
+                           "speedup_vs_dense_gemm": round(r["speedup_vs_dense"], 3),
+                           "dense_gemm_ms_per_step": round(r["dense_ms"], 5), "roofline": r["roofline"],
+                           "kernels_ms": r["kernels_ms"]}
+    if not args.no_extra:
+        log("[bench] other workloads")
+        out["other_workloads"] = other_workloads(max(5, args.steps // 2), 3)
+    if not args.no_cpu:
+        log("[bench] CPU oracle baseline")
+        out["cpu_baseline"] = cpu_baseline()
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -13,7 +13,6 @@ using namespace comera;
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr size_t kMaxLds = 64 * 1024;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 inline char *at(void *ws, size_t off) { return reinterpret_cast<char *>(ws) + off; }
 
@@ -48,10 +47,8 @@ bool embed_dims(const comera_tt_embed_shape *s, EmbedDims &dm) {
 
 // Limits of the kernels' LDS staging; larger tables are refused.
 bool embed_supported(const EmbedDims &dm) {
-    size_t rows_lds = sizeof(float) * (size_t(dm.Ep) * dm.R + size_t(dm.R) * dm.Es);
-    size_t dg_lds = sizeof(float) * size_t(dm.R) * dm.Vs * dm.Es;
     double table = double(dm.Vp) * double(dm.Ep) * double(dm.R) * 4.0;
-    return rows_lds <= kMaxLds && dg_lds <= kMaxLds && table <= 8.0e9;
+    return embed_kernels_support(int(dm.Ep), dm.R, dm.Es, dm.E) && embed_gs_fits(dm.R, dm.Vs, dm.Es) && table <= 8.0e9;
 }
 
 void embed_layout(const comera_tt_embed_shape *s, const EmbedDims &dm, int64_t n, EmbedLayout &L) {
@@ -79,15 +76,12 @@ void embed_layout(const comera_tt_embed_shape *s, const EmbedDims &dm, int64_t n
     L.valsA = take(4 * nn);
     L.keysB = take(4 * nn);
     L.valsB = take(4 * nn);
+    const size_t nblk = (nn + 1023) / 1024, nchunk = (nn + kEmbedItem - 1) / kEmbedItem;
+    L.hist = take(4 * 256 * nblk);
     L.meta = take(4 * 16);
-    L.uid = take(4 * (nn + 1));
-    L.ustart = take(4 * (nn + 1));
-    L.useg_item = take(4 * (nn + 1));
-    L.item_u = take(4 * (nn + 1));
-    L.item_beg = take(4 * (nn + 1));
-    L.item_len = take(4 * (nn + 1));
     L.S = take(sizeof(float) * nn * size_t(dm.E));
-    L.Spart = take(sizeof(float) * nn * size_t(dm.E));
+    L.Pfirst = take(sizeof(float) * nchunk * size_t(dm.E));
+    L.Plast = take(sizeof(float) * nchunk * size_t(dm.E));
     L.dA = take(sizeof(float) * size_t(dm.Vp * dm.Ep * dm.R));
     L.dglast_part = take(sizeof(float) * size_t(kEmbedChunks) * size_t(dm.R) * dm.Vs * dm.Es);
     Vl = 1;
@@ -97,15 +91,27 @@ void embed_layout(const comera_tt_embed_shape *s, const EmbedDims &dm, int64_t n
         El *= s->e[k - 1];
         L.e[k] = take(sizeof(float) * size_t(Vl * El * s->r[k]));
     }
+    {
+        size_t adj_max = 0;
+        int64_t Va = dm.Vp, Ea = dm.Ep;
+        for (int k = d - 2; k >= 1; --k) {
+            Va /= s->v[k];
+            Ea /= s->e[k];
+            int64_t M = Va * Ea, N = s->r[k], K = s->v[k] * s->e[k] * s->r[k + 1];
+            int sp = split_for(M, N, K);
+            L.adj_splits[k] = sp;
+            if (sp > 1) adj_max = std::max(adj_max, sizeof(float) * size_t(sp) * size_t(M * N));
+        }
+        L.adj_part = take(adj_max);
+    }
     Vl = 1;
     El = 1;
     for (int k = 0; k < d - 1; ++k) {
-        int64_t XY = Vl * El;
-        int64_t outs = s->r[k] * s->v[k] * s->e[k] * s->r[k + 1];
-        int64_t sp = std::min<int64_t>((XY + 511) / 512, 4096);
-        sp = std::max<int64_t>(1, std::min<int64_t>(sp, std::max<int64_t>(1, (1 << 20) / std::max<int64_t>(outs, 1))));
+        int64_t K = Vl * El;
+        int64_t M = s->r[k], N = s->v[k] * s->e[k] * s->r[k + 1];
+        int64_t sp = split_for(M, N, K);
         L.meet_splits[k] = int(sp);
-        L.gpart[k] = take(sizeof(float) * size_t(sp * outs));
+        L.gpart[k] = take(sizeof(float) * size_t(sp * M * N));
         Vl *= s->v[k];
         El *= s->e[k];
     }
@@ -123,6 +129,7 @@ int build_prefix(const comera_tt_embed_shape *s, const EmbedLayout &L, const flo
     fa.d = d;
     fa.nfold = d - 1;
     fa.compacted = 0;
+    fa.swap = 0;
     for (int k = 0; k < d; ++k) {
         fa.G[k] = G[k];
         fa.D[k] = (D && k < d - 1) ? D[k] : nullptr;
@@ -137,15 +144,14 @@ int build_prefix(const comera_tt_embed_shape *s, const EmbedLayout &L, const flo
     }
     int e = launch_fold(fa, stream);
     if (e) return e;
-    int64_t Vl = 1, El = 1;
-    const float *prev = nullptr;
-    for (int k = 0; k < d - 1; ++k) {
+    P[1] = gc[0];  // r_0 = 1: [v_0][e_0][r_1] is the folded core itself
+    int64_t Vl = s->v[0], El = s->e[0];
+    for (int k = 1; k < d - 1; ++k) {
         float *out = reinterpret_cast<float *>(at(ws, L.p[k + 1]));
-        e = launch_chain(prev, gc[k], out, nullptr, Vl, El, int(s->r[k]), int(s->v[k]), int(s->e[k]),
-                         int(s->r[k + 1]), 1, stream);
+        e = chain_gemm(P[k], gc[k], out, false, Vl, El, int(s->r[k]), int(s->v[k]), int(s->e[k]), int(s->r[k + 1]),
+                       stream);
         if (e) return e;
         P[k + 1] = out;
-        prev = out;
         Vl *= s->v[k];
         El *= s->e[k];
     }
@@ -158,15 +164,11 @@ EmbedWs embed_ws(const EmbedLayout &L, void *ws) {
     w.valsA = reinterpret_cast<uint32_t *>(at(ws, L.valsA));
     w.keysB = reinterpret_cast<uint32_t *>(at(ws, L.keysB));
     w.valsB = reinterpret_cast<uint32_t *>(at(ws, L.valsB));
+    w.hist = reinterpret_cast<int *>(at(ws, L.hist));
     w.meta = reinterpret_cast<int *>(at(ws, L.meta));
-    w.uid = reinterpret_cast<int *>(at(ws, L.uid));
-    w.ustart = reinterpret_cast<int *>(at(ws, L.ustart));
-    w.useg_item = reinterpret_cast<int *>(at(ws, L.useg_item));
-    w.item_u = reinterpret_cast<int *>(at(ws, L.item_u));
-    w.item_beg = reinterpret_cast<int *>(at(ws, L.item_beg));
-    w.item_len = reinterpret_cast<int *>(at(ws, L.item_len));
     w.S = reinterpret_cast<float *>(at(ws, L.S));
-    w.Spart = reinterpret_cast<float *>(at(ws, L.Spart));
+    w.Pfirst = reinterpret_cast<float *>(at(ws, L.Pfirst));
+    w.Plast = reinterpret_cast<float *>(at(ws, L.Plast));
     w.dglast_part = reinterpret_cast<float *>(at(ws, L.dglast_part));
     return w;
 }
@@ -238,9 +240,9 @@ comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int
     EmbedWs w = embed_ws(L, ws);
     e = launch_embed_sort(ids, int(n_tokens), dm.V, w, err_flag, stream);
     if (e) return COMERA_ERR_HIP;
-    e = launch_embed_segsum(dY, int(dm.E), int(n_tokens), w, stream);
+    e = launch_embed_segsum(dY, int(dm.E), int(n_tokens), dm.V, w, stream);
     if (e) return COMERA_ERR_HIP;
-    e = launch_embed_dglast(w, Apre, int(dm.Ep), dm.R, dm.Vs, dm.Es, stream);
+    e = launch_embed_dglast(w, int(n_tokens), dm.V, Apre, int(dm.Ep), dm.R, dm.Vs, dm.Es, stream);
     if (e) return COMERA_ERR_HIP;
     ExpandArgs xa;
     std::memset(&xa, 0, sizeof(xa));
@@ -259,30 +261,37 @@ comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int
     xa.part[d - 1] = w.dglast_part;
     xa.splits[d - 1] = kEmbedChunks;
     if (d > 1) {
-        // E_{d-1} = dA over the prefix table, then environments and meets on
-        // the prefix cores as for a linear layer (row factor = core axis 1)
+        // E_{d-1} = dA over the prefix table (blocked), then right
+        // environments and meets on the prefix cores as for a linear layer
         float *Ek[kMaxCores + 1] = {};
         Ek[d - 1] = reinterpret_cast<float *>(at(ws, L.dA));
-        e = launch_embed_dapre(w, G[d - 1], dm.Vp, int(dm.Ep), dm.R, dm.Vs, dm.Es, Ek[d - 1], stream);
+        e = launch_embed_dapre(w, int(n_tokens), dm.V, G[d - 1], dm.Vp, int(dm.Ep), dm.R, dm.Vs, dm.Es, int(s->v[d - 2]),
+                               int(s->e[d - 2]), Ek[d - 1], stream);
         if (e) return COMERA_ERR_HIP;
         int64_t Vl = dm.Vp, El = dm.Ep;
         for (int k = d - 2; k >= 1; --k) {
             Vl /= s->v[k];
             El /= s->e[k];
             Ek[k] = reinterpret_cast<float *>(at(ws, L.e[k]));
-            e = launch_adjoint(Ek[k + 1], gc[k], Ek[k], Vl, El, int(s->r[k]), int(s->v[k]), int(s->e[k]),
-                               int(s->r[k + 1]), 1, stream);
+            e = adjoint_gemm(Ek[k + 1], gc[k], Ek[k], Vl, El, int(s->r[k]), int(s->v[k]), int(s->e[k]),
+                             int(s->r[k + 1]), int(s->v[k - 1]), int(s->e[k - 1]), L.adj_splits[k],
+                             reinterpret_cast<float *>(at(ws, L.adj_part)), stream);
             if (e) return COMERA_ERR_HIP;
         }
         Vl = 1;
         El = 1;
         for (int k = 0; k < d - 1; ++k) {
-            float *part = reinterpret_cast<float *>(at(ws, L.gpart[k]));
-            e = launch_meet(k == 0 ? nullptr : P[k], Ek[k + 1], part, Vl, El, int(s->r[k]), int(s->v[k]),
-                            int(s->e[k]), int(s->r[k + 1]), 1, L.meet_splits[k], stream);
-            if (e) return COMERA_ERR_HIP;
-            xa.part[k] = part;
-            xa.splits[k] = L.meet_splits[k];
+            if (k == 0) {
+                xa.part[0] = Ek[1];
+                xa.splits[0] = 1;
+            } else {
+                float *part = reinterpret_cast<float *>(at(ws, L.gpart[k]));
+                e = meet_gemm(P[k], Ek[k + 1], part, Vl, El, int(s->r[k]), int(s->v[k]), int(s->e[k]),
+                              int(s->r[k + 1]), L.meet_splits[k], stream);
+                if (e) return COMERA_ERR_HIP;
+                xa.part[k] = part;
+                xa.splits[k] = L.meet_splits[k];
+            }
             Vl *= s->v[k];
             El *= s->e[k];
         }

@@ -13,12 +13,14 @@ namespace {
 inline char *at(void *ws, size_t off) { return reinterpret_cast<char *>(ws) + off; }
 
 struct DenseBuild {
-    float *gc[kMaxCores];
-    float *P[kMaxCores + 1];  // P[k] = product of cores 0..k-1, k = 1..d-1
+    float *gc[kMaxCores];      // folded cores, layout [rho_k][n_k][m_k][rho_{k+1}]
+    float *P[kMaxCores + 1];   // P[k] = product of cores 0..k-1 as [I_<k][J_<k][rho_k], k = 1..d-1
 };
 
 // Steps shared by forward and backward: fold the masks into compacted core
-// copies, then build the left chains P_1..P_{d-1} and W (eq. TTM / Wcompress).
+// copies (eq. Wcompress), then the left chains P_1..P_{d-1} and W (eq. TTM)
+// as one GEMM per core; the last one writes W[N_in, N_out] in the
+// activation dtype.
 int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *const *D, void *ws, void *stream,
                 DenseBuild &bd) {
     const DenseLayout &L = p->dense;
@@ -28,6 +30,7 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
     fa.d = d;
     fa.nfold = d;
     fa.compacted = p->compacted ? 1 : 0;
+    fa.swap = 1;
     for (int k = 0; k < d; ++k) {
         fa.G[k] = G[k];
         fa.D[k] = (D && k < d - 1) ? D[k] : nullptr;
@@ -44,20 +47,22 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
     int e = launch_fold(fa, stream);
     if (e) return e;
     const bool bf = p->s.act == COMERA_BF16;
-    int64_t Il = 1, Jl = 1;
-    const float *prev = nullptr;
-    for (int k = 0; k < d; ++k) {
-        const bool last = k == d - 1;
-        float *out = last ? (bf ? nullptr : reinterpret_cast<float *>(at(ws, L.w)))
-                          : reinterpret_cast<float *>(at(ws, L.p[k + 1]));
-        uint16_t *outb = (last && bf) ? reinterpret_cast<uint16_t *>(at(ws, L.w)) : nullptr;
-        e = launch_chain(prev, bd.gc[k], out, outb, Il, Jl, int(p->rho[k]), int(p->s.m[k]), int(p->s.n[k]),
-                         int(p->rho[k + 1]), 2, stream);
+    if (d == 1) {
+        // W = G_0[0, :, :, 0]^T: a GEMM with a single 1 on the left
+        float *ones = reinterpret_cast<float *>(at(ws, L.ones));
+        e = launch_fill_one(ones, stream);
         if (e) return e;
-        if (!last) {
-            bd.P[k + 1] = out;
-            prev = out;
-        }
+        return chain_gemm(ones, bd.gc[0], at(ws, L.w), bf, 1, 1, 1, int(p->s.n[0]), int(p->s.m[0]), 1, stream);
+    }
+    bd.P[1] = bd.gc[0];  // rho_0 = 1: [n_0][m_0][rho_1] is the folded core itself
+    int64_t Il = p->s.n[0], Jl = p->s.m[0];
+    for (int k = 1; k < d; ++k) {
+        const bool last = k == d - 1;
+        void *out = last ? at(ws, L.w) : at(ws, L.p[k + 1]);
+        e = chain_gemm(bd.P[k], bd.gc[k], out, last && bf, Il, Jl, int(p->rho[k]), int(p->s.n[k]), int(p->s.m[k]),
+                       int(p->rho[k + 1]), stream);
+        if (e) return e;
+        if (!last) bd.P[k + 1] = reinterpret_cast<float *>(out);
         Il *= p->s.n[k];
         Jl *= p->s.m[k];
     }
@@ -121,8 +126,22 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, 
     if (e) return COMERA_ERR_HIP;
     void *ev;
     timing_begin(p, COMERA_KERNEL_FWD, stream, &ev);
-    e = launch_gemm(p->s.act, true, false, p->s.act == COMERA_BF16, X, at(ws, p->dense.w), Y, b, p->N_out, p->N_in,
-                    p->N_in, p->N_out, p->N_out, 1, p->N_in, stream);
+    GemmArgs g;
+    g.dtype = p->s.act;
+    g.a_kc = true;
+    g.b_kc = false;
+    g.out_bf16 = p->s.act == COMERA_BF16;
+    g.A = X;
+    g.B = at(ws, p->dense.w);
+    g.C = Y;
+    g.M = b;
+    g.N = p->N_out;
+    g.K = p->N_in;
+    g.lda = p->N_in;
+    g.ldb = p->N_out;
+    g.rmap = remap_linear(p->N_out);
+    g.cmap = remap_linear(1);
+    e = launch_gemm(g, stream);
     timing_end(p, COMERA_KERNEL_FWD, stream, ev);
     return hip_status(e);
 }
@@ -158,27 +177,70 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
         // dX[b, N_in] = dY[b, N_out] W^T  (eq. back X)
         void *ev;
         timing_begin(p, COMERA_KERNEL_DX, stream, &ev);
-        e = launch_gemm(p->s.act, true, true, p->s.act == COMERA_BF16, dY, at(ws, L.w), dX, b, p->N_in, p->N_out,
-                        p->N_out, p->N_out, p->N_in, 1, p->N_out, stream);
+        GemmArgs g;
+        g.dtype = p->s.act;
+        g.a_kc = true;
+        g.b_kc = true;
+        g.out_bf16 = p->s.act == COMERA_BF16;
+        g.A = dY;
+        g.B = at(ws, L.w);
+        g.C = dX;
+        g.M = b;
+        g.N = p->N_in;
+        g.K = p->N_out;
+        g.lda = p->N_out;
+        g.ldb = p->N_out;
+        g.rmap = remap_linear(p->N_in);
+        g.cmap = remap_linear(1);
+        e = launch_gemm(g, stream);
         timing_end(p, COMERA_KERNEL_DX, stream, ev);
         if (e) return COMERA_ERR_HIP;
     }
     if (!want_dg) return COMERA_OK;
-    // dW[N_in, N_out] = X^T dY, split over tokens, fixed-order split sum
+    // dW = X^T dY (split over tokens, fixed-order split sum), written blocked
+    // as E_d[(I_<, J_<)][(x, y)] with x = i_{d-1}, y = j_{d-1}
+    const int64_t nl = p->s.n[d - 1], ml = p->s.m[d - 1];
+    const int64_t NJl = p->N_out / ml;
     const int splits = int((b + L.dw_kchunk - 1) / L.dw_kchunk);
     float *dw = reinterpret_cast<float *>(at(ws, L.dw));
     float *dwp = splits > 1 ? reinterpret_cast<float *>(at(ws, L.dw_part)) : dw;
-    void *ev;
-    timing_begin(p, COMERA_KERNEL_DW, stream, &ev);
-    e = launch_gemm(p->s.act, false, false, false, X, dY, dwp, p->N_in, p->N_out, b, p->N_in, p->N_out, p->N_out,
-                    splits, L.dw_kchunk, stream);
-    timing_end(p, COMERA_KERNEL_DW, stream, ev);
-    if (e) return COMERA_ERR_HIP;
+    {
+        void *ev;
+        timing_begin(p, COMERA_KERNEL_DW, stream, &ev);
+        GemmArgs g;
+        g.dtype = p->s.act;
+        g.a_kc = false;
+        g.b_kc = false;
+        g.out_bf16 = false;
+        g.A = X;
+        g.B = dY;
+        g.C = dwp;
+        g.M = p->N_in;
+        g.N = p->N_out;
+        g.K = b;
+        g.lda = p->N_in;
+        g.ldb = p->N_out;
+        g.rmap.nd = 2;
+        g.rmap.radix[1] = nl;
+        g.rmap.stride[0] = NJl * nl * ml;
+        g.rmap.stride[1] = ml;
+        g.cmap.nd = 2;
+        g.cmap.radix[1] = ml;
+        g.cmap.stride[0] = nl * ml;
+        g.cmap.stride[1] = 1;
+        g.splits = splits;
+        g.kchunk = L.dw_kchunk;
+        g.split_stride = p->N_in * p->N_out;
+        e = launch_gemm(g, stream);
+        timing_end(p, COMERA_KERNEL_DW, stream, ev);
+        if (e) return COMERA_ERR_HIP;
+    }
     if (splits > 1) {
         e = launch_sum_splits(dwp, dw, p->N_in * p->N_out, splits, stream);
         if (e) return COMERA_ERR_HIP;
     }
-    // right environments E_k = dW contracted with cores k..d-1
+    // right environments E_k = dW contracted with cores k..d-1, each written
+    // blocked for the next step (eq. back Gi, read right to left)
     float *E[kMaxCores + 1];
     E[d] = dw;
     int64_t Il = p->N_in, Jl = p->N_out;
@@ -186,30 +248,37 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
         Il /= p->s.n[k];
         Jl /= p->s.m[k];
         E[k] = reinterpret_cast<float *>(at(ws, L.e[k]));
-        e = launch_adjoint(E[k + 1], bd.gc[k], E[k], Il, Jl, int(p->rho[k]), int(p->s.m[k]), int(p->s.n[k]),
-                           int(p->rho[k + 1]), 2, stream);
+        e = adjoint_gemm(E[k + 1], bd.gc[k], E[k], Il, Jl, int(p->rho[k]), int(p->s.n[k]), int(p->s.m[k]),
+                         int(p->rho[k + 1]), int(p->s.n[k - 1]), int(p->s.m[k - 1]), L.adj_splits[k],
+                         reinterpret_cast<float *>(at(ws, L.adj_part)), stream);
         if (e) return COMERA_ERR_HIP;
     }
-    // core gradients: meet of P_k and E_{k+1} (eq. back Gi), then expand
+    // core gradients: meet of P_k and E_{k+1}, then expand to the full layout
     ExpandArgs xa;
     std::memset(&xa, 0, sizeof(xa));
     xa.d = d;
     xa.compacted = p->compacted ? 1 : 0;
+    xa.swap = 1;
     Il = 1;
     Jl = 1;
     for (int k = 0; k < d; ++k) {
-        float *part = reinterpret_cast<float *>(at(ws, L.gpart[k]));
-        if (dG[k]) {
-            e = launch_meet(k == 0 ? nullptr : bd.P[k], E[k + 1], part, Il, Jl, int(p->rho[k]), int(p->s.m[k]),
-                            int(p->s.n[k]), int(p->rho[k + 1]), 2, L.meet_splits[k], stream);
-            if (e) return COMERA_ERR_HIP;
+        if (k == 0) {
+            xa.part[0] = E[1];    // P_0 = 1: the gradient of core 0 is E_1 itself
+            xa.splits[0] = 1;
+        } else {
+            float *part = reinterpret_cast<float *>(at(ws, L.gpart[k]));
+            if (dG[k]) {
+                e = meet_gemm(bd.P[k], E[k + 1], part, Il, Jl, int(p->rho[k]), int(p->s.n[k]), int(p->s.m[k]),
+                              int(p->rho[k + 1]), L.meet_splits[k], stream);
+                if (e) return COMERA_ERR_HIP;
+            }
+            xa.part[k] = part;
+            xa.splits[k] = L.meet_splits[k];
         }
-        xa.part[k] = part;
         xa.D[k] = (D && k < d - 1) ? D[k] : nullptr;
         xa.dG[k] = dG[k];
         xa.m[k] = int(p->s.m[k]);
         xa.n[k] = int(p->s.n[k]);
-        xa.splits[k] = L.meet_splits[k];
         Il *= p->s.n[k];
         Jl *= p->s.m[k];
     }

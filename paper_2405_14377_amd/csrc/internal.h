@@ -32,6 +32,7 @@ struct DenseLayout {
     size_t gc[kMaxCores];      // compacted, mask-folded cores (fp32)
     size_t p[kMaxCores + 1];   // left chains P_k, k = 1..d-1 (fp32); p[d] unused
     size_t w;                  // W [N_in, N_out] in the activation dtype
+    size_t ones;               // a single 1.0f (left operand of the d = 1 build)
     size_t dw_part;            // split-K partials of dW (fp32)
     size_t dw;                 // dW (fp32)
     size_t e[kMaxCores + 1];   // right environments E_k, k = 1..d-1 (fp32)
@@ -40,6 +41,8 @@ struct DenseLayout {
     int dw_splits;             // split-K count of dW = X^T dY
     int64_t dw_kchunk;         // tokens per split
     int meet_splits[kMaxCores];
+    int adj_splits[kMaxCores];  // split-K of the adjoint step producing E_k
+    size_t adj_part;           // shared scratch for adjoint split partials
 };
 
 }  // namespace comera
@@ -86,6 +89,7 @@ struct FoldArgs {
     int d;
     int nfold;                   // cores folded (grid.y); d for a linear layer
     int compacted;
+    int swap;                    // write [a][n][m][c] instead of [a][m][n][c]
 };
 int launch_fold(const FoldArgs &a, void *stream);
 
@@ -101,27 +105,58 @@ struct ExpandArgs {
     int splits[kMaxCores];
     int d;
     int compacted;
+    int swap;                       // partials are [a][n][m][c]
 };
 int launch_expand(const ExpandArgs &a, void *stream);
 
-// out[(X x), (Y y), c] = sum_a P[X, Y, a] * G[a, .., .., c]; x is core axis
-// `xaxis` (1 or 2), y the other one.  P == nullptr means a single 1.
-// If out_bf16 is set (and c == 1), the result is written as bf16 instead.
-int launch_chain(const float *P, const float *G, float *out, uint16_t *out_bf16, int64_t NX,
-                 int64_t NY, int A, int m, int n, int C, int xaxis, void *stream);
-// out[X, Y, a] = sum_{x, y, c} E[(X x), (Y y), c] * G[a, .., .., c]
-int launch_adjoint(const float *E, const float *G, float *out, int64_t NX, int64_t NY, int A,
-                   int m, int n, int C, int xaxis, void *stream);
-// part[s][a, m, n, c] = sum_{(X, Y) in split s} P[X, Y, a] * E[(X x), (Y y), c]
-int launch_meet(const float *P, const float *E, float *part, int64_t NX, int64_t NY, int A,
-                int m, int n, int C, int xaxis, int splits, void *stream);
+// Output index remap of a GEMM: write idx in mixed radix (digit 0 most
+// significant and unbounded, digit t < nd has radix radix[t] for t >= 1) and
+// return sum_t digit_t * stride[t].
+struct Remap {
+    int nd;
+    int64_t radix[4];
+    int64_t stride[4];
+};
+Remap remap_linear(int64_t stride);
 
-// C = op(A) op(B): see ttm_kernels.hip for the operand conventions.
-int launch_gemm(int dtype, bool a_kcontig, bool b_kcontig, bool out_bf16, const void *A,
-                const void *B, void *C, int64_t M, int64_t N, int64_t K, int64_t lda,
-                int64_t ldb, int64_t ldc, int splits, int64_t kchunk, void *stream);
+struct GemmArgs {
+    int dtype = COMERA_F32;          // operand type
+    bool a_kc = true, b_kc = true;   // k contiguous in memory for A / B
+    bool out_bf16 = false;
+    const void *A = nullptr, *B = nullptr;
+    void *C = nullptr;
+    int64_t M = 0, N = 0, K = 0, lda = 0, ldb = 0;
+    Remap rmap{}, cmap{};
+    int splits = 1;
+    int64_t kchunk = 0;              // k per split (0 = K)
+    int64_t split_stride = 0;        // elements between split outputs
+    int tile = -1;                   // tile shape (-1 = automatic)
+};
+// C[rmap(m) + cmap(n)] = sum_k Aop(m, k) Bop(k, n); see gemm.hip.
+int launch_gemm(const GemmArgs &g, void *stream);
+
+// Core contractions as GEMMs (gemm.hip).  A core copy Gc has layout
+// [A][nx][ny][C]; x runs over the factors of the left index X, y over those
+// of the right index Y.
+//   chain:   out[(I x)][(J y)][c] = sum_a P[I][J][a] Gc[a][x][y][c]   (P == null: a single 1)
+//   adjoint: E[(I, J)][a] = sum_{x y c} En[(I, J)][(x y c)] Gc[a][(x y c)], written
+//            blocked for the next step: [(I', J')][(x', y')][a], I = I' nxp + x',
+//            J = J' nyp + y'
+//   meet:    part[s][a][(x y c)] = sum_{(I, J) in split s} P[(I, J)][a] En[(I, J)][(x y c)]
+int chain_gemm(const float *P, const float *Gc, void *out, bool out_bf16, int64_t NI, int64_t NJ, int A, int nx,
+               int ny, int C, void *stream);
+// With splits > 1 the split partials go to `scratch` (splits * NI * NJ * A
+// floats) and are summed into `out` in a fixed order.
+int adjoint_gemm(const float *En, const float *Gc, float *out, int64_t NI, int64_t NJ, int A, int nx, int ny, int C,
+                 int nxp, int nyp, int splits, float *scratch, void *stream);
+// split count for a GEMM with few output tiles and a long K
+int split_for(int64_t M, int64_t N, int64_t K);
+int meet_gemm(const float *P, const float *En, float *part, int64_t NI, int64_t NJ, int A, int nx, int ny, int C,
+              int splits, void *stream);
+
 int launch_sum_splits(const float *part, float *out, int64_t n, int splits, void *stream);
 int launch_fill_zero(void *ptr, size_t bytes, void *stream);
+int launch_fill_one(float *ptr, void *stream);
 
 // timing hooks (api_ttm.hip)
 void timing_begin(comera_ttm_plan_s *p, int kernel, void *stream, void **ev0);

@@ -163,6 +163,8 @@ void layout_dense(comera_ttm_plan_s *p) {
     }
     L.w = off;
     off = align_up(off + esz * size_t(p->N_in * p->N_out));
+    L.ones = off;
+    off = align_up(off + sizeof(float));
     // dW = X^T dY split over tokens so that the grid holds >= ~512 workgroups
     int64_t tiles = ((p->N_in + 127) / 128) * ((p->N_out + 127) / 128);
     int64_t b = std::max<int64_t>(p->batch, 1);
@@ -186,16 +188,32 @@ void layout_dense(comera_ttm_plan_s *p) {
         L.e[k] = off;
         off = align_up(off + sizeof(float) * size_t(Il * Jl * p->rho[k]));
     }
+    // adjoint k (k = d-1..1): M = I_<k J_<k, N = rho_k, K = n_k m_k rho_{k+1}
+    size_t adj_max = 0;
+    {
+        int64_t Ia = p->N_in, Ja = p->N_out;
+        for (int k = d - 1; k >= 1; --k) {
+            Ia /= p->s.n[k];
+            Ja /= p->s.m[k];
+            int64_t M = Ia * Ja, N = p->rho[k], K = p->s.n[k] * p->s.m[k] * p->rho[k + 1];
+            int sp = split_for(M, N, K);
+            L.adj_splits[k] = sp;
+            if (sp > 1) adj_max = std::max(adj_max, sizeof(float) * size_t(sp) * size_t(M * N));
+        }
+    }
+    L.adj_part = off;
+    off = align_up(off + adj_max);
+    // meet k: M = rho_k, N = n_k m_k rho_{k+1}, K = I_<k J_<k, split over K so
+    // that the grid holds a few hundred workgroups and each split keeps >= 512 k
     Il = 1;
     Jl = 1;
     for (int k = 0; k < d; ++k) {
-        int64_t XY = Il * Jl;
-        int64_t outs = p->rho[k] * p->s.m[k] * p->s.n[k] * p->rho[k + 1];
-        int64_t sp = std::min<int64_t>((XY + 511) / 512, 4096);
-        sp = std::max<int64_t>(1, std::min<int64_t>(sp, std::max<int64_t>(1, (1 << 20) / std::max<int64_t>(outs, 1))));
+        int64_t K = Il * Jl;
+        int64_t M = p->rho[k], N = p->s.n[k] * p->s.m[k] * p->rho[k + 1];
+        int64_t sp = split_for(M, N, K);
         L.meet_splits[k] = int(sp);
         L.gpart[k] = off;
-        off = align_up(off + sizeof(float) * size_t(sp * outs));
+        off = align_up(off + sizeof(float) * size_t(sp * M * N));
         Il *= p->s.n[k];
         Jl *= p->s.m[k];
     }
@@ -303,7 +321,7 @@ comera_status comera_ttm_plan(const comera_ttm_shape *s, int64_t batch, const ui
         }
         p->chosen = best < 0 ? 0 : best;
     }
-    layout_dense(p);
+    if (!p->zero) layout_dense(p);
     p->ws_bytes = p->zero ? 0 : p->dense.total;
     *out = p;
     return COMERA_OK;
