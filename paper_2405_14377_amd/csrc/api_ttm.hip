@@ -19,10 +19,10 @@ struct DenseBuild {
 
 // Steps shared by forward and backward: fold the masks into compacted core
 // copies (eq. Wcompress), then the left chains P_1..P_{d-1} and W (eq. TTM)
-// as one GEMM per core; the last one writes W[N_in, N_out] in the
-// activation dtype.
+// as one GEMM per core; the last one writes W[N_in, N_out] (or, with
+// transpose, W^T[N_out, N_in]) in the activation dtype.
 int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *const *D, void *ws, void *stream,
-                DenseBuild &bd) {
+                DenseBuild &bd, bool transpose) {
     const DenseLayout &L = p->dense;
     const int d = p->d;
     FoldArgs fa;
@@ -52,7 +52,8 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
         float *ones = reinterpret_cast<float *>(at(ws, L.ones));
         e = launch_fill_one(ones, stream);
         if (e) return e;
-        return chain_gemm(ones, bd.gc[0], at(ws, L.w), bf, 1, 1, 1, int(p->s.n[0]), int(p->s.m[0]), 1, stream);
+        return chain_gemm(ones, bd.gc[0], at(ws, L.w), bf, 1, 1, 1, int(p->s.n[0]), int(p->s.m[0]), 1, stream,
+                          transpose);
     }
     bd.P[1] = bd.gc[0];  // rho_0 = 1: [n_0][m_0][rho_1] is the folded core itself
     int64_t Il = p->s.n[0], Jl = p->s.m[0];
@@ -60,7 +61,7 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
         const bool last = k == d - 1;
         void *out = last ? at(ws, L.w) : at(ws, L.p[k + 1]);
         e = chain_gemm(bd.P[k], bd.gc[k], out, last && bf, Il, Jl, int(p->rho[k]), int(p->s.n[k]), int(p->s.m[k]),
-                       int(p->rho[k + 1]), stream);
+                       int(p->rho[k + 1]), stream, last && transpose);
         if (e) return e;
         if (!last) bd.P[k + 1] = reinterpret_cast<float *>(out);
         Il *= p->s.n[k];
@@ -122,14 +123,15 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, 
         if (!G[k]) return COMERA_ERR_INVALID_ARG;
     if (!ws || ws_bytes < p->ws_bytes) return COMERA_ERR_WORKSPACE;
     DenseBuild bd;
-    int e = build_dense(p, G, D, ws, stream, bd);
+    int e = build_dense(p, G, D, ws, stream, bd, true);
     if (e) return COMERA_ERR_HIP;
+    // Y[b, N_out] = X[b, N_in] W (eq. forward), W^T read row by row
     void *ev;
     timing_begin(p, COMERA_KERNEL_FWD, stream, &ev);
     GemmArgs g;
     g.dtype = p->s.act;
     g.a_kc = true;
-    g.b_kc = false;
+    g.b_kc = true;
     g.out_bf16 = p->s.act == COMERA_BF16;
     g.A = X;
     g.B = at(ws, p->dense.w);
@@ -138,7 +140,7 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, 
     g.N = p->N_out;
     g.K = p->N_in;
     g.lda = p->N_in;
-    g.ldb = p->N_out;
+    g.ldb = p->N_in;
     g.rmap = remap_linear(p->N_out);
     g.cmap = remap_linear(1);
     e = launch_gemm(g, stream);
@@ -171,7 +173,7 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
     if (!ws || ws_bytes < p->ws_bytes) return COMERA_ERR_WORKSPACE;
     const DenseLayout &L = p->dense;
     DenseBuild bd;
-    int e = build_dense(p, G, D, ws, stream, bd);
+    int e = build_dense(p, G, D, ws, stream, bd, false);
     if (e) return COMERA_ERR_HIP;
     if (dX) {
         // dX[b, N_in] = dY[b, N_out] W^T  (eq. back X)

@@ -12,9 +12,11 @@
 //
 // Four waves per workgroup; each wave owns a WM x WN block made of 32 x 32
 // MFMA tiles (bf16: v_mfma_f32_32x32x16_bf16, fp32: v_mfma_f32_32x32x2f32).
-// Both operand tiles are staged in LDS as rows of 64 bytes of K (k
-// contiguous), double buffered; operands whose k is strided in memory are
-// transposed in registers on the way in.  Lanes read 16-byte vectors from
+// Both operand tiles are staged in LDS as rows of K (k contiguous), double
+// buffered; operands whose k is strided in memory are transposed in
+// registers on the way in.  A general kernel (64-byte K rows, bounds-checked
+// loads) handles any shape; a fast kernel takes over when all accesses are
+// in bounds by construction.  Lanes read 16-byte vectors from
 // LDS; the k slots fed to successive MFMAs are one fixed permutation of the
 // tile's k range, shared by A and B, so the sum is unchanged.
 #include <hip/hip_runtime.h>
@@ -172,6 +174,32 @@ struct GemmParams {
     int vec_a, vec_b;
 };
 
+// Write the accumulators: 32x32 layout, element v of lane l is row
+// (v/4)*8 + (l/32)*4 + v%4 and column l%32.
+template <bool OUT_BF16, int TM, int TN, int WM, int WN>
+__device__ __forceinline__ void epilogue(const GemmParams &p, const f32x16 (&acc)[TM][TN], const int64_t *roff,
+                                         const int64_t *coff, int wm, int wn, int lr, int lh) {
+    const int64_t zoff = int64_t(blockIdx.z) * p.split_stride;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int cl = wn * WN + j * 32 + lr;
+        const int64_t co = coff[cl];
+        if (co < 0) continue;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int rl = wm * WM + i * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+                const int64_t ro = roff[rl];
+                if (ro < 0) continue;
+                if constexpr (OUT_BF16)
+                    reinterpret_cast<uint16_t *>(p.C)[zoff + ro + co] = f32_to_bf16_rne(acc[i][j][v]);
+                else
+                    reinterpret_cast<float *>(p.C)[zoff + ro + co] = acc[i][j][v];
+            }
+    }
+}
+
 template <typename T, bool A_KC, bool B_KC, bool OUT_BF16, int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
     constexpr int KT = GemmCfg<T>::KT;
@@ -266,24 +294,198 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
         __syncthreads();
     }
 
-    // 32x32 accumulator layout: element v of lane l is row (v/4)*8 + (l/32)*4 + v%4, column l%32
-    const int64_t zoff = int64_t(blockIdx.z) * p.split_stride;
+    epilogue<OUT_BF16, TM, TN, WM, WN>(p, acc, roff, coff, wm, wn, lr, lh);
+}
+
+// ---------------------------------------------------------------- fast path
+// Used when every 16-byte operand access is in bounds by construction: rows
+// aligned to 16 bytes, the K range of each split a multiple of the K tile,
+// and (for operands whose rows are contiguous in memory) the row count a
+// multiple of the 16-byte group.  Each thread computes its byte offsets
+// once; a K step only moves a wave-uniform base pointer, so the loop body is
+// loads, LDS traffic and MFMAs.  Rows past the end are clamped to the last
+// row (their results are never stored).  LDS rows hold 64 or 128 bytes of K
+// plus 16 bytes of padding; 128-byte rows (144-byte pitch) measure free of
+// LDS bank conflicts on gfx950, 64-byte rows are kept for the operands
+// transposed on the way in, where they load faster.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+// KTB = bytes of K per LDS row (64 or 128), FP = KTB + 16 = LDS row pitch
+template <typename T, bool KC, int RT, int KTB>
+struct FastLoader {
+    static constexpr int FP = KTB + 16;
+    static constexpr int E = GemmCfg<T>::E;
+    static constexpr int KT = KTB / int(sizeof(T));
+    static constexpr int CPR = KTB / 16;
+    static constexpr int NKC = (RT * CPR + 255) / 256;
+    static constexpr int KP = KT / 2;
+    static constexpr int MG = sizeof(T) == 2 ? 8 : 4;
+    static constexpr int NMB = (KP * (RT / MG) + 255) / 256;
+    static constexpr int NV = KC ? NKC : 2 * NMB;
+    u32x4 v[NV];
+    uint32_t off[NV];
+
+    __device__ __forceinline__ void setup(int64_t ld, int64_t r0, int64_t R, int tid) {
+        if constexpr (KC) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int64_t co = coff[wn * WN + j * 32 + lr];
-        if (co < 0) continue;
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t ro = roff[wm * WM + i * 32 + (v >> 2) * 8 + lh * 4 + (v & 3)];
-                if (ro < 0) continue;
-                if constexpr (OUT_BF16)
-                    reinterpret_cast<uint16_t *>(p.C)[zoff + ro + co] = f32_to_bf16_rne(acc[i][j][v]);
-                else
-                    reinterpret_cast<float *>(p.C)[zoff + ro + co] = acc[i][j][v];
+            for (int j = 0; j < NKC; ++j) {
+                const int c = min(tid + 256 * j, RT * CPR - 1);
+                const int64_t row = min(r0 + c / CPR, R - 1);
+                off[j] = uint32_t((row * ld + (c % CPR) * E) * int64_t(sizeof(T)));
             }
+        } else {
+#pragma unroll
+            for (int j = 0; j < NMB; ++j) {
+                const int id = min(tid + 256 * j, KP * (RT / MG) - 1);
+                const int kp = id % KP, mg = id / KP;
+                const int64_t row = min(r0 + MG * mg, R - MG);
+                off[2 * j] = uint32_t(((2 * kp) * ld + row) * int64_t(sizeof(T)));
+                off[2 * j + 1] = uint32_t(((2 * kp + 1) * ld + row) * int64_t(sizeof(T)));
+            }
+        }
     }
+    __device__ __forceinline__ void load(const char *__restrict__ base) {
+#pragma unroll
+        for (int j = 0; j < NV; ++j) v[j] = *reinterpret_cast<const u32x4 *>(base + off[j]);
+    }
+    __device__ __forceinline__ void store(char *lds, int tid) const {
+        if constexpr (KC) {
+#pragma unroll
+            for (int j = 0; j < NKC; ++j) {
+                const int c = tid + 256 * j;
+                if (RT * CPR % 256 == 0 || c < RT * CPR)
+                    *reinterpret_cast<u32x4 *>(lds + (c / CPR) * FP + (c % CPR) * 16) = v[j];
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < NMB; ++j) {
+                const int id = tid + 256 * j;
+                if (KP * (RT / MG) % 256 == 0 || id < KP * (RT / MG)) {
+                    const int kp = id % KP, mg = id / KP;
+                    if constexpr (sizeof(T) == 2) {
+                        // element e of the two k rows -> one dword (k even low, k odd high)
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+                            const uint32_t w = __builtin_amdgcn_perm(v[2 * j + 1][e >> 1], v[2 * j][e >> 1], sel);
+                            *reinterpret_cast<uint32_t *>(lds + (8 * mg + e) * FP + kp * 4) = w;
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            u32x2 w;
+                            w[0] = v[2 * j][e];
+                            w[1] = v[2 * j + 1][e];
+                            *reinterpret_cast<u32x2 *>(lds + (4 * mg + e) * FP + kp * 8) = w;
+                        }
+                    }
+                }
+            }
+        }
+    }
+};
+
+template <typename T, bool A_KC, bool B_KC, bool OUT_BF16, int BM, int BN, int WM, int WN, int KTB>
+__global__ __launch_bounds__(256) void gemm_fast_kernel(GemmParams p) {
+    constexpr int FP = KTB + 16;
+    constexpr int KT = KTB / int(sizeof(T));
+    constexpr int WAVES_N = BN / WN;
+    constexpr int TM = WM / 32, TN = WN / 32;
+    static_assert((BM / WM) * (BN / WN) == 4, "four waves per workgroup");
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    char *sA0 = smem;
+    char *sA1 = smem + BM * FP;
+    char *sB0 = smem + 2 * BM * FP;
+    char *sB1 = sB0 + BN * FP;
+    int64_t *roff = reinterpret_cast<int64_t *>(sB1 + BN * FP);
+    int64_t *coff = roff + BM;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int64_t m0 = int64_t(blockIdx.y) * BM, n0 = int64_t(blockIdx.x) * BN;
+    const int64_t kbeg = int64_t(blockIdx.z) * p.kchunk;
+    const int64_t kend = min(p.K, kbeg + p.kchunk);
+    const int ntiles = kend > kbeg ? int((kend - kbeg) / KT) : 0;
+    const char *abase = reinterpret_cast<const char *>(p.A) + (A_KC ? kbeg : kbeg * p.lda) * int64_t(sizeof(T));
+    const char *bbase = reinterpret_cast<const char *>(p.B) + (B_KC ? kbeg : kbeg * p.ldb) * int64_t(sizeof(T));
+    const int64_t astep = (A_KC ? KT : int64_t(KT) * p.lda) * int64_t(sizeof(T));
+    const int64_t bstep = (B_KC ? KT : int64_t(KT) * p.ldb) * int64_t(sizeof(T));
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    FastLoader<T, A_KC, BM, KTB> la;
+    FastLoader<T, B_KC, BN, KTB> lb;
+    la.setup(p.lda, m0, p.M, tid);
+    lb.setup(p.ldb, n0, p.N, tid);
+    if (ntiles > 0) {
+        la.load(abase);
+        lb.load(bbase);
+    }
+    for (int i = tid; i < BM; i += 256) roff[i] = m0 + i < p.M ? remap(p.rmap, m0 + i) : int64_t(-1);
+    for (int i = tid; i < BN; i += 256) coff[i] = n0 + i < p.N ? remap(p.cmap, n0 + i) : int64_t(-1);
+    if (ntiles > 0) {
+        la.store(sA0, tid);
+        lb.store(sB0, tid);
+    }
+    __syncthreads();
+
+    const int lr = lane & 31, lh = lane >> 5;
+    const int aoff = (wm * WM + lr) * FP + lh * 16, boff = (wn * WN + lr) * FP + lh * 16;
+    for (int kt = 0; kt < ntiles; ++kt) {
+        const int cur = kt & 1;
+        const bool more = kt + 1 < ntiles;
+        if (more) {
+            abase += astep;
+            bbase += bstep;
+            la.load(abase);
+            lb.load(bbase);
+        }
+        const char *a_s = (cur ? sA1 : sA0) + aoff;
+        const char *b_s = (cur ? sB1 : sB0) + boff;
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int ks = 0; ks < KT / 16; ++ks) {
+                bf16x8 av[TM], bv[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i) av[i] = *reinterpret_cast<const bf16x8 *>(a_s + i * 32 * FP + ks * 32);
+#pragma unroll
+                for (int j = 0; j < TN; ++j) bv[j] = *reinterpret_cast<const bf16x8 *>(b_s + j * 32 * FP + ks * 32);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int kq = 0; kq < KT / 8; ++kq) {
+                f32x4 av[TM], bv[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i) av[i] = *reinterpret_cast<const f32x4 *>(a_s + i * 32 * FP + kq * 32);
+#pragma unroll
+                for (int j = 0; j < TN; ++j) bv[j] = *reinterpret_cast<const f32x4 *>(b_s + j * 32 * FP + kq * 32);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                    for (int i = 0; i < TM; ++i)
+#pragma unroll
+                        for (int j = 0; j < TN; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][e], bv[j][e], acc[i][j], 0, 0, 0);
+            }
+        }
+        if (more) {
+            la.store(cur ? sA0 : sA1, tid);
+            lb.store(cur ? sB0 : sB1, tid);
+        }
+        __syncthreads();
+    }
+    epilogue<OUT_BF16, TM, TN, WM, WN>(p, acc, roff, coff, wm, wn, lr, lh);
 }
 
 enum TileId { T128x128 = 0, T64x64 = 1, T128x32 = 2, T32x128 = 3, T128x64 = 4, T64x128 = 5 };
@@ -322,6 +524,70 @@ int pick_tile(int64_t M, int64_t N, int splits) {
     return T64x64;
 }
 
+
+// Fast-path tiles: {BM, BN, K bytes per LDS row}.
+enum FastId { F128x128_128 = 0, F128x64_128, F64x128_128, F128x128_64, F256x128_64 };
+
+template <typename T, bool AK, bool BK, bool OB, int BM, int BN, int WM, int WN, int KTB>
+int go_fast(const GemmArgs &g, const GemmParams &p, void *stream) {
+    constexpr size_t lds = size_t(2) * (BM + BN) * (KTB + 16) + size_t(BM + BN) * sizeof(int64_t);
+    auto kern = gemm_fast_kernel<T, AK, BK, OB, BM, BN, WM, WN, KTB>;
+    // above the default 64 KB of dynamic LDS: raise the limit once per kernel
+    static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
+    if (set) return set;
+    dim3 grid(unsigned((g.N + BN - 1) / BN), unsigned((g.M + BM - 1) / BM), unsigned(g.splits));
+    hipLaunchKernelGGL(kern, grid, dim3(256), lds, hipStream_t(stream), p);
+    return int(hipGetLastError());
+}
+
+template <typename T, bool AK, bool BK, bool OB>
+int launch_fast(const GemmArgs &g, const GemmParams &p, int id, void *stream) {
+    switch (id) {
+        case F128x128_128: return go_fast<T, AK, BK, OB, 128, 128, 64, 64, 128>(g, p, stream);
+        case F128x64_128: return go_fast<T, AK, BK, OB, 128, 64, 64, 32, 128>(g, p, stream);
+        case F64x128_128: return go_fast<T, AK, BK, OB, 64, 128, 32, 64, 128>(g, p, stream);
+        case F128x128_64: return go_fast<T, AK, BK, OB, 128, 128, 64, 64, 64>(g, p, stream);
+        case F256x128_64: return go_fast<T, AK, BK, OB, 256, 128, 128, 64, 64>(g, p, stream);
+    }
+    return int(hipErrorInvalidValue);
+}
+
+// Tile for the fast path (measured on the layer shapes): operands that are
+// both K-contiguous take 128-byte K rows; products with a transposed operand
+// take 64-byte rows.  Returns -1 when the product is too small to fill the
+// chip with these tiles (the general kernel's smaller tiles do better).
+int pick_fast(const GemmArgs &g, int splits) {
+    const int64_t t128 = ceil_div(g.M, 128) * ceil_div(g.N, 128) * splits;
+    if (g.a_kc && g.b_kc) {
+        // fp32 tiles of 128 x 128 fit three workgroups per CU with 64-byte rows
+        if (g.dtype == COMERA_F32 && t128 >= 240) return F128x128_64;
+        if (t128 >= 512) return F128x128_128;
+        const int64_t t64 = ceil_div(g.M, g.M >= g.N ? 128 : 64) * ceil_div(g.N, g.M >= g.N ? 64 : 128) * splits;
+        if (t64 >= 240) return g.M >= g.N ? F128x64_128 : F64x128_128;
+        return -1;
+    }
+    if (!g.a_kc && !g.b_kc) {
+        if (ceil_div(g.M, 256) * ceil_div(g.N, 128) * splits >= 480) return F256x128_64;
+        return t128 >= 240 ? F128x128_64 : -1;
+    }
+    return t128 >= 240 ? F128x128_64 : -1;
+}
+
+// Whether every 16-byte access of the fast kernel stays inside the operand:
+// 16-byte aligned rows, whole K tiles in every split, row groups that divide
+// the row count of transposed operands, and byte offsets within 32 bits.
+bool fast_ok(const GemmArgs &g, int64_t kchunk, int ktb) {
+    const int64_t sz = g.dtype == COMERA_BF16 ? 2 : 4;
+    const int64_t kt = ktb / sz;
+    if (g.K % kt || kchunk % kt) return false;
+    auto op_ok = [&](const void *ptr, int64_t ld, bool kc, int64_t R) {
+        if (reinterpret_cast<uintptr_t>(ptr) % 16 || (ld * sz) % 16) return false;
+        if (kc) return R * ld * sz < (int64_t(1) << 32);
+        return R % (16 / sz) == 0 && (kt * ld + R) * sz < (int64_t(1) << 32);
+    };
+    return op_ok(g.A, g.lda, g.a_kc, g.M) && op_ok(g.B, g.ldb, g.b_kc, g.N);
+}
 }  // namespace
 
 Remap remap_linear(int64_t stride) {
@@ -354,9 +620,22 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     p.vec_b = aligned(g.B, g.ldb);
     GemmArgs gg = g;
     if (gg.splits < 1) gg.splits = 1;
+    // fast path: K chunk rounded up to whole K tiles (later splits may get
+    // fewer tiles or none; an empty split writes zeros)
+    int fast = g.fast >= 0 ? g.fast : (g.fast == -1 && g.tile < 0 ? pick_fast(gg, gg.splits) : -1);
+    GemmParams pf = p;
+    if (fast >= 0) {
+        const int ktb = (fast == F128x128_64 || fast == F256x128_64) ? 64 : 128;
+        const int64_t kt = ktb / (g.dtype == COMERA_BF16 ? 2 : 4);
+        pf.kchunk = ceil_div(p.kchunk, kt) * kt;
+        if (!fast_ok(gg, pf.kchunk, ktb)) fast = -1;
+    }
     const int tile = g.tile >= 0 ? g.tile : pick_tile(g.M, g.N, gg.splits);
-#define COMERA_GEMM_CASE(T, AK, BK, OB) \
-    if (g.a_kc == AK && g.b_kc == BK && g.out_bf16 == OB) return launch_t<T, AK, BK, OB>(gg, p, tile, stream);
+#define COMERA_GEMM_CASE(T, AK, BK, OB)                                                    \
+    if (g.a_kc == AK && g.b_kc == BK && g.out_bf16 == OB) {                                \
+        if (fast >= 0) return launch_fast<T, AK, BK, OB>(gg, pf, fast, stream);           \
+        return launch_t<T, AK, BK, OB>(gg, p, tile, stream);                               \
+    }
     if (g.dtype == COMERA_BF16) {
         COMERA_GEMM_CASE(uint16_t, true, false, true)
         COMERA_GEMM_CASE(uint16_t, true, true, true)
@@ -372,7 +651,8 @@ int launch_gemm(const GemmArgs &g, void *stream) {
 }
 
 int chain_gemm(const float *P, const float *Gc, void *out, bool out_bf16, int64_t NI, int64_t NJ, int A, int nx,
-               int ny, int C, void *stream) {
+               int ny, int C, void *stream, bool transpose) {
+    if (transpose && C != 1) return int(hipErrorInvalidValue);
     GemmArgs g;
     g.dtype = COMERA_F32;
     g.a_kc = true;
@@ -388,14 +668,23 @@ int chain_gemm(const float *P, const float *Gc, void *out, bool out_bf16, int64_
     g.ldb = g.N;
     g.rmap.nd = 2;
     g.rmap.radix[1] = NJ;
-    g.rmap.stride[0] = int64_t(nx) * NJ * ny * C;
-    g.rmap.stride[1] = int64_t(ny) * C;
     g.cmap.nd = 3;
     g.cmap.radix[1] = ny;
     g.cmap.radix[2] = C;
-    g.cmap.stride[0] = NJ * ny * C;
-    g.cmap.stride[1] = C;
-    g.cmap.stride[2] = 1;
+    if (!transpose) {
+        g.rmap.stride[0] = int64_t(nx) * NJ * ny * C;
+        g.rmap.stride[1] = int64_t(ny) * C;
+        g.cmap.stride[0] = NJ * ny * C;
+        g.cmap.stride[1] = C;
+        g.cmap.stride[2] = 1;
+    } else {
+        const int64_t rows_in = NI * nx;  // length of one (J y) row of the output
+        g.rmap.stride[0] = nx;
+        g.rmap.stride[1] = int64_t(ny) * rows_in;
+        g.cmap.stride[0] = 1;
+        g.cmap.stride[1] = rows_in;
+        g.cmap.stride[2] = 0;
+    }
     return launch_gemm(g, stream);
 }
 

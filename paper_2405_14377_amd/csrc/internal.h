@@ -130,7 +130,8 @@ struct GemmArgs {
     int splits = 1;
     int64_t kchunk = 0;              // k per split (0 = K)
     int64_t split_stride = 0;        // elements between split outputs
-    int tile = -1;                   // tile shape (-1 = automatic)
+    int tile = -1;                   // general-kernel tile (-1 = automatic)
+    int fast = -1;                   // fast-kernel tile (-1 = automatic, -2 = never)
 };
 // C[rmap(m) + cmap(n)] = sum_k Aop(m, k) Bop(k, n); see gemm.hip.
 int launch_gemm(const GemmArgs &g, void *stream);
@@ -143,8 +144,9 @@ int launch_gemm(const GemmArgs &g, void *stream);
 //            blocked for the next step: [(I', J')][(x', y')][a], I = I' nxp + x',
 //            J = J' nyp + y'
 //   meet:    part[s][a][(x y c)] = sum_{(I, J) in split s} P[(I, J)][a] En[(I, J)][(x y c)]
+//   chain with transpose (last core, C == 1): out[(J y)][(I x)] instead
 int chain_gemm(const float *P, const float *Gc, void *out, bool out_bf16, int64_t NI, int64_t NJ, int A, int nx,
-               int ny, int C, void *stream);
+               int ny, int C, void *stream, bool transpose = false);
 // With splits > 1 the split partials go to `scratch` (splits * NI * NJ * A
 // floats) and are summed into `out` in a fixed order.
 int adjoint_gemm(const float *En, const float *Gc, float *out, int64_t NI, int64_t NJ, int A, int nx, int ny, int C,
