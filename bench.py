@@ -29,7 +29,8 @@ METRIC = "TT-layer fwd+bwd tokens/s; % of MFMA or HBM roofline; speedup vs dense
 PEAK = {"f32": 157.3e12, "bf16": 2.5e15}
 HBM_PEAK = 8.0e12
 PROFILES = os.path.join(ROOT, "profiles")
-GEMM_SRC = os.path.join(ROOT, "paper_2405_14377_amd", "csrc", "ttm_kernels.hip")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2405_14377_amd", "csrc", f) for f in ("gemm.hip", "api_ttm.hip")]
+COPY_BYTES = 1 << 28          # plain device copy used to scale the HBM byte counters
 
 
 def log(msg):
@@ -116,7 +117,10 @@ def dense_step_fn(sh, X, dY):
 
 # ------------------------------------------------------------------ roofline
 def source_sha():
-    return hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in KERNEL_SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def traffic_from_profile(kernel_tag, act):
@@ -159,6 +163,76 @@ def kernel_roofline(layer, steps, act):
     return roof, out
 
 
+# ------------------------------------------------------------------ profile summaries (CPU only)
+def _read_csv(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def _find(dirpath, suffix):
+    for root, _, files in os.walk(dirpath):
+        for fn in files:
+            if fn.endswith(suffix):
+                return os.path.join(root, fn)
+    raise FileNotFoundError(f"no *{suffix} under {dirpath}")
+
+
+def kernel_stats_summary(prof_dir, out_path, command, top=25):
+    """Short text table of a rocprofv3 --kernel-trace --stats run."""
+    rows = _read_csv(_find(prof_dir, "kernel_stats.csv"))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    lines = ["# rocprofv3 kernel statistics", "", "command:", "", "```", command, "```", "",
+             "| calls | avg us | total ms | % | kernel |", "|---:|---:|---:|---:|---|"]
+    for r in rows[:top]:
+        name = r["Name"].replace("comera::(anonymous namespace)::", "").replace("|", "/")
+        if len(name) > 120:
+            name = name[:117] + "..."
+        lines.append(f"| {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
+                     f"{float(r['Percentage']):.1f} | `{name}` |")
+    open(out_path, "w").write("\n".join(lines) + "\n")
+
+
+def traffic_summary(fetch_dir, write_dir, kernel, grid, tag, act, out_path, commands):
+    """HBM bytes per launch of one kernel from two counter passes (FETCH_SIZE,
+    WRITE_SIZE, KiB per dispatch), each scaled by what the same counter reads
+    for a plain device copy of COPY_BYTES."""
+    def per_dispatch(d, counter):
+        rows = [r for r in _read_csv(_find(d, "counter_collection.csv")) if r["Counter_Name"] == counter]
+        k = [float(r["Counter_Value"]) for r in rows
+             if kernel in r["Kernel_Name"] and (grid is None or int(r["Grid_Size"]) == grid)]
+        c = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        if not k or not c:
+            raise RuntimeError(f"{counter}: {len(k)} kernel dispatches, {len(c)} copy dispatches")
+        return sum(k) / len(k), len(k), max(c)
+    kf, nf, cf = per_dispatch(fetch_dir, "FETCH_SIZE")
+    kw, nw, cw = per_dispatch(write_dir, "WRITE_SIZE")
+    sf = COPY_BYTES / 1024.0 / cf
+    sw = COPY_BYTES / 1024.0 / cw
+    hbm = kf * 1024 * sf + kw * 1024 * sw
+    lines = ["# HBM traffic per launch", "",
+             f"kernel: `{kernel}`" + (f" (grid size {grid} work-items)" if grid else ""),
+             f"tag: {tag} ({act})",
+             f"source_sha256_16: {source_sha()}",
+             f"fetch_kib_per_dispatch: {kf:.1f} (mean of {nf})",
+             f"write_kib_per_dispatch: {kw:.1f} (mean of {nw})",
+             f"copy_{COPY_BYTES}_bytes_fetch_kib: {cf:.1f} -> scale {sf:.4f}",
+             f"copy_{COPY_BYTES}_bytes_write_kib: {cw:.1f} -> scale {sw:.4f}",
+             f"hbm_bytes_per_launch: {hbm:.6e}", "", "commands:", "", "```"] + commands + ["```"]
+    open(out_path, "w").write("\n".join(lines) + "\n")
+    return hbm
+
+
+def calib_copy():
+    """A plain device-to-device copy of COPY_BYTES (the scale for the byte counters)."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+
+
 # ------------------------------------------------------------------ CPU oracle
 def cpu_baseline(min_seconds=10.0):
     import numpy as np
@@ -182,7 +256,7 @@ def cpu_baseline(min_seconds=10.0):
         OT.backward_dense(X, dY, inp.cores, inp.masks)
         reps += 1
         el = time.perf_counter() - t0
-        if el >= min_seconds or reps >= 50:
+        if el >= min_seconds or reps >= 1000:
             break
     tok_s = reps * b / el
     return {"value": round(tok_s, 1), "unit": "tokens/s", "cores": threads or len(os.sched_getaffinity(0)),
@@ -270,7 +344,22 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"], help="dtype of the reported value")
+    ap.add_argument("--calib-copy", action="store_true", help="also run a plain device copy of known size")
+    ap.add_argument("--stats-summary", nargs=3, metavar=("PROF_DIR", "OUT_MD", "COMMAND"),
+                    help="write a kernel-statistics table from a rocprofv3 run (no GPU)")
+    ap.add_argument("--traffic-summary", nargs=5, metavar=("FETCH_DIR", "WRITE_DIR", "KERNEL", "GRID", "TAG"),
+                    help="write profiles/traffic_<TAG>_<dtype>.md from two counter runs (no GPU); GRID 0 = any")
+    ap.add_argument("--commands", nargs="*", default=[], help="commands recorded in a summary")
     args = ap.parse_args()
+    if args.stats_summary:
+        kernel_stats_summary(*args.stats_summary)
+        return
+    if args.traffic_summary:
+        fd, wd, kern, grid, tag = args.traffic_summary
+        hbm = traffic_summary(fd, wd, kern, int(grid) or None, tag, args.dtype,
+                              os.path.join(PROFILES, f"traffic_{tag}_{args.dtype}.md"), args.commands)
+        print(f"hbm bytes per launch: {hbm:.4e}")
+        return
     ws = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or ws != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (the layer shards by tokens with "
@@ -325,6 +414,8 @@ def main():
                            "speedup_vs_dense_gemm": round(r["speedup_vs_dense"], 3),
                            "dense_gemm_ms_per_step": round(r["dense_ms"], 5), "roofline": r["roofline"],
                            "kernels_ms": r["kernels_ms"]}
+    if args.calib_copy:
+        calib_copy()
     if not args.no_extra:
         log("[bench] other workloads")
         out["other_workloads"] = other_workloads(max(5, args.steps // 2), 3)

@@ -172,14 +172,44 @@ struct GemmParams {
     int64_t M, N, K, lda, ldb, kchunk, split_stride;
     Remap rmap, cmap;
     int vec_a, vec_b;
+    int gw;   // tile-order group width in column tiles (see tile_of)
 };
+
+// Workgroup -> (split, row tile, column tile).  The dispatcher deals
+// consecutive workgroup ids round-robin to the 8 XCDs, each with its own L2.
+// The linear id is first turned into an XCD-major order (each XCD gets one
+// contiguous range), and that order walks the tiles in groups of gw column
+// tiles, row by row inside a group, so one XCD covers a compact block of the
+// output and fetches each operand row into its L2 about once.
+struct TileIdx {
+    int64_t z, row, col;
+};
+__device__ __forceinline__ TileIdx tile_of(const GemmParams &p) {
+    constexpr uint32_t kXcds = 8;
+    const uint32_t nx = gridDim.x, ny = gridDim.y;
+    const uint32_t per = nx * ny;
+    const uint32_t total = per * gridDim.z;
+    const uint32_t lin = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
+    const uint32_t x = lin % kXcds, i = lin / kXcds;
+    const uint32_t q = total / kXcds, rem = total % kXcds;
+    const uint32_t id = x * q + min(x, rem) + i;
+    TileIdx t;
+    t.z = id / per;
+    const uint32_t tt = id % per;
+    const uint32_t gw = p.gw > 0 ? min(uint32_t(p.gw), nx) : nx;
+    const uint32_t g = tt / (gw * ny), r = tt % (gw * ny);
+    const uint32_t w = min(gw, nx - g * gw);
+    t.row = r / w;
+    t.col = g * gw + r % w;
+    return t;
+}
 
 // Write the accumulators: 32x32 layout, element v of lane l is row
 // (v/4)*8 + (l/32)*4 + v%4 and column l%32.
 template <bool OUT_BF16, int TM, int TN, int WM, int WN>
 __device__ __forceinline__ void epilogue(const GemmParams &p, const f32x16 (&acc)[TM][TN], const int64_t *roff,
                                          const int64_t *coff, int wm, int wn, int lr, int lh) {
-    const int64_t zoff = int64_t(blockIdx.z) * p.split_stride;
+    const int64_t zoff = tile_of(p).z * p.split_stride;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int cl = wn * WN + j * 32 + lr;
@@ -215,8 +245,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
     const T *__restrict__ B = reinterpret_cast<const T *>(p.B);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-    const int64_t m0 = int64_t(blockIdx.y) * BM, n0 = int64_t(blockIdx.x) * BN;
-    const int64_t kbeg = int64_t(blockIdx.z) * p.kchunk;
+    const TileIdx ti = tile_of(p);
+    const int64_t m0 = ti.row * BM, n0 = ti.col * BN;
+    const int64_t kbeg = ti.z * p.kchunk;
     const int64_t kend = min(p.K, kbeg + p.kchunk);
     const int ntiles = kend > kbeg ? int((kend - kbeg + KT - 1) / KT) : 0;
 
@@ -402,8 +433,9 @@ __global__ __launch_bounds__(256) void gemm_fast_kernel(GemmParams p) {
     int64_t *coff = roff + BM;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-    const int64_t m0 = int64_t(blockIdx.y) * BM, n0 = int64_t(blockIdx.x) * BN;
-    const int64_t kbeg = int64_t(blockIdx.z) * p.kchunk;
+    const TileIdx ti = tile_of(p);
+    const int64_t m0 = ti.row * BM, n0 = ti.col * BN;
+    const int64_t kbeg = ti.z * p.kchunk;
     const int64_t kend = min(p.K, kbeg + p.kchunk);
     const int ntiles = kend > kbeg ? int((kend - kbeg) / KT) : 0;
     const char *abase = reinterpret_cast<const char *>(p.A) + (A_KC ? kbeg : kbeg * p.lda) * int64_t(sizeof(T));
@@ -490,11 +522,34 @@ __global__ __launch_bounds__(256) void gemm_fast_kernel(GemmParams p) {
 
 enum TileId { T128x128 = 0, T64x64 = 1, T128x32 = 2, T32x128 = 3, T128x64 = 4, T64x128 = 5 };
 
+// Group width for tile_of: split the XCDs that share one split's tiles
+// into p row blocks x q column blocks, choosing the split that fetches the
+// fewest operand bytes (A is fetched once per column block, B once per row
+// block).
+int choose_gw(const GemmArgs &g, int bm, int bn, int splits) {
+    const int64_t nx = (g.N + bn - 1) / bn, ny = (g.M + bm - 1) / bm;
+    const int per_slice = splits >= 8 ? 1 : 8 / splits;
+    int best_q = 1;
+    double best = -1.0;
+    for (int q = 1; q <= per_slice; q *= 2) {
+        const int pr = per_slice / q;
+        if (q > nx || pr > ny) continue;
+        const double cost = double(q) * double(g.M) + double(pr) * double(g.N);
+        if (best < 0 || cost < best) {
+            best = cost;
+            best_q = q;
+        }
+    }
+    return int((nx + best_q - 1) / best_q);
+}
+
 template <typename T, bool AK, bool BK, bool OB>
 int launch_t(const GemmArgs &g, const GemmParams &p, int tile, void *stream) {
     auto go = [&](auto kern, int bm, int bn) {
         dim3 grid(unsigned((g.N + bn - 1) / bn), unsigned((g.M + bm - 1) / bm), unsigned(g.splits));
-        hipLaunchKernelGGL(kern, grid, dim3(256), 0, hipStream_t(stream), p);
+        GemmParams q = p;
+        q.gw = choose_gw(g, bm, bn, g.splits);
+        hipLaunchKernelGGL(kern, grid, dim3(256), 0, hipStream_t(stream), q);
         return int(hipGetLastError());
     };
     switch (tile) {
@@ -537,7 +592,9 @@ int go_fast(const GemmArgs &g, const GemmParams &p, void *stream) {
                                                    hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
     if (set) return set;
     dim3 grid(unsigned((g.N + BN - 1) / BN), unsigned((g.M + BM - 1) / BM), unsigned(g.splits));
-    hipLaunchKernelGGL(kern, grid, dim3(256), lds, hipStream_t(stream), p);
+    GemmParams q = p;
+    q.gw = choose_gw(g, BM, BN, g.splits);
+    hipLaunchKernelGGL(kern, grid, dim3(256), lds, hipStream_t(stream), q);
     return int(hipGetLastError());
 }
 
@@ -618,6 +675,7 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     };
     p.vec_a = aligned(g.A, g.lda);
     p.vec_b = aligned(g.B, g.ldb);
+    p.gw = 0;
     GemmArgs gg = g;
     if (gg.splits < 1) gg.splits = 1;
     // fast path: K chunk rounded up to whole K tiles (later splits may get
