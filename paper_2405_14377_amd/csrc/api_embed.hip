@@ -22,6 +22,7 @@ bool embed_dims(const comera_tt_embed_shape *s, EmbedDims &dm) {
     double V = 1, E = 1;
     for (int k = 0; k < s->d; ++k) {
         if (s->v[k] < 1 || s->e[k] < 1 || s->r[k] < 1 || s->r[k + 1] < 1 || s->r[k] > 4096) return false;
+        if (double(s->r[k]) * double(s->v[k]) * double(s->e[k]) * double(s->r[k + 1]) > 2147483647.0) return false;
         V *= double(s->v[k]);
         E *= double(s->e[k]);
     }

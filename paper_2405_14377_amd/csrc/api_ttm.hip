@@ -60,6 +60,22 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
     for (int k = 1; k < d; ++k) {
         const bool last = k == d - 1;
         void *out = last ? at(ws, L.w) : at(ws, L.p[k + 1]);
+        int qb = 0;
+        if (last && wbuild_tiles(Il, Jl, int(p->rho[k]), int(p->s.n[k]), int(p->s.m[k]), transpose, qb)) {
+            WBuildArgs wa;
+            wa.P = bd.P[k];
+            wa.G = bd.gc[k];
+            wa.out = out;
+            wa.NI = Il;
+            wa.NJ = Jl;
+            wa.A = int(p->rho[k]);
+            wa.nx = int(p->s.n[k]);
+            wa.ny = int(p->s.m[k]);
+            wa.transpose = transpose ? 1 : 0;
+            wa.out_bf16 = bf ? 1 : 0;
+            wa.QB = qb;
+            return launch_wbuild(wa, stream);
+        }
         e = chain_gemm(bd.P[k], bd.gc[k], out, last && bf, Il, Jl, int(p->rho[k]), int(p->s.n[k]), int(p->s.m[k]),
                        int(p->rho[k + 1]), stream, last && transpose);
         if (e) return e;
@@ -71,6 +87,77 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
 }
 
 comera_status hip_status(int e) { return e ? COMERA_ERR_HIP : COMERA_OK; }
+
+// Core gradients from the split partials of dW (eq. back Gi): one fused
+// projection step per core k = d-1 .. 1 (right environment E_k and the meet
+// with P_k), then the expand kernel sums the meet partials (and, for core 0,
+// the slices of E_1) in a fixed order, unswaps, applies the masks and writes
+// zeros on inactive slices.
+comera_status project_dense(const comera_ttm_plan_s *p, const DenseBuild &bd, const float *dw_part, int splits,
+                            const float *const *D, float *const *dG, void *ws, void *stream) {
+    const DenseLayout &L = p->dense;
+    const int d = p->d;
+    const float *En = dw_part;
+    int nin = splits;
+    int64_t in_stride = p->N_in * p->N_out;
+    int64_t Il = p->N_in, Jl = p->N_out;
+    ExpandArgs xa;
+    std::memset(&xa, 0, sizeof(xa));
+    for (int k = d - 1; k >= 1; --k) {
+        Il /= p->s.n[k];
+        Jl /= p->s.m[k];
+        const int A = int(p->rho[k]);
+        const int64_t rows = Il * Jl, cols = p->s.n[k] * p->s.m[k] * p->rho[k + 1];
+        ProjArgs pa;
+        pa.En = En;
+        pa.nin = nin;
+        pa.in_stride = in_stride;
+        pa.Gc = bd.gc[k];
+        pa.P = dG[k] ? bd.P[k] : nullptr;
+        pa.Eout = reinterpret_cast<float *>(at(ws, L.e[k]));
+        pa.out_stride = rows * A;
+        // E_k blocked for step k-1: [(I', J')][(x', y')][a], I = I' n_{k-1} + x',
+        // J = J' m_{k-1} + y'
+        const int64_t nxp = p->s.n[k - 1], nyp = p->s.m[k - 1], NJp = Jl / nyp;
+        pa.rmap.nd = 4;
+        pa.rmap.radix[1] = nxp;
+        pa.rmap.radix[2] = NJp;
+        pa.rmap.radix[3] = nyp;
+        pa.rmap.stride[0] = NJp * nxp * nyp * A;
+        pa.rmap.stride[1] = nyp * A;
+        pa.rmap.stride[2] = nxp * nyp * A;
+        pa.rmap.stride[3] = A;
+        pa.part = reinterpret_cast<float *>(at(ws, L.gpart[k]));
+        pa.rows = rows;
+        pa.cols = cols;
+        pa.A = A;
+        pa.RT = L.proj_rt[k];
+        pa.CT = L.proj_ct[k];
+        if (int e = launch_proj(pa, stream)) return hip_status(e);
+        xa.part[k] = pa.part;
+        xa.splits[k] = L.meet_splits[k];
+        En = pa.Eout;
+        nin = L.e_slices[k];
+        in_stride = pa.out_stride;
+    }
+    xa.part[0] = En;     // P_0 = 1: the gradient of core 0 is E_1 (or dW when d = 1)
+    xa.splits[0] = nin;
+    xa.d = d;
+    xa.compacted = p->compacted ? 1 : 0;
+    xa.swap = 1;
+    for (int k = 0; k < d; ++k) {
+        xa.D[k] = (D && k < d - 1) ? D[k] : nullptr;
+        xa.dG[k] = dG[k];
+        xa.m[k] = int(p->s.m[k]);
+        xa.n[k] = int(p->s.n[k]);
+    }
+    for (int k = 0; k <= d; ++k) {
+        xa.r[k] = int(p->s.r[k]);
+        xa.rc[k] = int(p->rho[k]);
+        xa.act[k] = p->act[k];
+    }
+    return hip_status(launch_expand(xa, stream));
+}
 
 }  // namespace
 
@@ -205,7 +292,7 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
     const int64_t NJl = p->N_out / ml;
     const int splits = int((b + L.dw_kchunk - 1) / L.dw_kchunk);
     float *dw = reinterpret_cast<float *>(at(ws, L.dw));
-    float *dwp = splits > 1 ? reinterpret_cast<float *>(at(ws, L.dw_part)) : dw;
+    float *dwp = (splits > 1 || L.proj) ? reinterpret_cast<float *>(at(ws, L.dw_part)) : dw;
     {
         void *ev;
         timing_begin(p, COMERA_KERNEL_DW, stream, &ev);
@@ -237,6 +324,7 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
         timing_end(p, COMERA_KERNEL_DW, stream, ev);
         if (e) return COMERA_ERR_HIP;
     }
+    if (L.proj) return project_dense(p, bd, dwp, splits, D, dG, ws, stream);
     if (splits > 1) {
         e = launch_sum_splits(dwp, dw, p->N_in * p->N_out, splits, stream);
         if (e) return COMERA_ERR_HIP;

@@ -43,6 +43,13 @@ struct DenseLayout {
     int meet_splits[kMaxCores];
     int adj_splits[kMaxCores];  // split-K of the adjoint step producing E_k
     size_t adj_part;           // shared scratch for adjoint split partials
+    // fused projection route (all ranks within proj_supported): step k reads
+    // E_{k+1} as e_slices[k+1] slices and writes E_k as e_slices[k] slices
+    // (one per column chunk) and meet_splits[k] meet partials (one per row chunk)
+    bool proj;
+    int proj_rt[kMaxCores];
+    int proj_ct[kMaxCores];
+    int e_slices[kMaxCores + 1];
 };
 
 }  // namespace comera
@@ -118,6 +125,49 @@ struct Remap {
     int64_t stride[4];
 };
 Remap remap_linear(int64_t stride);
+
+// Fused projection step of the core gradients for one core k (dense order):
+// with En = E_{k+1} (rows (I, J), columns (x, y, c)), the folded core
+// Gc = G~_k [A][cols] and the left chain P = P_k [rows][A],
+//   adjoint  E_k[row][a]   = sum_c En[row][c] Gc[a][c]       (per column chunk)
+//   meet     part[a][c]    = sum_row P[row][a] En[row][c]     (per row chunk)
+// En may come as `nin` slices that are summed in slice order on load.  The
+// adjoint output of column chunk j goes to Eout + j * out_stride +
+// rmap(row) + a; the meet partial of row chunk i to part + i * A * cols.
+struct ProjArgs {
+    const float *En;
+    int nin;
+    int64_t in_stride;
+    const float *Gc;    // null: no adjoint
+    const float *P;     // null: no meet
+    float *Eout;
+    int64_t out_stride;
+    Remap rmap;
+    float *part;
+    int64_t rows, cols;
+    int A;
+    int RT, CT;
+};
+// tile choice (rows per chunk RT, columns per chunk CT) for a projection step
+void proj_tiles(int64_t rows, int64_t cols, int A, int &RT, int &CT);
+bool proj_supported(int A);
+int launch_proj(const ProjArgs &a, void *stream);
+
+// Last step of the W rebuild (proj.hip): out = W [N_in][N_out] or W^T
+// [N_out][N_in] from P_{d-1} [NI][NJ][A] and the folded last core [A][nx][ny].
+struct WBuildArgs {
+    const float *P;
+    const float *G;
+    void *out;
+    int64_t NI, NJ;
+    int A, nx, ny;
+    int transpose;
+    int out_bf16;
+    int QB;
+};
+bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, bool transpose, int &QB);
+int launch_wbuild(const WBuildArgs &a, void *stream);
+
 
 struct GemmArgs {
     int dtype = COMERA_F32;          // operand type

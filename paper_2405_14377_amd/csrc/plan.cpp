@@ -135,6 +135,8 @@ bool validate(const comera_ttm_shape *s, int64_t batch) {
     for (int k = 0; k < s->d; ++k) {
         if (s->n[k] < 1 || s->m[k] < 1 || s->r[k] < 1 || s->r[k + 1] < 1) return false;
         if (s->r[k] > 4096) return false;
+        // every core (and its gradient) is indexed with 32-bit offsets
+        if (double(s->r[k]) * double(s->m[k]) * double(s->n[k]) * double(s->r[k + 1]) > 2147483647.0) return false;
         nin *= double(s->n[k]);
         nout *= double(s->m[k]);
     }
@@ -176,6 +178,36 @@ void layout_dense(comera_ttm_plan_s *p) {
     splits = (b + kchunk - 1) / kchunk;
     L.dw_splits = int(splits);
     L.dw_kchunk = kchunk;
+    L.proj = true;
+    for (int k = 1; k < d; ++k) L.proj = L.proj && proj_supported(int(p->rho[k]));
+    if (L.proj) {
+        // fused projections: dW stays as its split partials, each step writes
+        // its environment as column-chunk slices and its meet partials
+        L.dw_part = off;
+        off = align_up(off + sizeof(float) * size_t(splits) * size_t(p->N_in * p->N_out));
+        L.dw = L.dw_part;
+        L.e_slices[d] = int(splits);
+        int64_t Ia = p->N_in, Ja = p->N_out;
+        for (int k = d - 1; k >= 1; --k) {
+            Ia /= p->s.n[k];
+            Ja /= p->s.m[k];
+            const int64_t rows = Ia * Ja, cols = p->s.n[k] * p->s.m[k] * p->rho[k + 1];
+            const int A = int(p->rho[k]);
+            int RT = 0, CT = 0;
+            proj_tiles(rows, cols, A, RT, CT);
+            L.proj_rt[k] = RT;
+            L.proj_ct[k] = CT;
+            L.e_slices[k] = int((cols + CT - 1) / CT);
+            L.meet_splits[k] = int((rows + RT - 1) / RT);
+            L.e[k] = off;
+            off = align_up(off + sizeof(float) * size_t(L.e_slices[k]) * size_t(rows * A));
+            L.gpart[k] = off;
+            off = align_up(off + sizeof(float) * size_t(L.meet_splits[k]) * size_t(A * cols));
+        }
+        L.meet_splits[0] = L.e_slices[1];
+        L.total = off;
+        return;
+    }
     L.dw_part = off;
     if (splits > 1) off = align_up(off + sizeof(float) * size_t(splits) * size_t(p->N_in * p->N_out));
     L.dw = off;

@@ -55,29 +55,33 @@ __global__ void fold_kernel(FoldArgs a) {
     const int k = blockIdx.y;
     if (k >= a.nfold) return;
     const int rl = a.rc[k], rr = a.rc[k + 1], m = a.m[k], n = a.n[k];
-    const int64_t total = int64_t(rl) * m * n * rr;
+    const int total = rl * m * n * rr;     // core sizes are far below 2^31 (host checks)
+    const int mn_ = m * n;
     const float *G = a.G[k];
     const float *D = (k < a.d - 1) ? a.D[k] : nullptr;
-    for (int64_t o = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; o < total;
-         o += int64_t(gridDim.x) * blockDim.x) {
-        int c = int(o % rr);
-        int64_t t = o / rr;
-        int mn = int(t % (int64_t(m) * n));
-        int al = int(t / (int64_t(m) * n));
+    for (int o = blockIdx.x * blockDim.x + threadIdx.x; o < total; o += gridDim.x * blockDim.x) {
+        const int c = o % rr;
+        const int t = o / rr;
+        const int mn = t % mn_;
+        const int al = t / mn_;
         int fa = al, fc = c;
         if (a.compacted) {
             fa = (k == 0) ? 0 : select_bit(a.act[k], al);
             fc = (k == a.d - 1) ? 0 : select_bit(a.act[k + 1], c);
         }
         // output element o = (al, q, c) with q over (m, n), or (n, m) when swapped
-        int jm = a.swap ? mn % m : mn / n, in = a.swap ? mn / m : mn % n;
-        float v = G[((int64_t(fa) * m + jm) * n + in) * a.r[k + 1] + fc];
+        const int jm = a.swap ? mn % m : mn / n, in = a.swap ? mn / m : mn % n;
+        float v = G[((fa * m + jm) * n + in) * a.r[k + 1] + fc];
         if (D) v *= D[fc];
         a.Gc[k][o] = v;
     }
 }
 
-__global__ void expand_kernel(ExpandArgs a) {
+// Workgroup of 256 threads = 32 outputs x 8 split groups: group g sums the
+// splits [g S / 8, (g + 1) S / 8) in order, then group 0 adds the eight group
+// sums in order.  The result is the same for every launch shape.
+__global__ __launch_bounds__(256) void expand_kernel(ExpandArgs a) {
+    __shared__ float red[8][33];
     const int k = blockIdx.y;
     if (k >= a.d || !a.dG[k]) return;
     const int rl = a.r[k], rr = a.r[k + 1], m = a.m[k], n = a.n[k];
@@ -85,25 +89,52 @@ __global__ void expand_kernel(ExpandArgs a) {
     const int64_t total = int64_t(rl) * m * n * rr;
     const int64_t csize = int64_t(crl) * m * n * crr;
     const float *D = (k < a.d - 1) ? a.D[k] : nullptr;
-    for (int64_t o = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; o < total;
-         o += int64_t(gridDim.x) * blockDim.x) {
-        int c = int(o % rr);
-        int64_t t = o / rr;
-        int mn = int(t % (int64_t(m) * n));
-        int al = int(t / (int64_t(m) * n));
-        int ca = al, cc = c;
-        if (a.compacted) {
-            ca = (k == 0) ? 0 : rank_bit(a.act[k], al);
-            cc = (k == a.d - 1) ? 0 : rank_bit(a.act[k + 1], c);
+    const int lo = threadIdx.x & 31, g = threadIdx.x >> 5;
+    const int S = a.splits[k];
+    const int s0 = int(int64_t(g) * S / 8), s1 = int(int64_t(g + 1) * S / 8);
+    const float *part = a.part[k];
+    const int tot32 = int(total), mn_ = m * n;   // core sizes are far below 2^31 (host checks)
+    for (int base = blockIdx.x * 32; base < tot32; base += gridDim.x * 32) {
+        const int o = base + lo;
+        int ci = -1;
+        if (o < tot32) {
+            const int c = o % rr;
+            const int t = o / rr;
+            const int mn = t % mn_;
+            const int al = t / mn_;
+            int ca = al, cc = c;
+            if (a.compacted) {
+                ca = (k == 0) ? 0 : rank_bit(a.act[k], al);
+                cc = (k == a.d - 1) ? 0 : rank_bit(a.act[k + 1], c);
+            }
+            if (ca >= 0 && cc >= 0) {
+                const int jm = mn / n, in = mn % n;
+                ci = (ca * mn_ + (a.swap ? in * m + jm : mn)) * crr + cc;
+            }
         }
         float v = 0.f;
-        if (ca >= 0 && cc >= 0) {
-            const int jm = mn / n, in = mn % n;
-            const int64_t ci = (int64_t(ca) * m * n + (a.swap ? in * m + jm : mn)) * crr + cc;
-            for (int s = 0; s < a.splits[k]; ++s) v += a.part[k][s * csize + ci];
-            if (D) v *= D[c];
+        if (ci >= 0) {
+            int s = s0;
+            for (; s + 8 <= s1; s += 8) {
+                float x[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) x[u] = part[(s + u) * csize + ci];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) v += x[u];
+            }
+            for (; s < s1; ++s) v += part[s * csize + ci];
         }
-        a.dG[k][o] = v;
+        red[g][lo] = v;
+        __syncthreads();
+        if (g == 0 && o < tot32) {
+            float t = red[0][lo];
+#pragma unroll
+            for (int gg = 1; gg < 8; ++gg) t += red[gg][lo];
+            if (ci < 0) t = 0.f;
+            else if (D) t *= D[o % rr];
+            a.dG[k][o] = t;
+        }
+        __syncthreads();
     }
 }
 
@@ -141,7 +172,7 @@ int launch_fold(const FoldArgs &a, void *stream) {
 int launch_expand(const ExpandArgs &a, void *stream) {
     int64_t mx = 1;
     for (int k = 0; k < a.d; ++k) mx = std::max<int64_t>(mx, int64_t(a.r[k]) * a.m[k] * a.n[k] * a.r[k + 1]);
-    dim3 grid(grid_for(mx), a.d);
+    dim3 grid(grid_for(mx, 32), a.d);
     hipLaunchKernelGGL(expand_kernel, grid, dim3(256), 0, hipStream_t(stream), a);
     return int(hipGetLastError());
 }
