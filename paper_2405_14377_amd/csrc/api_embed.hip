@@ -48,79 +48,73 @@ bool embed_dims(const comera_tt_embed_shape *s, EmbedDims &dm) {
 
 // Limits of the kernels' LDS staging; larger tables are refused.
 bool embed_supported(const EmbedDims &dm) {
-    double table = double(dm.Vp) * double(dm.Ep) * double(dm.R) * 4.0;
-    return embed_kernels_support(int(dm.Ep), dm.R, dm.Es, dm.E) && embed_gs_fits(dm.R, dm.Vs, dm.Es) && table <= 8.0e9;
+    const double table = double(dm.Vp) * double(dm.Ep) * double(dm.R) * 4.0;
+    return embed_kernels_support(dm.Ep, dm.R, dm.Vs, dm.Es, dm.d) && table <= 8.0e9;
+}
+
+int radix_passes(int64_t V) {
+    int bits = 0;
+    while ((int64_t(1) << bits) <= V) ++bits;   // keys 0..V inclusive (V marks an out-of-range id)
+    return (bits + 7) / 8;
 }
 
 void embed_layout(const comera_tt_embed_shape *s, const EmbedDims &dm, int64_t n, EmbedLayout &L) {
     std::memset(&L, 0, sizeof(L));
     const int d = dm.d;
     size_t off = 0;
-    for (int k = 0; k < d - 1; ++k) {
-        L.gc[k] = off;
-        off = align_up(off + sizeof(float) * size_t(s->r[k] * s->v[k] * s->e[k] * s->r[k + 1]));
-    }
-    int64_t Vl = 1, El = 1;
-    for (int k = 1; k < d; ++k) {
-        Vl *= s->v[k - 1];
-        El *= s->e[k - 1];
-        L.p[k] = off;
-        off = align_up(off + sizeof(float) * size_t(Vl * El * s->r[k]));
-    }
-    const size_t nn = size_t(std::max<int64_t>(n, 1));
     auto take = [&](size_t bytes) {
         size_t o = off;
         off = align_up(off + bytes);
         return o;
     };
+    for (int k = 0; k < d - 1; ++k) L.gc[k] = take(sizeof(float) * size_t(s->r[k] * s->v[k] * s->e[k] * s->r[k + 1]));
+    int64_t Vl = 1, El = 1;
+    for (int k = 1; k < d; ++k) {
+        Vl *= s->v[k - 1];
+        El *= s->e[k - 1];
+        L.p[k] = take(sizeof(float) * size_t(Vl * El * s->r[k]));
+    }
+    const size_t nn = size_t(std::max<int64_t>(n, 1));
+    L.passes = radix_passes(dm.V);
     L.keysA = take(4 * nn);
     L.valsA = take(4 * nn);
     L.keysB = take(4 * nn);
     L.valsB = take(4 * nn);
     const size_t nblk = (nn + 1023) / 1024, nchunk = (nn + kEmbedItem - 1) / kEmbedItem;
-    L.hist = take(4 * 256 * nblk);
+    L.hist = take(4 * (256 * nblk + nblk));   // one pass's digit histograms, then out-of-range counts
     L.meta = take(4 * 16);
+    L.headpos = take(4 * size_t(dm.V));
     L.S = take(sizeof(float) * nn * size_t(dm.E));
     L.Pfirst = take(sizeof(float) * nchunk * size_t(dm.E));
     L.Plast = take(sizeof(float) * nchunk * size_t(dm.E));
-    L.dA = take(sizeof(float) * size_t(dm.Vp * dm.Ep * dm.R));
-    L.dglast_part = take(sizeof(float) * size_t(kEmbedChunks) * size_t(dm.R) * dm.Vs * dm.Es);
-    Vl = 1;
-    El = 1;
-    for (int k = 1; k < d - 1; ++k) {
-        Vl *= s->v[k - 1];
-        El *= s->e[k - 1];
-        L.e[k] = take(sizeof(float) * size_t(Vl * El * s->r[k]));
+    L.nvp = embed_dglast_chunks(dm.Vp);
+    if (d > 1) {
+        L.dA = take(sizeof(float) * size_t(dm.Vp * dm.Ep * dm.R));
+        L.dglast_part = take(sizeof(float) * size_t(L.nvp) * size_t(dm.R) * dm.Vs * dm.Es);
     }
-    {
-        size_t adj_max = 0;
-        int64_t Va = dm.Vp, Ea = dm.Ep;
-        for (int k = d - 2; k >= 1; --k) {
-            Va /= s->v[k];
-            Ea /= s->e[k];
-            int64_t M = Va * Ea, N = s->r[k], K = s->v[k] * s->e[k] * s->r[k + 1];
-            int sp = split_for(M, N, K);
-            L.adj_splits[k] = sp;
-            if (sp > 1) adj_max = std::max(adj_max, sizeof(float) * size_t(sp) * size_t(M * N));
-        }
-        L.adj_part = take(adj_max);
-    }
-    Vl = 1;
-    El = 1;
-    for (int k = 0; k < d - 1; ++k) {
-        int64_t K = Vl * El;
-        int64_t M = s->r[k], N = s->v[k] * s->e[k] * s->r[k + 1];
-        int64_t sp = split_for(M, N, K);
-        L.meet_splits[k] = int(sp);
-        L.gpart[k] = take(sizeof(float) * size_t(sp * M * N));
-        Vl *= s->v[k];
-        El *= s->e[k];
+    // projections of dA onto the prefix cores k = d-2 .. 1, as for a linear
+    // layer: rows (V_<k, E_<k), columns (v_k, e_k, r_{k+1}), rank r_k
+    L.e_slices[d - 1] = 1;
+    int64_t Va = dm.Vp, Ea = dm.Ep;
+    for (int k = d - 2; k >= 1; --k) {
+        Va /= s->v[k];
+        Ea /= s->e[k];
+        const int64_t rows = Va * Ea, cols = s->v[k] * s->e[k] * s->r[k + 1];
+        const int A = int(s->r[k]);
+        int RT = 0, CT = 0;
+        proj_tiles(rows, cols, A, RT, CT);
+        L.proj_rt[k] = RT;
+        L.proj_ct[k] = CT;
+        L.e_slices[k] = int((cols + CT - 1) / CT);
+        L.meet_splits[k] = int((rows + RT - 1) / RT);
+        L.e[k] = take(sizeof(float) * size_t(L.e_slices[k]) * size_t(rows * A));
+        L.gpart[k] = take(sizeof(float) * size_t(L.meet_splits[k]) * size_t(A * cols));
     }
     L.total = off;
 }
 
 // fold the masks into the prefix cores and build the prefix table
-// A = P_{d-1}[Vp, Ep, r_{d-1}] (eq. emb_A1 over cores 0..d-2)
+// A = P_{d-1} (eq. emb_A1 over cores 0..d-2), stored [Vp][r_{d-1}][Ep]
 int build_prefix(const comera_tt_embed_shape *s, const EmbedLayout &L, const float *const *G, const float *const *D,
                  void *ws, void *stream, float **gc, float **P) {
     const int d = s->d;
@@ -149,8 +143,10 @@ int build_prefix(const comera_tt_embed_shape *s, const EmbedLayout &L, const flo
     int64_t Vl = s->v[0], El = s->e[0];
     for (int k = 1; k < d - 1; ++k) {
         float *out = reinterpret_cast<float *>(at(ws, L.p[k + 1]));
+        // the prefix table itself (k = d-2) is written rank-major, [Vp][R][Ep],
+        // so that a wave reads a row A[vp, :, a] with coalesced loads
         e = chain_gemm(P[k], gc[k], out, false, Vl, El, int(s->r[k]), int(s->v[k]), int(s->e[k]), int(s->r[k + 1]),
-                       stream);
+                       stream, k == d - 2 ? kChainRankMajor : kChainNormal);
         if (e) return e;
         P[k + 1] = out;
         Vl *= s->v[k];
@@ -167,11 +163,20 @@ EmbedWs embed_ws(const EmbedLayout &L, void *ws) {
     w.valsB = reinterpret_cast<uint32_t *>(at(ws, L.valsB));
     w.hist = reinterpret_cast<int *>(at(ws, L.hist));
     w.meta = reinterpret_cast<int *>(at(ws, L.meta));
+    w.headpos = reinterpret_cast<int *>(at(ws, L.headpos));
     w.S = reinterpret_cast<float *>(at(ws, L.S));
     w.Pfirst = reinterpret_cast<float *>(at(ws, L.Pfirst));
     w.Plast = reinterpret_cast<float *>(at(ws, L.Plast));
-    w.dglast_part = reinterpret_cast<float *>(at(ws, L.dglast_part));
+    w.dA = L.dA ? reinterpret_cast<float *>(at(ws, L.dA)) : nullptr;
+    w.dglast_part = L.dglast_part ? reinterpret_cast<float *>(at(ws, L.dglast_part)) : nullptr;
     return w;
+}
+
+// the prefix-core projections take ranks up to the projection kernel's limit
+bool embed_proj_ok(const comera_tt_embed_shape *s) {
+    for (int k = 1; k < s->d - 1; ++k)
+        if (!proj_supported(int(s->r[k]))) return false;
+    return true;
 }
 
 comera_status hip_status(int e) { return e ? COMERA_ERR_HIP : COMERA_OK; }
@@ -206,8 +211,9 @@ comera_status comera_tt_embed_forward(const comera_tt_embed_shape *s, const int6
     int e = build_prefix(s, L, G, D, ws, stream, gc, P);
     if (e) return COMERA_ERR_HIP;
     const float *Apre = s->d > 1 ? P[s->d - 1] : nullptr;
-    return hip_status(launch_embed_rows(ids, n_tokens, dm.V, Apre, G[s->d - 1], Y, int(dm.Ep), dm.R, dm.Vs, dm.Es,
-                                        err_flag, stream));
+    // the prefix table is rank-major when it comes from a chain (d >= 3)
+    return hip_status(launch_embed_rows(ids, n_tokens, dm.V, Apre, s->d >= 3, G[s->d - 1], Y, int(dm.Ep), dm.R, dm.Vs,
+                                        dm.Es, err_flag, stream));
 }
 
 comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int64_t *ids, int64_t n_tokens,
@@ -217,7 +223,7 @@ comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int
     (void)deterministic;
     EmbedDims dm;
     if (!embed_dims(s, dm) || n_tokens < 0 || n_tokens >= 2147483647) return COMERA_ERR_INVALID_ARG;
-    if (!embed_supported(dm)) return COMERA_ERR_UNSUPPORTED;
+    if (!embed_supported(dm) || !embed_proj_ok(s)) return COMERA_ERR_UNSUPPORTED;
     if (!dG || !G) return COMERA_ERR_INVALID_ARG;
     const int d = s->d;
     for (int k = 0; k < d; ++k)
@@ -239,16 +245,69 @@ comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int
     if (e) return COMERA_ERR_HIP;
     const float *Apre = d > 1 ? P[d - 1] : nullptr;
     EmbedWs w = embed_ws(L, ws);
-    e = launch_embed_sort(ids, int(n_tokens), dm.V, w, err_flag, stream);
+    const int n = int(n_tokens);
+    // group tokens by id (dA cleared on the way: prefixes without ids keep 0)
+    e = launch_embed_sort(ids, n, dm.V, L.passes, w, err_flag, dm.V, w.dA, d > 1 ? dm.Vp * dm.Ep * dm.R : 0, stream);
     if (e) return COMERA_ERR_HIP;
-    e = launch_embed_segsum(dY, int(dm.E), int(n_tokens), dm.V, w, stream);
+    e = launch_embed_segsum(dY, int(dm.E), n, L.passes, w, stream);
     if (e) return COMERA_ERR_HIP;
-    e = launch_embed_dglast(w, int(n_tokens), dm.V, Apre, int(dm.Ep), dm.R, dm.Vs, dm.Es, stream);
+    if (d == 1) return hip_status(launch_embed_gather(w, dm.V, int(dm.E), dG[0], stream));
+    e = launch_embed_dapre(w, G[d - 1], dm.Vp, int(dm.Ep), dm.R, dm.Vs, dm.Es, int(s->v[d - 2]), int(s->e[d - 2]),
+                           stream);
     if (e) return COMERA_ERR_HIP;
+    e = launch_embed_dglast(w, Apre, d >= 3, dm.Vp, int(dm.Ep), dm.R, dm.Vs, dm.Es, stream);
+    if (e) return COMERA_ERR_HIP;
+    // dA is E_{d-1} for the prefix cores: project it right to left as for a
+    // linear layer (folded cores gc[k], left chains P[k])
     ExpandArgs xa;
     std::memset(&xa, 0, sizeof(xa));
+    const float *En = w.dA;
+    int nin = 1;
+    int64_t in_stride = 0;
+    int64_t Vl = dm.Vp, El = dm.Ep;
+    for (int k = d - 2; k >= 1; --k) {
+        Vl /= s->v[k];
+        El /= s->e[k];
+        const int A = int(s->r[k]);
+        const int64_t rows = Vl * El, cols = s->v[k] * s->e[k] * s->r[k + 1];
+        ProjArgs pa;
+        pa.En = En;
+        pa.nin = nin;
+        pa.in_stride = in_stride;
+        pa.Gc = gc[k];
+        pa.P = P[k];
+        pa.Eout = reinterpret_cast<float *>(at(ws, L.e[k]));
+        pa.out_stride = rows * A;
+        const int64_t nxp = s->v[k - 1], nyp = s->e[k - 1], NJp = El / nyp;
+        pa.rmap.nd = 4;
+        pa.rmap.radix[1] = nxp;
+        pa.rmap.radix[2] = NJp;
+        pa.rmap.radix[3] = nyp;
+        pa.rmap.stride[0] = NJp * nxp * nyp * A;
+        pa.rmap.stride[1] = nyp * A;
+        pa.rmap.stride[2] = nxp * nyp * A;
+        pa.rmap.stride[3] = A;
+        pa.part = reinterpret_cast<float *>(at(ws, L.gpart[k]));
+        pa.rows = rows;
+        pa.cols = cols;
+        pa.A = A;
+        pa.RT = L.proj_rt[k];
+        pa.CT = L.proj_ct[k];
+        e = launch_proj(pa, stream);
+        if (e) return COMERA_ERR_HIP;
+        xa.part[k] = pa.part;
+        xa.splits[k] = L.meet_splits[k];
+        En = pa.Eout;
+        nin = L.e_slices[k];
+        in_stride = pa.out_stride;
+    }
+    xa.part[0] = En;     // the gradient of core 0 is E_1 (or dA itself when d = 2)
+    xa.splits[0] = nin;
+    xa.part[d - 1] = w.dglast_part;
+    xa.splits[d - 1] = L.nvp;
     xa.d = d;
     xa.compacted = 0;
+    xa.swap = 0;
     for (int k = 0; k <= d; ++k) {
         xa.r[k] = int(s->r[k]);
         xa.rc[k] = int(s->r[k]);
@@ -258,44 +317,6 @@ comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int
         xa.dG[k] = dG[k];
         xa.m[k] = int(s->v[k]);
         xa.n[k] = int(s->e[k]);
-    }
-    xa.part[d - 1] = w.dglast_part;
-    xa.splits[d - 1] = kEmbedChunks;
-    if (d > 1) {
-        // E_{d-1} = dA over the prefix table (blocked), then right
-        // environments and meets on the prefix cores as for a linear layer
-        float *Ek[kMaxCores + 1] = {};
-        Ek[d - 1] = reinterpret_cast<float *>(at(ws, L.dA));
-        e = launch_embed_dapre(w, int(n_tokens), dm.V, G[d - 1], dm.Vp, int(dm.Ep), dm.R, dm.Vs, dm.Es, int(s->v[d - 2]),
-                               int(s->e[d - 2]), Ek[d - 1], stream);
-        if (e) return COMERA_ERR_HIP;
-        int64_t Vl = dm.Vp, El = dm.Ep;
-        for (int k = d - 2; k >= 1; --k) {
-            Vl /= s->v[k];
-            El /= s->e[k];
-            Ek[k] = reinterpret_cast<float *>(at(ws, L.e[k]));
-            e = adjoint_gemm(Ek[k + 1], gc[k], Ek[k], Vl, El, int(s->r[k]), int(s->v[k]), int(s->e[k]),
-                             int(s->r[k + 1]), int(s->v[k - 1]), int(s->e[k - 1]), L.adj_splits[k],
-                             reinterpret_cast<float *>(at(ws, L.adj_part)), stream);
-            if (e) return COMERA_ERR_HIP;
-        }
-        Vl = 1;
-        El = 1;
-        for (int k = 0; k < d - 1; ++k) {
-            if (k == 0) {
-                xa.part[0] = Ek[1];
-                xa.splits[0] = 1;
-            } else {
-                float *part = reinterpret_cast<float *>(at(ws, L.gpart[k]));
-                e = meet_gemm(P[k], Ek[k + 1], part, Vl, El, int(s->r[k]), int(s->v[k]), int(s->e[k]),
-                              int(s->r[k + 1]), L.meet_splits[k], stream);
-                if (e) return COMERA_ERR_HIP;
-                xa.part[k] = part;
-                xa.splits[k] = L.meet_splits[k];
-            }
-            Vl *= s->v[k];
-            El *= s->e[k];
-        }
     }
     return hip_status(launch_expand(xa, stream));
 }

@@ -53,7 +53,7 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
         e = launch_fill_one(ones, stream);
         if (e) return e;
         return chain_gemm(ones, bd.gc[0], at(ws, L.w), bf, 1, 1, 1, int(p->s.n[0]), int(p->s.m[0]), 1, stream,
-                          transpose);
+                          transpose ? kChainT : kChainNormal);
     }
     bd.P[1] = bd.gc[0];  // rho_0 = 1: [n_0][m_0][rho_1] is the folded core itself
     int64_t Il = p->s.n[0], Jl = p->s.m[0];
@@ -77,7 +77,7 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
             return launch_wbuild(wa, stream);
         }
         e = chain_gemm(bd.P[k], bd.gc[k], out, last && bf, Il, Jl, int(p->rho[k]), int(p->s.n[k]), int(p->s.m[k]),
-                       int(p->rho[k + 1]), stream, last && transpose);
+                       int(p->rho[k + 1]), stream, last && transpose ? kChainT : kChainNormal);
         if (e) return e;
         if (!last) bd.P[k + 1] = reinterpret_cast<float *>(out);
         Il *= p->s.n[k];

@@ -9,7 +9,6 @@
 namespace comera {
 
 constexpr int kEmbedItem = 16;     // sorted positions per chunk of the backward segment sums
-constexpr int kEmbedChunks = 256;  // fixed split of the sorted positions for dG_last
 
 struct EmbedDims {
     int d;
@@ -21,37 +20,49 @@ struct EmbedDims {
 struct EmbedLayout {
     size_t gc[kMaxCores];      // mask-folded prefix cores
     size_t p[kMaxCores];       // prefix chains P_k, k = 1..d-1 (P_{d-1} = prefix table)
-    size_t keysA, valsA, keysB, valsB, hist, meta;
+    size_t keysA, valsA, keysB, valsB, hist, meta, headpos;
     size_t S, Pfirst, Plast, dA, dglast_part;
-    size_t e[kMaxCores];       // environments E_k, k = 1..d-2
-    size_t gpart[kMaxCores];   // meet partials for the prefix cores
+    int passes;                // radix passes
+    int nvp;                   // dG_last partials (chunks of prefixes)
+    // projections onto the prefix cores k = d-2 .. 1 (as for a linear layer)
+    size_t e[kMaxCores];       // environment slices E_k
+    size_t gpart[kMaxCores];   // meet partials of core k
+    int e_slices[kMaxCores + 1];
     int meet_splits[kMaxCores];
-    int adj_splits[kMaxCores];
-    size_t adj_part;
+    int proj_rt[kMaxCores], proj_ct[kMaxCores];
     size_t total;
 };
 
 struct EmbedWs {
     uint32_t *keysA, *valsA, *keysB, *valsB;
-    int *hist;
-    int *meta;   // meta[0] = number of in-range ids
-    float *S, *Pfirst, *Plast, *dglast_part;
+    int *hist;      // [256][nblk] digit counts of the current pass, then [nblk] out-of-range counts
+    int *meta;      // meta[0] = number of in-range ids
+    int *headpos;   // [V] sorted position of the first token of each id, -1 if absent
+    float *S, *Pfirst, *Plast, *dA, *dglast_part;
 };
 
-int launch_embed_rows(const int64_t *ids, int64_t n, int64_t V, const float *Apre, const float *Gs, float *Y, int Ep,
-                      int R, int Vs, int Es, int *err_flag, void *stream);
-int launch_embed_sort(const int64_t *ids, int n, int64_t V, const EmbedWs &w, int *err_flag, void *stream);
-int launch_embed_segsum(const float *dY, int E, int n, int64_t V, const EmbedWs &w, void *stream);
-int launch_embed_dglast(const EmbedWs &w, int n, int64_t V, const float *Apre, int Ep, int R, int Vs, int Es,
-                        void *stream);
-// dA is written blocked for the prefix-core projections: [(V', E')][(vq, eq)][R]
-// with vp = V' vq + x, ep = E' eq + y (vq, eq = factors of the last prefix core)
-int launch_embed_dapre(const EmbedWs &w, int n, int64_t V, const float *Gs, int64_t Vp, int Ep, int R, int Vs, int Es,
-                       int vq, int eq, float *dA, void *stream);
-// shapes the embedding kernels handle (rank of the last bond <= 64, a dY row
-// of the backward fix-up fits in LDS four times)
-bool embed_kernels_support(int Ep, int R, int Es, int64_t E);
-// the last core fits in LDS (staged whole by the row and dA kernels)
-bool embed_gs_fits(int R, int Vs, int Es);
+// A = prefix table [Vp][Ep][R], or [Vp][R][Ep] when rank_major
+int launch_embed_rows(const int64_t *ids, int64_t n, int64_t V, const float *Apre, bool rank_major, const float *Gs,
+                      float *Y, int Ep, int R, int Vs, int Es, int *err_flag, void *stream);
+// stable LSD radix sort of the ids (out-of-range ids get the key V and sort
+// last) and n_valid into meta[0]; its first kernel also clears
+// headpos[0 .. nclear) to -1 and zero[0 .. nzero) to 0
+int launch_embed_sort(const int64_t *ids, int n, int64_t V, int passes, const EmbedWs &w, int *err_flag,
+                      int64_t nclear, float *zero, int64_t nzero, void *stream);
+const uint32_t *embed_sorted_keys(const EmbedWs &w, int passes);
+// per-id sums of dY rows in token order: S[head] (and headpos[id] = head)
+int launch_embed_segsum(const float *dY, int E, int n, int passes, const EmbedWs &w, void *stream);
+// dA [Vp][Ep][R] per prefix (written blocked for the prefix projections:
+// [(V', E')][(vq, eq)][R] with vp = V' vq + x, ep = E' eq + y)
+int launch_embed_dapre(const EmbedWs &w, const float *Gs, int64_t Vp, int Ep, int R, int Vs, int Es, int vq, int eq,
+                       void *stream);
+// dG_last partials, one per chunk of prefixes: [chunk][R][Vs][Es]
+int launch_embed_dglast(const EmbedWs &w, const float *Apre, bool rank_major, int64_t Vp, int Ep, int R, int Vs,
+                        int Es, void *stream);
+int embed_dglast_chunks(int64_t Vp);
+// d = 1: dG_0[0, v, e, 0] = S[headpos[v]][e] (0 for absent ids)
+int launch_embed_gather(const EmbedWs &w, int64_t V, int E, float *dG0, void *stream);
+// shapes the embedding kernels handle (LDS staging limits)
+bool embed_kernels_support(int64_t Ep, int R, int Vs, int Es, int d);
 
 }  // namespace comera

@@ -1,7 +1,7 @@
 // HIP kernels (gfx950) for the TTM embedding table of Sec. 4.1.
 //
 // The table T[V, E] is never formed.  The cores before the last one are
-// contracted into a prefix table A[Vp, Ep, r] over every value of the leading
+// contracted into a prefix table A[Vp, Ep, R] over every value of the leading
 // digits (eq. emb_A1 generalised to d-1 cores); a row is then
 //   T[id, (ep, es)] = sum_a A[vp, ep, a] * G_last[a, vs, es]
 // with vp = id / v_last and vs = id % v_last (eq. emb_unique with the last
@@ -10,19 +10,14 @@
 // Backward (the paper states only the lookup; the gradients follow from its
 // linearity).  Tokens are grouped by id with a stable LSD radix sort; the dY
 // rows of each id are summed in token order into S[p], p = the sorted
-// position of the id's first token (long runs are cut into chunks whose
-// partial sums are added in chunk order); then
-//   dG_last[a, vs, es] = sum_ids sum_ep A[vp, ep, a] S[ep, es]
-//   dA[vp, ep, a]      = sum_{ids in vp} sum_es S[ep, es] G_last[a, vs, es]
+// position of the id's first token (runs longer than a chunk are summed
+// chunk by chunk, the chunk sums added in chunk order).  Then, per prefix vp
+// and its ids u (in id order),
+//   dA[vp, ep, a]      = sum_u sum_es S_u[ep, es] G_last[a, vs_u, es]
+//   dG_last[a, vs, es] = sum_u sum_ep A[vp, ep, a] S_u[ep, es]
 // and dA is projected onto the prefix cores exactly like dW is for a linear
 // layer.  Every sum runs in a fixed order, so results are bitwise
 // reproducible.
-//
-// The contraction kernels are wave-centric: one wave owns a token, a prefix
-// or a (suffix digit, chunk) pair, keeps its accumulators in registers and
-// never waits on a workgroup barrier; operands whose address is the same for
-// the whole wave are read with scalar loads, and inner loops are unrolled
-// with clamped (always valid) indices so that loads are issued in batches.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -33,7 +28,11 @@
 namespace comera {
 namespace {
 
-constexpr int kMaxEs = 16;   // columns of the last core per register pass
+constexpr int kMaxEs = 16;          // columns of the last core per register pass
+constexpr int kBlk = 1024;          // keys per radix workgroup (256 threads x 4)
+constexpr int kSub = kBlk / 256;
+constexpr int kGlVp = 8;            // prefixes per dG_last workgroup (= partial)
+constexpr size_t kEmbLds = 64 * 1024;
 
 __device__ __forceinline__ uint64_t lanemask_lt() {
     const int lane = threadIdx.x & 63;
@@ -65,75 +64,78 @@ __device__ int wave_lower_bound(const uint32_t *__restrict__ keys, int lo, int h
 }
 
 // ---------------------------------------------------------------- forward rows
-// G_last is staged once per workgroup in LDS.  One wave per token: lane ep
-// loads its prefix row A[vp, ep, :] into registers (all loads issued before
-// the arithmetic) and accumulates T[id, ep, :] from LDS broadcast reads of
-// G_last[:, vs, :].
-__device__ __forceinline__ void stage_to_lds(float *dst, const float *__restrict__ src, int count) {
-    if ((reinterpret_cast<uintptr_t>(src) & 15) == 0 && (count & 3) == 0) {
-        const float4 *s4 = reinterpret_cast<const float4 *>(src);
-        float4 *d4 = reinterpret_cast<float4 *>(dst);
-        for (int i = threadIdx.x; i < count / 4; i += blockDim.x) d4[i] = s4[i];
-    } else {
-        for (int i = threadIdx.x; i < count; i += blockDim.x) dst[i] = src[i];
-    }
+// One wave per token.  Lane ep loads its prefix row A[vp, ep, :] into
+// registers (with the rank-major table, a wave reads 64 consecutive floats
+// per rank), the wave copies the slice G_last[:, vs, :] (R x Es floats) into
+// its own LDS region, all loads issued before any store; the slice is read
+// back as broadcast 16-byte LDS reads and every lane writes Es consecutive
+// outputs.  A element (vp, ep, a) sits at vp Ep R + ep sE + a sR.
+__device__ __forceinline__ void wave_sync_lds() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int RMAX>
+template <int RMAX, int NJ4>
 __global__ __launch_bounds__(256) void embed_rows_kernel(const int64_t *__restrict__ ids, int64_t n_tokens,
                                                          int64_t V, const float *__restrict__ Apre,
                                                          const float *__restrict__ Gs, float *__restrict__ Y, int Ep,
-                                                         int R, int Vs, int Es, int *__restrict__ err_flag) {
-    extern __shared__ float gs_s[];   // [R][Vs][Es]
-    stage_to_lds(gs_s, Gs, R * Vs * Es);
-    __syncthreads();
-    const int lane = threadIdx.x & 63;
-    const int64_t nw = int64_t(gridDim.x) * 4;
+                                                         int R, int Vs, int Es, int sE, int sR,
+                                                         int *__restrict__ err_flag) {
+    constexpr int ES4 = 4 * NJ4;
+    __shared__ __attribute__((aligned(16))) float gsl[4][RMAX * ES4];   // per wave: [RMAX][ES4], zero padded
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t t = int64_t(blockIdx.x) * 4 + wave;
+    if (t >= n_tokens) return;
+    const int64_t id = wave_uniform64(ids[t]);
     const int E = Ep * Es;
-    for (int64_t t = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6); t < n_tokens; t += nw) {
-        const int64_t id = wave_uniform64(ids[t]);
-        float *yrow = Y + t * E;
-        if (id < 0 || id >= V) {
-            if (lane == 0 && err_flag) *err_flag = 1;
-            for (int o = lane; o < E; o += 64) yrow[o] = 0.f;
-            continue;
-        }
-        const int64_t vp = id / Vs;
-        const int vs = int(id - vp * Vs);
-        for (int ep = lane; ep < Ep; ep += 64) {
-            float av[RMAX];
-            if (Apre) {
-                const float *ar = Apre + (vp * Ep + ep) * R;
+    float *yrow = Y + t * E;
+    if (id < 0 || id >= V) {
+        if (lane == 0 && err_flag) *err_flag = 1;
+        for (int o = lane; o < E; o += 64) yrow[o] = 0.f;
+        return;
+    }
+    const uint32_t vp = uint32_t(id) / uint32_t(Vs);        // ids are below 2^31
+    const int vs = int(uint32_t(id) - vp * uint32_t(Vs));
+    float *gw = gsl[wave];
+    for (int ep0 = 0; ep0 < Ep; ep0 += 64) {
+        const int ep = ep0 + lane;
+        const int epc = min(ep, Ep - 1);
+        float av[RMAX];
+        const float *ar = Apre ? Apre + int64_t(vp) * Ep * R + int64_t(epc) * sE : nullptr;
 #pragma unroll
-                for (int a = 0; a < RMAX; ++a) av[a] = ar[min(a, R - 1)];
+        for (int a = 0; a < RMAX; ++a) av[a] = ar ? ar[int64_t(min(a, R - 1)) * sR] : 1.f;
+        if (ep0 == 0)
+            stage_lds<(RMAX * ES4 + 63) / 64>(gw, RMAX * ES4, lane, 64, [&](int i) {
+                const int a = i / ES4, es = i - a * ES4;
+                return (a < R && es < Es) ? Gs[(int64_t(a) * Vs + vs) * Es + es] : 0.f;
+            });
+        wave_sync_lds();
+        float acc[ES4];
+#pragma unroll
+        for (int j = 0; j < ES4; ++j) acc[j] = 0.f;
+        // rows a >= R of the slice are zero, so the products for a >= R vanish
+#pragma unroll
+        for (int a = 0; a < RMAX; ++a) {
+#pragma unroll
+            for (int j4 = 0; j4 < NJ4; ++j4) {
+                const float4 g4 = *reinterpret_cast<const float4 *>(gw + a * ES4 + 4 * j4);
+                acc[4 * j4 + 0] += av[a] * g4.x;
+                acc[4 * j4 + 1] += av[a] * g4.y;
+                acc[4 * j4 + 2] += av[a] * g4.z;
+                acc[4 * j4 + 3] += av[a] * g4.w;
+            }
+        }
+        if (ep < Ep) {
+            float *yr = yrow + int64_t(ep) * Es;
+            if (Es == ES4 && (reinterpret_cast<uintptr_t>(yr) & 15) == 0) {
+#pragma unroll
+                for (int j = 0; j < ES4; j += 4)
+                    *reinterpret_cast<float4 *>(yr + j) = make_float4(acc[j], acc[j + 1], acc[j + 2], acc[j + 3]);
             } else {
 #pragma unroll
-                for (int a = 0; a < RMAX; ++a) av[a] = 1.f;
-            }
-            __builtin_amdgcn_sched_barrier(0);
-            for (int e0 = 0; e0 < Es; e0 += kMaxEs) {
-                const int ne = min(kMaxEs, Es - e0);
-                float acc[kMaxEs];
-#pragma unroll
-                for (int j = 0; j < kMaxEs; ++j) acc[j] = 0.f;
-#pragma unroll
-                for (int a = 0; a < RMAX; ++a) {
-                    if (a < R) {
-                        const float *g = gs_s + (a * Vs + vs) * Es + e0;
-#pragma unroll
-                        for (int j = 0; j < kMaxEs; ++j) acc[j] += av[a] * g[min(j, ne - 1)];
-                    }
-                }
-                float *yr = yrow + int64_t(ep) * Es + e0;
-                if (ne % 4 == 0 && (reinterpret_cast<uintptr_t>(yr) & 15) == 0) {
-#pragma unroll
-                    for (int j = 0; j < kMaxEs; j += 4)
-                        if (j < ne) *reinterpret_cast<float4 *>(yr + j) = make_float4(acc[j], acc[j + 1], acc[j + 2], acc[j + 3]);
-                } else {
-#pragma unroll
-                    for (int j = 0; j < kMaxEs; ++j)
-                        if (j < ne) yr[j] = acc[j];
-                }
+                for (int j = 0; j < ES4; ++j)
+                    if (j < Es) yr[j] = acc[j];
             }
         }
     }
@@ -142,45 +144,58 @@ __global__ __launch_bounds__(256) void embed_rows_kernel(const int64_t *__restri
 // ---------------------------------------------------------------- radix sort
 // Stable LSD radix sort of (key, token) pairs, 8-bit digits, kBlk keys per
 // workgroup.  Keys are the ids; out-of-range ids get the key V and sort last.
-constexpr int kBlk = 1024;          // keys per workgroup (256 threads x 4)
-constexpr int kSub = kBlk / 256;    // sub-tiles of 256 keys
-
+// Every pass takes the per-workgroup digit histograms of its own input order.
 __device__ __forceinline__ uint32_t key_of(const int64_t *ids, int i, int64_t V) {
     const int64_t id = ids[i];
     return (id >= 0 && id < V) ? uint32_t(id) : uint32_t(V);
 }
 
+// Workgroups b < nblk take the digit histogram of their kBlk keys (pass 0
+// reads the ids and also counts out-of-range ones); the others clear
+// headpos[0 .. nclear) to -1 and zero[0 .. nzero) to 0.0f.
 __global__ __launch_bounds__(256) void radix_hist_kernel(const int64_t *__restrict__ ids, const uint32_t *kin, int n,
                                                          int64_t V, int shift, int nblk, int *__restrict__ hist,
-                                                         int *err_flag) {
+                                                         int *__restrict__ bad_out, int *err_flag,
+                                                         int *__restrict__ headpos, int64_t nclear,
+                                                         float *__restrict__ zero, int64_t nzero) {
     __shared__ int h[256];
-    h[threadIdx.x] = 0;
-    __syncthreads();
+    __shared__ int bad_s;
     const int b = blockIdx.x;
-    bool bad = false;
+    if (b >= nblk) {
+        const int64_t stride = int64_t(gridDim.x - nblk) * 256;
+        const int64_t i0 = int64_t(b - nblk) * 256 + threadIdx.x;
+        for (int64_t i = i0; i < nclear; i += stride) headpos[i] = -1;
+        for (int64_t i = i0; i < nzero; i += stride) zero[i] = 0.f;
+        return;
+    }
+    h[threadIdx.x] = 0;
+    if (threadIdx.x == 0) bad_s = 0;
+    __syncthreads();
+    int bad = 0;
     for (int j = 0; j < kSub; ++j) {
         const int i = b * kBlk + j * 256 + threadIdx.x;
         if (i < n) {
-            uint32_t key;
-            if (kin) {
-                key = kin[i];
-            } else {
-                key = key_of(ids, i, V);
-                bad |= key == uint32_t(V);
-            }
+            const uint32_t key = kin ? kin[i] : key_of(ids, i, V);
+            bad += key == uint32_t(V);
             atomicAdd(&h[(key >> shift) & 255u], 1);
         }
     }
-    if (bad && err_flag) *err_flag = 1;
+    if (bad) atomicAdd(&bad_s, bad);
     __syncthreads();
     hist[threadIdx.x * nblk + b] = h[threadIdx.x];
+    if (threadIdx.x == 0 && bad_out) {
+        bad_out[b] = bad_s;
+        if (bad_s && err_flag) *err_flag = 1;
+    }
 }
 
-// exclusive scan of hist[256 * nblk] in place (digit-major order)
-__global__ __launch_bounds__(1024) void radix_scan_kernel(int *hist, int total) {
+// Exclusive scan of hist[256 * nblk] in place (digit-major order); with
+// bad != null also meta[0] = n - (number of out-of-range ids).
+__global__ __launch_bounds__(1024) void radix_scan_kernel(int *hist, int nblk, const int *bad, int n, int *meta) {
     __shared__ int wsum[17];
     __shared__ int carry;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int total = 256 * nblk;
     if (threadIdx.x == 0) carry = 0;
     __syncthreads();
     for (int base = 0; base < total; base += 1024) {
@@ -207,6 +222,11 @@ __global__ __launch_bounds__(1024) void radix_scan_kernel(int *hist, int total) 
         __syncthreads();
         if (threadIdx.x == 0) carry += wsum[16];
         __syncthreads();
+    }
+    if (threadIdx.x == 0 && bad) {
+        int nb = 0;
+        for (int b = 0; b < nblk; ++b) nb += bad[b];
+        meta[0] = n - nb;
     }
 }
 
@@ -266,26 +286,24 @@ __global__ __launch_bounds__(256) void radix_scatter_kernel(const int64_t *__res
     }
 }
 
-// number of in-range keys (position of the first key V) -> meta[0]
-__global__ __launch_bounds__(64) void nvalid_kernel(const uint32_t *__restrict__ keys, int n, int64_t V, int *meta) {
-    const int nv = wave_lower_bound(keys, 0, n, uint32_t(V));
-    if (threadIdx.x == 0) meta[0] = nv;
-}
-
 // ---------------------------------------------------------------- segment sums
 // Chunk c covers sorted positions [c * kEmbedItem, (c + 1) * kEmbedItem).
 // Each run of equal keys inside it is summed in position (= token) order.  A
 // run that is a whole segment goes to S[head]; a run cut by the chunk's end
-// goes to Plast[c]; a run cut by the chunk's start goes to Pfirst[c].  Every
-// dY row of the chunk is loaded once, all loads before the sums.
+// goes to Plast[c]; a run cut by the chunk's start goes to Pfirst[c].  A head
+// (first token of an id) inside the chunk records headpos[id].  Every dY row
+// of the chunk is loaded once, all loads before the sums, 16 bytes per load
+// when rows are 16-byte aligned.
 __global__ __launch_bounds__(256) void embed_segsum_kernel(const float *__restrict__ dY, int E,
                                                            const int *__restrict__ meta,
                                                            const uint32_t *__restrict__ keys,
                                                            const uint32_t *__restrict__ vals, float *__restrict__ S,
-                                                           float *__restrict__ Pfirst, float *__restrict__ Plast) {
+                                                           float *__restrict__ Pfirst, float *__restrict__ Plast,
+                                                           int *__restrict__ headpos) {
     __shared__ uint32_t sv[kEmbedItem];
-    __shared__ int run_end[kEmbedItem];     // 1 if position j closes its run
-    __shared__ float *dst_s[kEmbedItem];     // destination row of the run closed at j
+    __shared__ int run_end[kEmbedItem];
+    __shared__ int dst_kind[kEmbedItem];    // destination of the run closed at j: 0 S, 1 Pfirst, 2 Plast
+    __shared__ int64_t dst_off[kEmbedItem]; // row offset (floats) in that buffer
     const int nv = meta[0];
     const int c = blockIdx.x;
     const int p0 = c * kEmbedItem;
@@ -296,6 +314,7 @@ __global__ __launch_bounds__(256) void embed_segsum_kernel(const float *__restri
         const int j = threadIdx.x;
         const uint32_t k = keys[p0 + j];
         sv[j] = vals[p0 + j];
+        if (p0 + j == 0 || keys[p0 + j - 1] != k) headpos[k] = p0 + j;
         const bool end = j == len - 1 || keys[p0 + j + 1] != k;
         run_end[j] = end;
         if (end) {
@@ -303,24 +322,52 @@ __global__ __launch_bounds__(256) void embed_segsum_kernel(const float *__restri
             while (r0 > 0 && keys[p0 + r0 - 1] == k) --r0;
             const bool cut_front = r0 == 0 && p0 > 0 && keys[p0 - 1] == k;
             const bool cut_back = j == len - 1 && p1 < nv && keys[p1] == k;
-            dst_s[j] = cut_front ? Pfirst + int64_t(c) * E
-                                 : (cut_back ? Plast + int64_t(c) * E : S + int64_t(p0 + r0) * E);
+            dst_kind[j] = cut_front ? 1 : (cut_back ? 2 : 0);
+            dst_off[j] = (cut_front || cut_back) ? int64_t(c) * E : int64_t(p0 + r0) * E;
         }
     }
     __syncthreads();
-    for (int col = threadIdx.x; col < E; col += blockDim.x) {
-        float x[kEmbedItem];
+    auto dst_row = [&](int j) -> float * {
+        const int kd = dst_kind[j];
+        return (kd == 0 ? S : (kd == 1 ? Pfirst : Plast)) + dst_off[j];
+    };
+    if ((E & 3) == 0 && (reinterpret_cast<uintptr_t>(dY) & 15) == 0) {
+        const int E4 = E >> 2;
+        for (int col = threadIdx.x; col < E4; col += blockDim.x) {
+            float4 x[kEmbedItem];
 #pragma unroll
-        for (int j = 0; j < kEmbedItem; ++j) x[j] = j < len ? dY[int64_t(sv[j]) * E + col] : 0.f;
-        __builtin_amdgcn_sched_barrier(0);
-        float acc = 0.f;
+            for (int j = 0; j < kEmbedItem; ++j)
+                x[j] = j < len ? reinterpret_cast<const float4 *>(dY + int64_t(sv[j]) * E)[col]
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+            float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int j = 0; j < kEmbedItem; ++j) {
-            if (j < len) {
-                acc += x[j];
-                if (run_end[j]) {
-                    dst_s[j][col] = acc;
-                    acc = 0.f;
+            for (int j = 0; j < kEmbedItem; ++j) {
+                if (j < len) {
+                    acc.x += x[j].x;
+                    acc.y += x[j].y;
+                    acc.z += x[j].z;
+                    acc.w += x[j].w;
+                    if (run_end[j]) {
+                        reinterpret_cast<float4 *>(dst_row(j))[col] = acc;
+                        acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                    }
+                }
+            }
+        }
+    } else {
+        for (int col = threadIdx.x; col < E; col += blockDim.x) {
+            float x[kEmbedItem];
+#pragma unroll
+            for (int j = 0; j < kEmbedItem; ++j) x[j] = j < len ? dY[int64_t(sv[j]) * E + col] : 0.f;
+            float acc = 0.f;
+#pragma unroll
+            for (int j = 0; j < kEmbedItem; ++j) {
+                if (j < len) {
+                    acc += x[j];
+                    if (run_end[j]) {
+                        dst_row(j)[col] = acc;
+                        acc = 0.f;
+                    }
                 }
             }
         }
@@ -328,15 +375,15 @@ __global__ __launch_bounds__(256) void embed_segsum_kernel(const float *__restri
 }
 
 // A segment that starts in chunk c and runs past its end: S[head] =
-// Plast[c] + Pfirst[c+1] + ... + Pfirst[cend-1].  The four waves each sum a
-// fixed quarter of that list (four interleaved partial sums each); the
-// quarters are then added in order.
+// Plast[c] + Pfirst[c+1] + ... + Pfirst[cend-1].  Workgroup (c, column
+// block) of 64 columns x 4 groups: group g sums a fixed quarter of that list
+// in order (eight loads in flight), then the quarters are added in order.
 __global__ __launch_bounds__(256) void embed_segfix_kernel(int E, const int *__restrict__ meta,
                                                            const uint32_t *__restrict__ keys,
                                                            const float *__restrict__ Pfirst,
                                                            const float *__restrict__ Plast, float *__restrict__ S) {
-    extern __shared__ float part_s[];   // [4][E]
     __shared__ int info[2];
+    __shared__ float red[4][64];
     const int nv = meta[0];
     const int c = blockIdx.x;
     const int p0 = c * kEmbedItem, p1 = min(nv, p0 + kEmbedItem);
@@ -344,7 +391,6 @@ __global__ __launch_bounds__(256) void embed_segfix_kernel(int E, const int *__r
     const uint32_t k = keys[p1 - 1];
     if (keys[p1] != k) return;                              // the last run ends inside the chunk
     if (threadIdx.x < 64) {
-        // head of the last run, and the end of its segment
         const int head = wave_lower_bound(keys, p0 > 0 ? p0 - 1 : 0, p1, k);
         const int pend = wave_lower_bound(keys, p1, nv, k + 1);
         if (threadIdx.x == 0) {
@@ -356,287 +402,376 @@ __global__ __launch_bounds__(256) void embed_segfix_kernel(int E, const int *__r
     const int head = info[0];
     if (head < 0) return;
     const int cnt = info[1] - c;           // Plast[c] then Pfirst[c+1 .. cend-1]
-    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int i0 = int(int64_t(w) * cnt / 4), i1 = int(int64_t(w + 1) * cnt / 4);
-    for (int col = lane; col < E; col += 64) {
-        float acc[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int i = i0; i < i1; i += 4) {
-            float x[4];
+    const int g = threadIdx.x >> 6, lc = threadIdx.x & 63;
+    const int col = blockIdx.y * 64 + lc;
+    const int colc = min(col, E - 1);
+    const int i0 = int(int64_t(g) * cnt / 4), i1 = int(int64_t(g + 1) * cnt / 4);
+    float acc = 0.f;
+    for (int i = i0; i < i1; i += 8) {
+        float x[8];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int ii = min(i + u, i1 - 1);
-                x[u] = ii == 0 ? Plast[int64_t(c) * E + col] : Pfirst[int64_t(c + ii) * E + col];
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-                if (i + u < i1) acc[u] += x[u];
+        for (int u = 0; u < 8; ++u) {
+            const int ii = min(i + u, i1 - 1);
+            x[u] = ii == 0 ? Plast[int64_t(c) * E + colc] : Pfirst[int64_t(c + ii) * E + colc];
         }
-        part_s[w * E + col] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (i + u < i1) acc += x[u];
     }
+    red[g][lc] = acc;
     __syncthreads();
-    for (int col = threadIdx.x; col < E; col += blockDim.x)
-        S[int64_t(head) * E + col] = ((part_s[col] + part_s[E + col]) + part_s[2 * E + col]) + part_s[3 * E + col];
+    if (g == 0 && col < E) S[int64_t(head) * E + col] = ((red[0][lc] + red[1][lc]) + red[2][lc]) + red[3][lc];
 }
 
-// ---------------------------------------------------------------- dG_last
-// One wave per (vs, chunk c): it walks the segment heads among sorted
-// positions [c nv / chunks, (c + 1) nv / chunks) in order, keeps those whose
-// id ends in digit vs, stages each head's prefix block A[vp] and row S in its
-// own LDS region, and accumulates A[vp]^T S into registers (lane a holds
-// dG_last[a, vs, :]).  Every (chunk, vs) slot of `part` is written by exactly
-// one wave; the chunk partials are summed in chunk order afterwards.
-__device__ __forceinline__ void wave_sync_lds() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-__device__ __forceinline__ void wave_copy(float *dst, const float *__restrict__ src, int count) {
-    const int lane = threadIdx.x & 63;
-    if ((reinterpret_cast<uintptr_t>(src) & 15) == 0 && (count & 3) == 0) {
-        const float4 *s4 = reinterpret_cast<const float4 *>(src);
-        float4 *d4 = reinterpret_cast<float4 *>(dst);
-        const int n4 = count / 4;
-        for (int i0 = 0; i0 < n4; i0 += 64 * 8) {
-            float4 r[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int i = i0 + u * 64 + lane;
-                r[u] = s4[min(i, n4 - 1)];
-            }
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int i = i0 + u * 64 + lane;
-                if (i < n4) d4[i] = r[u];
-            }
-        }
-    } else {
-        for (int i = lane; i < count; i += 64) dst[i] = src[i];
-    }
-}
-
-__global__ __launch_bounds__(256) void embed_dglast_kernel(const int *__restrict__ meta,
-                                                           const uint32_t *__restrict__ keys,
-                                                           const float *__restrict__ S,
-                                                           const float *__restrict__ Apre, int Ep, int R, int Vs,
-                                                           int Es, int chunks, float *__restrict__ part) {
-    extern __shared__ float lds[];
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int E = Ep * Es;
-    float *sa = lds + w * (E + Ep * R);      // [Ep][R]
-    float *ss = sa + Ep * R;                  // [Ep][Es]
-    const int64_t wid = int64_t(blockIdx.x) * 4 + w;
-    if (wid >= int64_t(Vs) * chunks) return;
-    const int vs = int(wid % Vs), c = int(wid / Vs);
-    const int nv = meta[0];
-    const int q0 = int(int64_t(c) * nv / chunks), q1 = int(int64_t(c + 1) * nv / chunks);
-    const int64_t tot = int64_t(R) * Vs * Es;
-    const int la = min(lane, R - 1);
-    for (int e0 = 0; e0 < Es; e0 += kMaxEs) {
-        const int ne = min(kMaxEs, Es - e0);
-        float acc[kMaxEs];
-#pragma unroll
-        for (int j = 0; j < kMaxEs; ++j) acc[j] = 0.f;
-        for (int base = q0; base < q1; base += 64) {
-            const int p = base + lane;
-            bool take = false;
-            if (p < q1) {
-                const uint32_t kk = keys[p];
-                take = (p == 0 || keys[p - 1] != kk) && int(kk % uint32_t(Vs)) == vs;
-            }
-            uint64_t m = __ballot(take);
-            while (m) {
-                const int h = __builtin_ctzll(m);
-                m &= m - 1;
-                const int hp = base + h;
-                const int64_t vp = keys[hp] / uint32_t(Vs);
-                wave_sync_lds();
-                if (Apre) wave_copy(sa, Apre + vp * Ep * R, Ep * R);
-                else if (lane == 0) sa[0] = 1.f;
-                wave_copy(ss, S + int64_t(hp) * E, E);
-                wave_sync_lds();
-                for (int ep = 0; ep < Ep; ++ep) {
-                    const float av = sa[ep * R + la];
-                    const float *sr = ss + ep * Es + e0;
-#pragma unroll
-                    for (int j = 0; j < kMaxEs; ++j) acc[j] += av * sr[min(j, ne - 1)];
-                }
-            }
-        }
-        if (lane < R) {
-            float *dst = part + int64_t(c) * tot + (int64_t(lane) * Vs + vs) * Es + e0;
-#pragma unroll
-            for (int j = 0; j < kMaxEs; ++j)
-                if (j < ne) dst[j] = acc[j];
-        }
-    }
-}
-
-// ---------------------------------------------------------------- dA
-// One wave per prefix vp: the ids of vp sit between two wave searches in the
-// sorted keys; lane ep accumulates dA[vp, ep, :] (RMAX registers, RMAX >= r)
-// over the segment heads in order, S[ep, :] by vector loads and
-// G_last[:, vs, :] by scalar loads.  dA is written blocked for the
-// projections onto the prefix cores.
-template <int RMAX>
-__global__ __launch_bounds__(256) void embed_dapre_kernel(const int *__restrict__ meta,
-                                                          const uint32_t *__restrict__ keys,
+// ---------------------------------------------------------------- per prefix
+// dA: one workgroup per prefix vp; its ids (at most Vs) come from headpos[],
+// in id order.  For a batch of ids the S rows and G_last slices are staged
+// in LDS; wave w and lane (q, g) = (lane % 16, lane / 16) accumulate
+// dA[vp, ep, a] for ep = q + 16 w + 64 e and a = g + 4 i in registers:
+//   dA[vp, ep, a] = sum_u sum_es S_u[ep, es] G_last[a, vs_u, es]
+// Prefixes without ids exit at once (dA was cleared before the sort).
+template <int NJ4>
+__global__ __launch_bounds__(256) void embed_dapre_kernel(const int *__restrict__ headpos,
                                                           const float *__restrict__ S, const float *__restrict__ Gs,
-                                                          int64_t Vp, int Ep, int R, int Vs, int Es, int vq, int eq,
+                                                          int Ep, int R, int Vs, int Es, int vq, int eq, int nbmax,
                                                           float *__restrict__ dA) {
-    extern __shared__ float gs_s[];   // [R][Vs][Es]
-    stage_to_lds(gs_s, Gs, R * Vs * Es);
-    __syncthreads();
-    const int lane = threadIdx.x & 63;
-    const int64_t vp = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
-    if (vp >= Vp) return;
-    const int nv = meta[0];
-    const int pb = wave_lower_bound(keys, 0, nv, uint32_t(vp * Vs));
-    const int pe = wave_lower_bound(keys, pb, nv, uint32_t((vp + 1) * Vs));
+    constexpr int ES4 = 4 * NJ4;
+    extern __shared__ __attribute__((aligned(16))) float lds[];
+    __shared__ int nid;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int vp = blockIdx.x;
     const int E = Ep * Es;
-    const int64_t NEq = Ep / eq;
-    for (int ep0 = 0; ep0 < Ep; ep0 += 64) {
-        const int ep = ep0 + lane;
-        const int epc = min(ep, Ep - 1);
-        float acc[RMAX];
+    float *G_s = lds;                                    // [nbmax][R][ES4]
+    float *S_s = G_s + nbmax * R * ES4;                  // [nbmax][Ep][ES4]
+    int *idl = reinterpret_cast<int *>(S_s + nbmax * Ep * ES4);   // [Vs] ids, then [Vs] heads
+    int *hpl = idl + Vs;
+    if (tid < 64) {
+        int cnt = 0;
+        for (int j0 = 0; j0 < Vs; j0 += 64) {
+            const int j = j0 + lane;
+            const int hp = j < Vs ? headpos[int64_t(vp) * Vs + j] : -1;
+            const uint64_t m = __ballot(hp >= 0);
+            if (hp >= 0) {
+                const int slot = cnt + __popcll(m & lanemask_lt());
+                idl[slot] = j;
+                hpl[slot] = hp;
+            }
+            cnt += __popcll(m);
+        }
+        if (lane == 0) nid = cnt;
+    }
+    __syncthreads();
+    const int ni = nid;
+    if (ni == 0) return;
+    const int q = lane & 15, g = lane >> 4;
+    float acc[2][16];
 #pragma unroll
-        for (int a = 0; a < RMAX; ++a) acc[a] = 0.f;
-        for (int base = pb; base < pe; base += 64) {
-            const int p = base + lane;
-            const bool head = p < pe && (p == 0 || keys[p - 1] != keys[p]);
-            uint64_t m = __ballot(head);
-            while (m) {
-                const int h = __builtin_ctzll(m);
-                m &= m - 1;
-                const int hp = base + h;
-                const int vs = int(keys[hp] % uint32_t(Vs));
-                const float *sr = S + int64_t(hp) * E + int64_t(epc) * Es;
-                for (int e0 = 0; e0 < Es; e0 += kMaxEs) {
-                    const int ne = min(kMaxEs, Es - e0);
-                    float sv[kMaxEs];
+    for (int e = 0; e < 2; ++e)
 #pragma unroll
-                    for (int j = 0; j < kMaxEs; ++j) sv[j] = j < ne ? sr[e0 + min(j, ne - 1)] : 0.f;
-                    __builtin_amdgcn_sched_barrier(0);
+        for (int i = 0; i < 16; ++i) acc[e][i] = 0.f;
+    for (int b0 = 0; b0 < ni; b0 += nbmax) {
+        const int nb = min(nbmax, ni - b0);
+        stage_lds<8>(G_s, nb * R * ES4, tid, 256, [&](int i) {
+            const int u = i / (R * ES4), r = i - u * (R * ES4);
+            const int a = r / ES4, es = r - a * ES4;
+            return es < Es ? Gs[(int64_t(a) * Vs + idl[b0 + u]) * Es + es] : 0.f;
+        });
+        stage_lds<8>(S_s, nb * Ep * ES4, tid, 256, [&](int i) {
+            const int u = i / (Ep * ES4), r = i - u * (Ep * ES4);
+            const int ep = r / ES4, es = r - ep * ES4;
+            return es < Es ? S[int64_t(hpl[b0 + u]) * E + ep * Es + es] : 0.f;
+        });
+        __syncthreads();
+        for (int u = 0; u < nb; ++u) {
+            const float *gu = G_s + u * R * ES4;
+            const float *su = S_s + u * Ep * ES4;
 #pragma unroll
-                    for (int a = 0; a < RMAX; ++a) {
-                        const float *g = gs_s + (min(a, R - 1) * Vs + vs) * Es + e0;
-                        float v = 0.f;
+            for (int e = 0; e < 2; ++e) {
+                const int ep = q + 16 * wave + 64 * e;
+                if (ep >= Ep) continue;
+                float4 s4[NJ4];
 #pragma unroll
-                        for (int j = 0; j < kMaxEs; ++j) v += sv[j] * g[min(j, ne - 1)];
-                        acc[a] += v;
+                for (int j4 = 0; j4 < NJ4; ++j4) s4[j4] = *reinterpret_cast<const float4 *>(su + ep * ES4 + 4 * j4);
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int a = g + 4 * i;
+                    if (a < R) {
+                        float t = 0.f;
+#pragma unroll
+                        for (int j4 = 0; j4 < NJ4; ++j4) {
+                            const float4 g4 = *reinterpret_cast<const float4 *>(gu + a * ES4 + 4 * j4);
+                            t += s4[j4].x * g4.x;
+                            t += s4[j4].y * g4.y;
+                            t += s4[j4].z * g4.z;
+                            t += s4[j4].w * g4.w;
+                        }
+                        acc[e][i] += t;
                     }
                 }
             }
         }
-        if (ep < Ep) {
-            const int64_t Vh = vp / vq, x = vp % vq, Eh = ep / eq, y = ep % eq;
-            float *dst = dA + (((Vh * NEq + Eh) * vq + x) * eq + y) * R;
+        __syncthreads();
+    }
+    // dA[vp] written blocked for the prefix-core projections
+    const int Vh = vp / vq, x = vp - Vh * vq;
+    const int NEq = Ep / eq;
 #pragma unroll
-            for (int a = 0; a < RMAX; ++a)
-                if (a < R) dst[a] = acc[a];
+    for (int e = 0; e < 2; ++e) {
+        const int ep = q + 16 * wave + 64 * e;
+        if (ep >= Ep) continue;
+        const int Eh = ep / eq, y = ep - Eh * eq;
+        float *dst = dA + (((int64_t(Vh) * NEq + Eh) * vq + x) * eq + y) * R;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int a = g + 4 * i;
+            if (a < R) dst[a] = acc[e][i];
         }
     }
 }
 
-}  // namespace
-
-bool embed_kernels_support(int Ep, int R, int Es, int64_t E) {
-    const int64_t gs = int64_t(R) * 32 * Es;   // upper bound check done at launch with the real Vs
-    (void)gs;
-    return R <= 64 && E * 4 * int64_t(sizeof(float)) <= 64 * 1024 &&
-           4 * (E + int64_t(Ep) * R) * int64_t(sizeof(float)) <= 64 * 1024;
+// dG_last: workgroup (vs, chunk) sums, over the ids vp Vs + vs with vp in
+// [kGlVp chunk, kGlVp (chunk + 1)) in vp order,
+//   part[chunk][a][vs][es] = sum_u sum_ep A[vp_u, ep, a] S_u[ep, es]
+// with A blocks (ranks padded to R4 = 4 ceil(R / 4)) and S rows of a batch
+// of ids staged in LDS.  Thread item (a quad, es quad, ep eighth) keeps a
+// 4 x 4 block of sums; the eight ep parts are added in order at the end.
+// The expand kernel adds the chunk partials in order.
+template <int NJ4>
+__global__ __launch_bounds__(256) void embed_dglast_kernel(const int *__restrict__ headpos,
+                                                           const float *__restrict__ S,
+                                                           const float *__restrict__ Apre, int sE, int sR, int64_t Vp,
+                                                           int Ep, int R, int Vs, int Es, int nbmax,
+                                                           float *__restrict__ part) {
+    constexpr int ES4 = 4 * NJ4;
+    extern __shared__ __attribute__((aligned(16))) float lds[];
+    __shared__ int vpl[kGlVp], hpl[kGlVp];
+    __shared__ int nid;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int vs = blockIdx.x, chunk = blockIdx.y;
+    const int E = Ep * Es;
+    const int R4 = (R + 3) & ~3, na4 = R4 / 4;
+    float *A_s = lds;                                  // [nbmax][Ep][R4]
+    float *S_s = A_s + nbmax * Ep * R4;                // [nbmax][Ep][ES4]
+    float *red = S_s + nbmax * Ep * ES4;               // [8][R4][ES4] ep-part sums
+    if (tid < 64) {
+        const int64_t vp = int64_t(chunk) * kGlVp + lane;
+        const int hp = (lane < kGlVp && vp < Vp) ? headpos[vp * Vs + vs] : -1;
+        const uint64_t m = __ballot(hp >= 0);
+        if (hp >= 0) {
+            const int slot = __popcll(m & lanemask_lt());
+            vpl[slot] = int(vp);
+            hpl[slot] = hp;
+        }
+        if (lane == 0) nid = __popcll(m);
+    }
+    __syncthreads();
+    const int ni = nid;
+    const int items = na4 * NJ4 * 8;                    // (a quad, es quad, ep eighth)
+    const bool act = tid < items;
+    const int pe = tid & 7, rest = tid >> 3;
+    const int aq = act ? rest / NJ4 : 0, jq = act ? rest - (rest / NJ4) * NJ4 : 0;
+    const int ept = (Ep + 7) / 8;
+    const int ep0 = pe * ept, ep1 = min(Ep, ep0 + ept);
+    float acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+    for (int b0 = 0; b0 < ni; b0 += nbmax) {
+        const int nb = min(nbmax, ni - b0);
+        stage_lds<8>(A_s, nb * Ep * R4, tid, 256, [&](int i) {
+            const int u = i / (Ep * R4), r = i - u * (Ep * R4);
+            const int ep = r / R4, a = r - ep * R4;
+            return a < R ? (Apre ? Apre[int64_t(vpl[b0 + u]) * Ep * R + int64_t(ep) * sE + int64_t(a) * sR] : 1.f)
+                         : 0.f;
+        });
+        stage_lds<8>(S_s, nb * Ep * ES4, tid, 256, [&](int i) {
+            const int u = i / (Ep * ES4), r = i - u * (Ep * ES4);
+            const int ep = r / ES4, es = r - ep * ES4;
+            return es < Es ? S[int64_t(hpl[b0 + u]) * E + ep * Es + es] : 0.f;
+        });
+        __syncthreads();
+        if (act)
+            for (int u = 0; u < nb; ++u) {
+                const float *au = A_s + u * Ep * R4 + 4 * aq;
+                const float *su = S_s + u * Ep * ES4 + 4 * jq;
+                for (int ep = ep0; ep < ep1; ++ep) {
+                    const float4 a4 = *reinterpret_cast<const float4 *>(au + ep * R4);
+                    const float4 s4 = *reinterpret_cast<const float4 *>(su + ep * ES4);
+                    const float av[4] = {a4.x, a4.y, a4.z, a4.w};
+                    const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) acc[i][j] += av[i] * sv[j];
+                }
+            }
+        __syncthreads();
+    }
+    if (act)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) red[(pe * R4 + 4 * aq + i) * ES4 + 4 * jq + j] = acc[i][j];
+    __syncthreads();
+    float *dst = part + int64_t(chunk) * R * Vs * Es;
+    for (int o = tid; o < R * Es; o += 256) {
+        const int a = o / Es, es = o - a * Es;
+        float v = red[(0 * R4 + a) * ES4 + es];
+#pragma unroll
+        for (int p = 1; p < 8; ++p) v += red[(p * R4 + a) * ES4 + es];
+        dst[(int64_t(a) * Vs + vs) * Es + es] = v;
+    }
 }
 
-bool embed_gs_fits(int R, int Vs, int Es) { return int64_t(R) * Vs * Es * int64_t(sizeof(float)) <= 64 * 1024; }
+// d = 1: the table is the core itself; dG_0[0, v, e, 0] = S[headpos[v]][e].
+__global__ __launch_bounds__(256) void embed_gather_kernel(const int *__restrict__ headpos,
+                                                           const float *__restrict__ S, int64_t V, int E,
+                                                           float *__restrict__ dG0) {
+    const int64_t total = V * E;
+    for (int64_t o = int64_t(blockIdx.x) * 256 + threadIdx.x; o < total; o += int64_t(gridDim.x) * 256) {
+        const int64_t v = o / E;
+        const int e = int(o - v * E);
+        const int hp = headpos[v];
+        dG0[o] = hp >= 0 ? S[int64_t(hp) * E + e] : 0.f;
+    }
+}
 
-int launch_embed_rows(const int64_t *ids, int64_t n, int64_t V, const float *Apre, const float *Gs, float *Y, int Ep,
-                      int R, int Vs, int Es, int *err_flag, void *stream) {
+int es4_of(int Es) { return 4 * ((Es + 3) / 4); }
+
+// ids staged per batch so that the LDS use stays within kEmbLds (0: too large)
+int dapre_batch(int Ep, int R, int Vs, int Es) {
+    const size_t per = sizeof(float) * size_t(R + Ep) * es4_of(Es);
+    const size_t fixed = 2 * sizeof(int) * size_t(Vs);
+    if (fixed + per > kEmbLds) return 0;
+    return int(std::min<size_t>(8, (kEmbLds - fixed) / per));
+}
+size_t dapre_lds_bytes(int Ep, int R, int Vs, int Es, int nb) {
+    return sizeof(float) * size_t(nb) * (R + Ep) * es4_of(Es) + 2 * sizeof(int) * size_t(Vs);
+}
+
+int dglast_batch(int Ep, int R, int Es) {
+    const int R4 = (R + 3) & ~3;
+    const size_t per = sizeof(float) * size_t(Ep) * (R4 + es4_of(Es));
+    const size_t fixed = sizeof(float) * size_t(8) * R4 * es4_of(Es);
+    if (fixed + per > kEmbLds) return 0;
+    return int(std::min<size_t>(kGlVp, (kEmbLds - fixed) / per));
+}
+size_t dglast_lds_bytes(int Ep, int R, int Es, int nb) {
+    const int R4 = (R + 3) & ~3;
+    return sizeof(float) * (size_t(nb) * Ep * (R4 + es4_of(Es)) + size_t(8) * R4 * es4_of(Es));
+}
+
+const uint32_t *sorted_vals(const EmbedWs &w, int passes) { return (passes & 1) ? w.valsA : w.valsB; }
+
+}  // namespace
+
+bool embed_kernels_support(int64_t Ep, int R, int Vs, int Es, int d) {
+    if (R < 1 || R > 64 || Es < 1 || Es > kMaxEs) return false;
+    if (d == 1) return true;
+    // dG_last items (a quad, es quad, ep eighth) must fit one workgroup
+    return Ep <= 128 && Vs <= 1024 && dapre_batch(int(Ep), R, Vs, Es) > 0 && dglast_batch(int(Ep), R, Es) > 0 &&
+           ((R + 3) / 4) * ((Es + 3) / 4) * 8 <= 256;
+}
+
+template <int RM>
+void launch_rows_nj(int nj4, dim3 grid, void *stream, const int64_t *ids, int64_t n, int64_t V, const float *Apre,
+                    const float *Gs, float *Y, int Ep, int R, int Vs, int Es, int sE, int sR, int *err_flag) {
+    switch (nj4) {
+        case 1: hipLaunchKernelGGL((embed_rows_kernel<RM, 1>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
+        case 2: hipLaunchKernelGGL((embed_rows_kernel<RM, 2>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
+        case 3: hipLaunchKernelGGL((embed_rows_kernel<RM, 3>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
+        default: hipLaunchKernelGGL((embed_rows_kernel<RM, 4>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
+    }
+}
+
+int launch_embed_rows(const int64_t *ids, int64_t n, int64_t V, const float *Apre, bool rank_major, const float *Gs,
+                      float *Y, int Ep, int R, int Vs, int Es, int *err_flag, void *stream) {
     if (n <= 0) return 0;
-    const int64_t groups = (n + 3) / 4;
-    const int grid = int(std::min<int64_t>(groups, 512));
-    const size_t lds = sizeof(float) * size_t(R) * Vs * Es;
-#define COMERA_ROWS(RM)                                                                                       \
-    hipLaunchKernelGGL((embed_rows_kernel<RM>), dim3(grid), dim3(256), lds, hipStream_t(stream), ids, n, V, Apre, \
-                       Gs, Y, Ep, R, Vs, Es, err_flag)
-    if (R <= 8) COMERA_ROWS(8);
-    else if (R <= 16) COMERA_ROWS(16);
-    else if (R <= 32) COMERA_ROWS(32);
-    else COMERA_ROWS(64);
-#undef COMERA_ROWS
+    const dim3 grid(unsigned((n + 3) / 4));
+    const int nj4 = (Es + 3) / 4;
+    const int sE = rank_major ? 1 : R, sR = rank_major ? Ep : 1;
+    if (R <= 8) launch_rows_nj<8>(nj4, grid, stream, ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag);
+    else if (R <= 16) launch_rows_nj<16>(nj4, grid, stream, ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag);
+    else if (R <= 32) launch_rows_nj<32>(nj4, grid, stream, ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag);
+    else launch_rows_nj<64>(nj4, grid, stream, ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag);
     return int(hipGetLastError());
 }
 
-const uint32_t *sorted_keys(const EmbedWs &w, int64_t V) {
-    int bits = 0;
-    while ((int64_t(1) << bits) <= V) ++bits;
-    const int passes = (bits + 7) / 8;
-    return (passes & 1) ? w.keysA : w.keysB;
-}
-const uint32_t *sorted_vals(const EmbedWs &w, int64_t V) {
-    int bits = 0;
-    while ((int64_t(1) << bits) <= V) ++bits;
-    const int passes = (bits + 7) / 8;
-    return (passes & 1) ? w.valsA : w.valsB;
-}
+const uint32_t *embed_sorted_keys(const EmbedWs &w, int passes) { return (passes & 1) ? w.keysA : w.keysB; }
 
-int launch_embed_sort(const int64_t *ids, int n, int64_t V, const EmbedWs &w, int *err_flag, void *stream) {
-    int bits = 0;
-    while ((int64_t(1) << bits) <= V) ++bits;  // keys 0..V inclusive (V marks an out-of-range id)
+int launch_embed_sort(const int64_t *ids, int n, int64_t V, int passes, const EmbedWs &w, int *err_flag,
+                      int64_t nclear, float *zero, int64_t nzero, void *stream) {
     const int nblk = (n + kBlk - 1) / kBlk;
+    int *bad = w.hist + 256 * nblk;
     const uint32_t *kin = nullptr, *vin = nullptr;
     uint32_t *kout = w.keysA, *vout = w.valsA;
-    for (int shift = 0, pass = 0; shift < bits; shift += 8, ++pass) {
-        hipLaunchKernelGGL(radix_hist_kernel, dim3(nblk), dim3(256), 0, hipStream_t(stream), ids, kin, n, V, shift,
-                           nblk, w.hist, pass == 0 ? err_flag : nullptr);
-        hipLaunchKernelGGL(radix_scan_kernel, dim3(1), dim3(1024), 0, hipStream_t(stream), w.hist, 256 * nblk);
+    for (int p = 0; p < passes; ++p) {
+        // pass 0 also clears the buffers, counts out-of-range ids and sets meta[0]
+        const int nclr = p == 0 ? int(std::min<int64_t>(2048, std::max<int64_t>(1, (nclear + nzero + 4095) / 4096))) : 0;
+        hipLaunchKernelGGL(radix_hist_kernel, dim3(nblk + nclr), dim3(256), 0, hipStream_t(stream), ids, kin, n, V,
+                           8 * p, nblk, w.hist, p == 0 ? bad : nullptr, err_flag, w.headpos, p == 0 ? nclear : 0,
+                           zero, p == 0 ? nzero : 0);
+        hipLaunchKernelGGL(radix_scan_kernel, dim3(1), dim3(1024), 0, hipStream_t(stream), w.hist, nblk,
+                           p == 0 ? bad : nullptr, n, w.meta);
         hipLaunchKernelGGL(radix_scatter_kernel, dim3(nblk), dim3(256), 0, hipStream_t(stream), ids, kin, vin, n, V,
-                           shift, nblk, w.hist, kout, vout);
-        if (int e = int(hipGetLastError())) return e;
+                           8 * p, nblk, w.hist, kout, vout);
         kin = kout;
         vin = vout;
         kout = (kout == w.keysA) ? w.keysB : w.keysA;
         vout = (vout == w.valsA) ? w.valsB : w.valsA;
     }
-    hipLaunchKernelGGL(nvalid_kernel, dim3(1), dim3(64), 0, hipStream_t(stream), sorted_keys(w, V), n, V, w.meta);
     return int(hipGetLastError());
 }
 
-int launch_embed_segsum(const float *dY, int E, int n, int64_t V, const EmbedWs &w, void *stream) {
+int launch_embed_segsum(const float *dY, int E, int n, int passes, const EmbedWs &w, void *stream) {
     const int chunks = (n + kEmbedItem - 1) / kEmbedItem;
-    const uint32_t *keys = sorted_keys(w, V), *vals = sorted_vals(w, V);
+    const uint32_t *keys = embed_sorted_keys(w, passes), *vals = sorted_vals(w, passes);
     hipLaunchKernelGGL(embed_segsum_kernel, dim3(chunks), dim3(256), 0, hipStream_t(stream), dY, E, w.meta, keys, vals,
-                       w.S, w.Pfirst, w.Plast);
+                       w.S, w.Pfirst, w.Plast, w.headpos);
     if (int e = int(hipGetLastError())) return e;
-    hipLaunchKernelGGL(embed_segfix_kernel, dim3(chunks), dim3(256), sizeof(float) * 4 * size_t(E),
-                       hipStream_t(stream), E, w.meta, keys, w.Pfirst, w.Plast, w.S);
+    hipLaunchKernelGGL(embed_segfix_kernel, dim3(chunks, unsigned((E + 63) / 64)), dim3(256), 0, hipStream_t(stream),
+                       E, w.meta, keys, w.Pfirst, w.Plast, w.S);
     return int(hipGetLastError());
 }
 
-int launch_embed_dglast(const EmbedWs &w, int n, int64_t V, const float *Apre, int Ep, int R, int Vs, int Es,
-                        void *stream) {
-    (void)n;
-    const int64_t waves = int64_t(Vs) * kEmbedChunks;
-    const size_t lds = sizeof(float) * 4 * size_t(Ep * Es + Ep * R);
-    hipLaunchKernelGGL(embed_dglast_kernel, dim3(unsigned((waves + 3) / 4)), dim3(256), lds, hipStream_t(stream), w.meta,
-                       sorted_keys(w, V), w.S, Apre, Ep, R, Vs, Es, kEmbedChunks, w.dglast_part);
+int launch_embed_dapre(const EmbedWs &w, const float *Gs, int64_t Vp, int Ep, int R, int Vs, int Es, int vq, int eq,
+                       void *stream) {
+    const int nb = dapre_batch(Ep, R, Vs, Es);
+    if (nb <= 0) return int(hipErrorInvalidValue);
+    const size_t lds = dapre_lds_bytes(Ep, R, Vs, Es, nb);
+    const dim3 grid(static_cast<unsigned>(Vp), 1, 1);
+    switch ((Es + 3) / 4) {
+        case 1: hipLaunchKernelGGL((embed_dapre_kernel<1>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
+        case 2: hipLaunchKernelGGL((embed_dapre_kernel<2>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
+        case 3: hipLaunchKernelGGL((embed_dapre_kernel<3>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
+        default: hipLaunchKernelGGL((embed_dapre_kernel<4>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
+    }
     return int(hipGetLastError());
 }
 
-int launch_embed_dapre(const EmbedWs &w, int n, int64_t V, const float *Gs, int64_t Vp, int Ep, int R, int Vs, int Es,
-                       int vq, int eq, float *dA, void *stream) {
-    (void)n;
-    const dim3 grid(unsigned((Vp + 3) / 4));
-    const uint32_t *keys = sorted_keys(w, V);
-    const size_t lds = sizeof(float) * size_t(R) * Vs * Es;
-    if (R <= 16)
-        hipLaunchKernelGGL((embed_dapre_kernel<16>), grid, dim3(256), lds, hipStream_t(stream), w.meta, keys, w.S, Gs,
-                           Vp, Ep, R, Vs, Es, vq, eq, dA);
-    else if (R <= 32)
-        hipLaunchKernelGGL((embed_dapre_kernel<32>), grid, dim3(256), lds, hipStream_t(stream), w.meta, keys, w.S, Gs,
-                           Vp, Ep, R, Vs, Es, vq, eq, dA);
-    else
-        hipLaunchKernelGGL((embed_dapre_kernel<64>), grid, dim3(256), lds, hipStream_t(stream), w.meta, keys, w.S, Gs,
-                           Vp, Ep, R, Vs, Es, vq, eq, dA);
+int embed_dglast_chunks(int64_t Vp) { return int((Vp + kGlVp - 1) / kGlVp); }
+
+int launch_embed_dglast(const EmbedWs &w, const float *Apre, bool rank_major, int64_t Vp, int Ep, int R, int Vs,
+                        int Es, void *stream) {
+    const int sE = rank_major ? 1 : R, sR = rank_major ? Ep : 1;
+    const int nb = dglast_batch(Ep, R, Es);
+    if (nb <= 0) return int(hipErrorInvalidValue);
+    const size_t lds = dglast_lds_bytes(Ep, R, Es, nb);
+    const dim3 grid(unsigned(Vs), unsigned(embed_dglast_chunks(Vp)));
+    switch ((Es + 3) / 4) {
+        case 1: hipLaunchKernelGGL((embed_dglast_kernel<1>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
+        case 2: hipLaunchKernelGGL((embed_dglast_kernel<2>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
+        case 3: hipLaunchKernelGGL((embed_dglast_kernel<3>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
+        default: hipLaunchKernelGGL((embed_dglast_kernel<4>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
+    }
+    return int(hipGetLastError());
+}
+
+int launch_embed_gather(const EmbedWs &w, int64_t V, int E, float *dG0, void *stream) {
+    const int64_t total = V * E;
+    const int grid = int(std::max<int64_t>(1, std::min<int64_t>((total + 255) / 256, 65536)));
+    hipLaunchKernelGGL(embed_gather_kernel, dim3(grid), dim3(256), 0, hipStream_t(stream), w.headpos, w.S, V, E, dG0);
     return int(hipGetLastError());
 }
 

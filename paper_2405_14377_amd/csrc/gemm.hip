@@ -709,7 +709,8 @@ int launch_gemm(const GemmArgs &g, void *stream) {
 }
 
 int chain_gemm(const float *P, const float *Gc, void *out, bool out_bf16, int64_t NI, int64_t NJ, int A, int nx,
-               int ny, int C, void *stream, bool transpose) {
+               int ny, int C, void *stream, int layout) {
+    const bool transpose = layout == kChainT;
     if (transpose && C != 1) return int(hipErrorInvalidValue);
     GemmArgs g;
     g.dtype = COMERA_F32;
@@ -729,7 +730,14 @@ int chain_gemm(const float *P, const float *Gc, void *out, bool out_bf16, int64_
     g.cmap.nd = 3;
     g.cmap.radix[1] = ny;
     g.cmap.radix[2] = C;
-    if (!transpose) {
+    if (layout == kChainRankMajor) {
+        const int64_t ncol = NJ * ny;   // length of one (J y) run
+        g.rmap.stride[0] = int64_t(nx) * C * ncol;
+        g.rmap.stride[1] = ny;
+        g.cmap.stride[0] = C * ncol;
+        g.cmap.stride[1] = 1;
+        g.cmap.stride[2] = ncol;
+    } else if (!transpose) {
         g.rmap.stride[0] = int64_t(nx) * NJ * ny * C;
         g.rmap.stride[1] = int64_t(ny) * C;
         g.cmap.stride[0] = NJ * ny * C;

@@ -2,6 +2,8 @@
 // kernel launchers.  Nothing here is part of the public ABI.
 #pragma once
 
+#include <hip/hip_runtime.h>
+
 #include <cstddef>
 #include <cstdint>
 #include <string>
@@ -194,9 +196,30 @@ int launch_gemm(const GemmArgs &g, void *stream);
 //            blocked for the next step: [(I', J')][(x', y')][a], I = I' nxp + x',
 //            J = J' nyp + y'
 //   meet:    part[s][a][(x y c)] = sum_{(I, J) in split s} P[(I, J)][a] En[(I, J)][(x y c)]
-//   chain with transpose (last core, C == 1): out[(J y)][(I x)] instead
+//   layout kChainT (last core, C == 1): out[(J y)][(I x)] instead
+//   layout kChainRankMajor: out[(I x)][c][(J y)] instead
+constexpr int kChainNormal = 0, kChainT = 1, kChainRankMajor = 2;
 int chain_gemm(const float *P, const float *Gc, void *out, bool out_bf16, int64_t NI, int64_t NJ, int A, int nx,
-               int ny, int C, void *stream, bool transpose = false);
+               int ny, int C, void *stream, int layout = kChainNormal);
+
+// Batched staging into LDS: count elements, element i = src(i), U loads in
+// flight per thread before the stores (threads t0, t0 + nt, ...).
+template <int U, class Src>
+__device__ __forceinline__ void stage_lds(float *dst, int count, int t0, int nt, Src src) {
+    for (int i0 = t0; i0 < count; i0 += nt * U) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * nt;
+            v[u] = i < count ? src(i) : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * nt;
+            if (i < count) dst[i] = v[u];
+        }
+    }
+}
 // With splits > 1 the split partials go to `scratch` (splits * NI * NJ * A
 // floats) and are summed into `out` in a fixed order.
 int adjoint_gemm(const float *En, const float *Gc, float *out, int64_t NI, int64_t NJ, int A, int nx, int ny, int C,

@@ -120,15 +120,38 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjArgs a) {
             En_s[r * pe + c] = v;
         }
     }
+    // core and left-chain slices: every thread issues its loads before its stores
     if (a.Gc)
-        for (int i = tid; i < A4 * CT4; i += kProjThreads) {
-            const int al = i / CT4, c = i - al * CT4;
-            Gc_s[al * pe + c] = (al < A && c < nc) ? a.Gc[int64_t(al) * a.cols + c0 + c] : 0.f;
+        for (int i0 = tid; i0 < A4 * CT4; i0 += kProjThreads * 4) {
+            float v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * kProjThreads;
+                const int al = i / CT4, c = i - al * CT4;
+                v[u] = (i < A4 * CT4 && al < A && c < nc) ? a.Gc[int64_t(al) * a.cols + c0 + c] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * kProjThreads;
+                const int al = i / CT4, c = i - al * CT4;
+                if (i < A4 * CT4) Gc_s[al * pe + c] = v[u];
+            }
         }
     if (a.P)
-        for (int i = tid; i < RT * A4; i += kProjThreads) {
-            const int r = i / A4, al = i - r * A4;
-            P_s[r * pp + al] = (r < nr && al < A) ? a.P[(r0 + r) * A + al] : 0.f;
+        for (int i0 = tid; i0 < RT * A4; i0 += kProjThreads * 4) {
+            float v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * kProjThreads;
+                const int r = i / A4, al = i - r * A4;
+                v[u] = (i < RT * A4 && r < nr && al < A) ? a.P[(r0 + r) * A + al] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * kProjThreads;
+                const int r = i / A4, al = i - r * A4;
+                if (i < RT * A4) P_s[r * pp + al] = v[u];
+            }
         }
     __syncthreads();
 
@@ -233,21 +256,17 @@ __global__ __launch_bounds__(256) void wbuild_kernel(WBuildArgs a) {
     const int64_t O = blockIdx.x;
     const int64_t Q0 = int64_t(blockIdx.y) * QB;
     const int nQ = int(min<int64_t>(QB, NQ - Q0));
-    for (int i = threadIdx.x; i < gsz; i += 256) {
+    stage_lds<8>(G_s, gsz, threadIdx.x, 256, [&](int i) {
         const int o = i % NO4, t = i / NO4;
         const int q = t % nq, al = t / nq;
-        float v = 0.f;
-        if (o < no) {
-            const int x = TR ? q : o, y = TR ? o : q;
-            v = a.G[(al * a.nx + x) * a.ny + y];
-        }
-        G_s[i] = v;
-    }
-    for (int i = threadIdx.x; i < nQ * A; i += 256) {
+        const int x = TR ? q : o, y = TR ? o : q;
+        return o < no ? a.G[(al * a.nx + x) * a.ny + y] : 0.f;
+    });
+    stage_lds<8>(P_s, nQ * A, threadIdx.x, 256, [&](int i) {
         const int ql = i / A, al = i - ql * A;
         const int64_t I = TR ? Q0 + ql : O, J = TR ? O : Q0 + ql;
-        P_s[i] = a.P[(I * a.NJ + J) * A + al];
-    }
+        return a.P[(I * a.NJ + J) * A + al];
+    });
     __syncthreads();
     const int64_t rowlen = NQ * nq;
     for (int item = threadIdx.x; item < nQ * nq; item += 256) {

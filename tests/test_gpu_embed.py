@@ -102,6 +102,19 @@ def test_all_tokens_one_id():
     _check(v, e, r, cores, D, ids, dY)
 
 
+@pytest.mark.parametrize("v,e,r", [((16, 32), (2, 4), (1, 3, 1)), ((8, 8, 8), (2, 3, 4), (1, 3, 5, 1))])
+def test_two_pass_sort_many_blocks(v, e, r):
+    """Vocabularies above 256 ids take two radix passes; with several
+    thousand skewed tokens the second pass sees its own per-block digit
+    counts, which differ from the first pass's."""
+    cores, D, _, _ = _problem(11, v, e, r, 8)
+    V = int(np.prod(v))
+    T = 5000
+    ids = wl.token_ids(T, V, "zipf1.1", 77)
+    dY = np.random.default_rng(12).standard_normal((T, int(np.prod(e)))).astype(np.float32)
+    _check(v, e, r, cores, D, ids, dY)
+
+
 @pytest.mark.parametrize("dist", ["zipf1.1", "uniform"])
 def test_workload_parity_and_determinism(dist):
     import torch
