@@ -281,7 +281,16 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
         g.ldb = p->N_out;
         g.rmap = remap_linear(p->N_in);
         g.cmap = remap_linear(1);
+        if (L.dx_splits > 1) {
+            g.C = at(ws, L.dx_part);
+            g.splits = L.dx_splits;
+            g.kchunk = L.dx_kchunk;
+            g.split_stride = b * p->N_in;
+        }
         e = launch_gemm(g, stream);
+        if (!e && L.dx_splits > 1)
+            e = launch_sum_splits(reinterpret_cast<const float *>(at(ws, L.dx_part)), reinterpret_cast<float *>(dX),
+                                  b * p->N_in, L.dx_splits, stream);
         timing_end(p, COMERA_KERNEL_DX, stream, ev);
         if (e) return COMERA_ERR_HIP;
     }

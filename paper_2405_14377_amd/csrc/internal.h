@@ -43,6 +43,9 @@ struct DenseLayout {
     int dw_splits;             // split-K count of dW = X^T dY
     int64_t dw_kchunk;         // tokens per split
     int meet_splits[kMaxCores];
+    int dx_splits;             // split of dX = dY W^T over N_out (1: none)
+    int64_t dx_kchunk;
+    size_t dx_part;            // split partials of dX (fp32)
     int adj_splits[kMaxCores];  // split-K of the adjoint step producing E_k
     size_t adj_part;           // shared scratch for adjoint split partials
     // fused projection route (all ranks within proj_supported): step k reads

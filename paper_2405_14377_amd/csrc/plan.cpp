@@ -168,9 +168,11 @@ void layout_dense(comera_ttm_plan_s *p) {
     L.ones = off;
     off = align_up(off + sizeof(float));
     // dW = X^T dY split over tokens so that the grid holds >= ~512 workgroups
+    // (fp32: about three 128 x 128 tiles per CU, measured best on gfx950)
     int64_t tiles = ((p->N_in + 127) / 128) * ((p->N_out + 127) / 128);
     int64_t b = std::max<int64_t>(p->batch, 1);
     int64_t splits = std::max<int64_t>(1, (512 + tiles - 1) / tiles);
+    if (p->s.act == COMERA_F32) splits = std::max<int64_t>(1, (768 + tiles / 2) / tiles);
     splits = std::min<int64_t>(splits, std::max<int64_t>(1, b / 256));
     splits = std::min<int64_t>(splits, 64);
     int64_t kchunk = (b + splits - 1) / splits;
@@ -178,6 +180,23 @@ void layout_dense(comera_ttm_plan_s *p) {
     splits = (b + kchunk - 1) / kchunk;
     L.dw_splits = int(splits);
     L.dw_kchunk = kchunk;
+    // fp32 dX = dY W^T split over N_out when the output alone gives too few
+    // 128 x 128 tiles (the partials are summed in a fixed order)
+    L.dx_splits = 1;
+    L.dx_kchunk = p->N_out;
+    if (p->s.act == COMERA_F32) {
+        const int64_t xt = ((b + 127) / 128) * ((p->N_in + 127) / 128);
+        int64_t sx = std::max<int64_t>(1, (768 + xt / 2) / xt);
+        sx = std::min<int64_t>(std::min<int64_t>(sx, 8), std::max<int64_t>(1, p->N_out / 512));
+        if (sx > 1) {
+            int64_t kc = (p->N_out + sx - 1) / sx;
+            kc = (kc + 31) / 32 * 32;
+            L.dx_splits = int((p->N_out + kc - 1) / kc);
+            L.dx_kchunk = kc;
+            L.dx_part = off;
+            off = align_up(off + sizeof(float) * size_t(L.dx_splits) * size_t(b) * size_t(p->N_in));
+        }
+    }
     L.proj = true;
     for (int k = 1; k < d; ++k) L.proj = L.proj && proj_supported(int(p->rho[k]));
     if (L.proj) {
