@@ -118,6 +118,8 @@ struct ExpandArgs {
     int d;
     int compacted;
     int swap;                       // partials are [a][n][m][c]
+    int groups[kMaxCores];          // set by launch_expand
+    int blk0[kMaxCores];            // set by launch_expand
 };
 int launch_expand(const ExpandArgs &a, void *stream);
 

@@ -29,7 +29,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kProjMaxA = 64;
 constexpr size_t kProjLds = 64 * 1024;
-constexpr int kProjThreads = 1024;  // threads per projection workgroup
+constexpr int kProjThreadsMax = 1024;  // threads per projection workgroup (large tiles)
 
 __device__ __forceinline__ int64_t remap_off(const Remap &r, int64_t idx) {
     int64_t off = 0;
@@ -51,6 +51,7 @@ __host__ __device__ inline size_t proj_lds_floats(int RT, int CT, int A) {
     return size_t(RT) * (CT4 + 4) + size_t(A4) * (CT4 + 4) + size_t(RT) * (A4 + 4) + size_t(round4(2 * RT));
 }
 
+template <int kProjThreads>
 __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjArgs a) {
     extern __shared__ __attribute__((aligned(16))) float sm[];
     const int RT = a.RT, CT = a.CT, A = a.A;
@@ -325,8 +326,9 @@ bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, bool transpose,
     const int nq = transpose ? nx : ny;
     const int no = transpose ? ny : nx;
     const size_t g = size_t(A) * nq * round4(no);
-    // about 256 output columns per workgroup (several workgroups per CU),
-    // blocks of equal size
+    // about 256 output columns per workgroup: several workgroups per CU hide
+    // the staging latency better than fewer, larger ones (measured); blocks of
+    // equal size
     int64_t qb = std::max<int64_t>(1, std::min<int64_t>(NQ, 256 / std::max(1, nq)));
     const int64_t nblk = (NQ + qb - 1) / qb;
     qb = (NQ + nblk - 1) / nblk;
@@ -356,7 +358,13 @@ int launch_proj(const ProjArgs &a, void *stream) {
     const size_t lds = proj_lds_floats(a.RT, a.CT, a.A) * sizeof(float);
     if (lds > kProjLds) return int(hipErrorInvalidValue);
     dim3 grid(unsigned((a.cols + a.CT - 1) / a.CT), unsigned((a.rows + a.RT - 1) / a.RT));
-    hipLaunchKernelGGL(proj_kernel, grid, dim3(kProjThreads), lds, hipStream_t(stream), a);
+    // 1024 threads when the tile load is large (many loads in flight per CU),
+    // else 256 (several workgroups per CU)
+    const int64_t loads4 = int64_t(a.RT) * ((a.CT + 3) / 4) * std::max(1, a.nin);
+    if (loads4 > 4096)
+        hipLaunchKernelGGL((proj_kernel<kProjThreadsMax>), grid, dim3(kProjThreadsMax), lds, hipStream_t(stream), a);
+    else
+        hipLaunchKernelGGL((proj_kernel<256>), grid, dim3(256), lds, hipStream_t(stream), a);
     return int(hipGetLastError());
 }
 

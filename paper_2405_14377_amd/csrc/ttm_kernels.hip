@@ -77,64 +77,64 @@ __global__ void fold_kernel(FoldArgs a) {
     }
 }
 
-// Workgroup of 256 threads = 32 outputs x 8 split groups: group g sums the
-// splits [g S / 8, (g + 1) S / 8) in order, then group 0 adds the eight group
-// sums in order.  The result is the same for every launch shape.
+// Workgroup of 256 threads = (256 / G) outputs x G split groups (G = 1 .. 8
+// per core, about eight splits per group): group g sums the splits
+// [g S / G, (g + 1) S / G) in order, then group 0 adds the G group sums in
+// order.  One flattened grid covers all cores (a.blk0[k] = first block of
+// core k).  The result does not depend on the launch shape other than G.
 __global__ __launch_bounds__(256) void expand_kernel(ExpandArgs a) {
-    __shared__ float red[8][33];
-    const int k = blockIdx.y;
-    if (k >= a.d || !a.dG[k]) return;
+    __shared__ float red[8][257];
+    int k = 0;
+    while (k + 1 < a.d && int(blockIdx.x) >= a.blk0[k + 1]) ++k;
+    if (!a.dG[k]) return;
+    const int G = a.groups[k], no = 256 / G;
     const int rl = a.r[k], rr = a.r[k + 1], m = a.m[k], n = a.n[k];
     const int crl = a.rc[k], crr = a.rc[k + 1];
-    const int64_t total = int64_t(rl) * m * n * rr;
+    const int tot32 = rl * m * n * rr;     // core sizes are far below 2^31 (host checks)
     const int64_t csize = int64_t(crl) * m * n * crr;
+    const int mn_ = m * n;
     const float *D = (k < a.d - 1) ? a.D[k] : nullptr;
-    const int lo = threadIdx.x & 31, g = threadIdx.x >> 5;
+    const int lo = threadIdx.x % no, g = threadIdx.x / no;
     const int S = a.splits[k];
-    const int s0 = int(int64_t(g) * S / 8), s1 = int(int64_t(g + 1) * S / 8);
+    const int s0 = int(int64_t(g) * S / G), s1 = int(int64_t(g + 1) * S / G);
     const float *part = a.part[k];
-    const int tot32 = int(total), mn_ = m * n;   // core sizes are far below 2^31 (host checks)
-    for (int base = blockIdx.x * 32; base < tot32; base += gridDim.x * 32) {
-        const int o = base + lo;
-        int ci = -1;
-        if (o < tot32) {
-            const int c = o % rr;
-            const int t = o / rr;
-            const int mn = t % mn_;
-            const int al = t / mn_;
-            int ca = al, cc = c;
-            if (a.compacted) {
-                ca = (k == 0) ? 0 : rank_bit(a.act[k], al);
-                cc = (k == a.d - 1) ? 0 : rank_bit(a.act[k + 1], c);
-            }
-            if (ca >= 0 && cc >= 0) {
-                const int jm = mn / n, in = mn % n;
-                ci = (ca * mn_ + (a.swap ? in * m + jm : mn)) * crr + cc;
-            }
+    const int o = (int(blockIdx.x) - a.blk0[k]) * no + lo;
+    int ci = -1;
+    if (o < tot32) {
+        const int c = o % rr;
+        const int t = o / rr;
+        const int mn = t % mn_;
+        const int al = t / mn_;
+        int ca = al, cc = c;
+        if (a.compacted) {
+            ca = (k == 0) ? 0 : rank_bit(a.act[k], al);
+            cc = (k == a.d - 1) ? 0 : rank_bit(a.act[k + 1], c);
         }
-        float v = 0.f;
-        if (ci >= 0) {
-            int s = s0;
-            for (; s + 8 <= s1; s += 8) {
-                float x[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) x[u] = part[(s + u) * csize + ci];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) v += x[u];
-            }
-            for (; s < s1; ++s) v += part[s * csize + ci];
+        if (ca >= 0 && cc >= 0) {
+            const int jm = mn / n, in = mn % n;
+            ci = (ca * mn_ + (a.swap ? in * m + jm : mn)) * crr + cc;
         }
-        red[g][lo] = v;
-        __syncthreads();
-        if (g == 0 && o < tot32) {
-            float t = red[0][lo];
+    }
+    float v = 0.f;
+    if (ci >= 0) {
+        int s = s0;
+        for (; s + 8 <= s1; s += 8) {
+            float x[8];
 #pragma unroll
-            for (int gg = 1; gg < 8; ++gg) t += red[gg][lo];
-            if (ci < 0) t = 0.f;
-            else if (D) t *= D[o % rr];
-            a.dG[k][o] = t;
+            for (int u = 0; u < 8; ++u) x[u] = part[(s + u) * csize + ci];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v += x[u];
         }
-        __syncthreads();
+        for (; s < s1; ++s) v += part[s * csize + ci];
+    }
+    red[g][lo] = v;
+    __syncthreads();
+    if (g == 0 && o < tot32) {
+        float t = red[0][lo];
+        for (int gg = 1; gg < G; ++gg) t += red[gg][lo];
+        if (ci < 0) t = 0.f;
+        else if (D) t *= D[o % rr];
+        a.dG[k][o] = t;
     }
 }
 
@@ -169,11 +169,20 @@ int launch_fold(const FoldArgs &a, void *stream) {
     return int(hipGetLastError());
 }
 
-int launch_expand(const ExpandArgs &a, void *stream) {
-    int64_t mx = 1;
-    for (int k = 0; k < a.d; ++k) mx = std::max<int64_t>(mx, int64_t(a.r[k]) * a.m[k] * a.n[k] * a.r[k + 1]);
-    dim3 grid(grid_for(mx, 32), a.d);
-    hipLaunchKernelGGL(expand_kernel, grid, dim3(256), 0, hipStream_t(stream), a);
+int launch_expand(const ExpandArgs &a_in, void *stream) {
+    ExpandArgs a = a_in;
+    int blocks = 0;
+    for (int k = 0; k < a.d; ++k) {
+        int G = 1;
+        while (G < 8 && G * 8 < a.splits[k]) G *= 2;
+        a.groups[k] = G;
+        a.blk0[k] = blocks;
+        const int64_t total = a.dG[k] ? int64_t(a.r[k]) * a.m[k] * a.n[k] * a.r[k + 1] : 0;
+        blocks += int((total + 256 / G - 1) / (256 / G));
+    }
+    for (int k = a.d; k < kMaxCores; ++k) a.blk0[k] = blocks;
+    if (blocks == 0) return 0;
+    hipLaunchKernelGGL(expand_kernel, dim3(unsigned(blocks)), dim3(256), 0, hipStream_t(stream), a);
     return int(hipGetLastError());
 }
 
