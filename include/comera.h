@@ -206,6 +206,11 @@ comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int
 /* Static English text for a status code. */
 const char *comera_status_string(comera_status s);
 
+/* The HIP error behind the last COMERA_ERR_HIP returned on the calling
+ * thread: its HIP name and the step that reported it ("" if none).  The
+ * text stays valid until the next failing call on the same thread. */
+const char *comera_last_hip_error(void);
+
 #ifdef __cplusplus
 }
 #endif

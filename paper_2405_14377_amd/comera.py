@@ -25,7 +25,7 @@ EXPORTS = (
     "comera_ttm_plan", "comera_ttm_plan_num_orders", "comera_ttm_plan_chosen",
     "comera_ttm_plan_order_info", "comera_ttm_workspace_bytes", "comera_ttm_forward",
     "comera_ttm_backward", "comera_ttm_plan_destroy", "comera_tt_embed_workspace_bytes",
-    "comera_tt_embed_forward", "comera_tt_embed_backward", "comera_status_string",
+    "comera_tt_embed_forward", "comera_tt_embed_backward", "comera_status_string", "comera_last_hip_error",
     "comera_ttm_plan_set_timing", "comera_ttm_plan_kernel_time",
 )
 KERNEL_FWD, KERNEL_DX, KERNEL_DW = 0, 1, 2
@@ -33,7 +33,8 @@ KERNEL_FWD, KERNEL_DX, KERNEL_DW = 0, 1, 2
 
 class ComeraError(RuntimeError):
     def __init__(self, status: int, where: str):
-        super().__init__(f"{where}: status {status} ({comera_status_string(status)})")
+        extra = f": {comera_last_hip_error()}" if status == ERR_HIP else ""
+        super().__init__(f"{where}: status {status} ({comera_status_string(status)}){extra}")
         self.status = status
 
 
@@ -60,6 +61,14 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with paper_2405_14377_amd/build.py "
                           "(the HIP library is required; there is no CPU fallback)")
+    # One HIP runtime per process: torch ships its own libamdhip64 under a
+    # different file name, so if this library were opened first the process
+    # would end up with two runtimes and the second one finds no device.
+    # Loading torch first makes this library bind to torch's runtime.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     vp, i32, i64, sz, dbl = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_double
     P = ctypes.POINTER
@@ -91,6 +100,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comera_ttm_plan_kernel_time.restype = i32
     lib.comera_status_string.argtypes = [i32]
     lib.comera_status_string.restype = ctypes.c_char_p
+    lib.comera_last_hip_error.argtypes = []
+    lib.comera_last_hip_error.restype = ctypes.c_char_p
     _lib = lib
     return lib
 
@@ -160,6 +171,10 @@ def tt_embed_shape(v: Sequence[int], e: Sequence[int], r: Sequence[int]) -> come
 # ------------------------------------------------------------------ entry points
 def comera_status_string(status: int) -> str:
     return load().comera_status_string(int(status)).decode()
+
+
+def comera_last_hip_error() -> str:
+    return load().comera_last_hip_error().decode()
 
 
 def comera_ttm_plan(shape: comera_ttm_shape, batch: int, mask_active=None, force_order: int = -1,

@@ -124,7 +124,6 @@ int build_prefix(const comera_tt_embed_shape *s, const EmbedLayout &L, const flo
     fa.d = d;
     fa.nfold = d - 1;
     fa.compacted = 0;
-    fa.swap = 0;
     for (int k = 0; k < d; ++k) {
         fa.G[k] = G[k];
         fa.D[k] = (D && k < d - 1) ? D[k] : nullptr;
@@ -132,6 +131,7 @@ int build_prefix(const comera_tt_embed_shape *s, const EmbedLayout &L, const flo
         fa.Gc[k] = gc[k];
         fa.m[k] = int(s->v[k]);
         fa.n[k] = int(s->e[k]);
+        fa.st[k] = core_strides(int(s->r[k]), fa.m[k], fa.n[k], int(s->r[k + 1]), false);
     }
     for (int k = 0; k <= d; ++k) {
         fa.r[k] = int(s->r[k]);
@@ -179,7 +179,7 @@ bool embed_proj_ok(const comera_tt_embed_shape *s) {
     return true;
 }
 
-comera_status hip_status(int e) { return e ? COMERA_ERR_HIP : COMERA_OK; }
+comera_status hip_status(int e) { return note_hip(e, "embedding kernel") ? COMERA_ERR_HIP : COMERA_OK; }
 
 }  // namespace
 
@@ -307,7 +307,6 @@ comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int
     xa.splits[d - 1] = L.nvp;
     xa.d = d;
     xa.compacted = 0;
-    xa.swap = 0;
     for (int k = 0; k <= d; ++k) {
         xa.r[k] = int(s->r[k]);
         xa.rc[k] = int(s->r[k]);
@@ -317,6 +316,7 @@ comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int
         xa.dG[k] = dG[k];
         xa.m[k] = int(s->v[k]);
         xa.n[k] = int(s->e[k]);
+        xa.st[k] = core_strides(int(s->r[k]), xa.m[k], xa.n[k], int(s->r[k + 1]), false);
     }
     return hip_status(launch_expand(xa, stream));
 }

@@ -173,6 +173,7 @@ struct GemmParams {
     Remap rmap, cmap;
     int vec_a, vec_b;
     int gw;   // tile-order group width in column tiles (see tile_of)
+    uint32_t tx, ty;   // column tiles, row tiles (the grid is one-dimensional)
 };
 
 // Workgroup -> (split, row tile, column tile).  The dispatcher deals
@@ -186,10 +187,10 @@ struct TileIdx {
 };
 __device__ __forceinline__ TileIdx tile_of(const GemmParams &p) {
     constexpr uint32_t kXcds = 8;
-    const uint32_t nx = gridDim.x, ny = gridDim.y;
+    const uint32_t nx = p.tx, ny = p.ty;
     const uint32_t per = nx * ny;
-    const uint32_t total = per * gridDim.z;
-    const uint32_t lin = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
+    const uint32_t total = gridDim.x;
+    const uint32_t lin = blockIdx.x;
     const uint32_t x = lin % kXcds, i = lin / kXcds;
     const uint32_t q = total / kXcds, rem = total % kXcds;
     const uint32_t id = x * q + min(x, rem) + i;
@@ -543,11 +544,23 @@ int choose_gw(const GemmArgs &g, int bm, int bn, int splits) {
     return int((nx + best_q - 1) / best_q);
 }
 
+// One-dimensional grid over (split, row tile, column tile); 0 when the tile
+// count does not fit 31 bits.
+dim3 tile_grid(const GemmArgs &g, int bm, int bn, GemmParams &q) {
+    const int64_t tx = (g.N + bn - 1) / bn, ty = (g.M + bm - 1) / bm;
+    const int64_t total = tx * ty * int64_t(g.splits);
+    if (total <= 0 || total >= (int64_t(1) << 31)) return dim3(0, 1, 1);
+    q.tx = uint32_t(tx);
+    q.ty = uint32_t(ty);
+    return dim3(static_cast<unsigned>(total), 1, 1);
+}
+
 template <typename T, bool AK, bool BK, bool OB>
 int launch_t(const GemmArgs &g, const GemmParams &p, int tile, void *stream) {
     auto go = [&](auto kern, int bm, int bn) {
-        dim3 grid(unsigned((g.N + bn - 1) / bn), unsigned((g.M + bm - 1) / bm), unsigned(g.splits));
         GemmParams q = p;
+        const dim3 grid = tile_grid(g, bm, bn, q);
+        if (!grid.x) return int(hipErrorInvalidConfiguration);
         q.gw = choose_gw(g, bm, bn, g.splits);
         hipLaunchKernelGGL(kern, grid, dim3(256), 0, hipStream_t(stream), q);
         return int(hipGetLastError());
@@ -591,8 +604,9 @@ int go_fast(const GemmArgs &g, const GemmParams &p, void *stream) {
     static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                                    hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
     if (set) return set;
-    dim3 grid(unsigned((g.N + BN - 1) / BN), unsigned((g.M + BM - 1) / BM), unsigned(g.splits));
     GemmParams q = p;
+    const dim3 grid = tile_grid(g, BM, BN, q);
+    if (!grid.x) return int(hipErrorInvalidConfiguration);
     q.gw = choose_gw(g, BM, BN, g.splits);
     hipLaunchKernelGGL(kern, grid, dim3(256), lds, hipStream_t(stream), q);
     return int(hipGetLastError());

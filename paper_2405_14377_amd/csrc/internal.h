@@ -6,6 +6,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <memory>
 #include <string>
 #include <vector>
 
@@ -27,6 +28,13 @@ struct Order {
     double flops_fwd = 0, flops_bwd = 0, bytes = 0, t_pred = 0;
     bool executable = false;
     std::string desc;
+};
+
+// Placement of one compacted core copy: element (a, m, n, c) (left bond,
+// output factor, input factor, right bond; bonds compacted) sits at
+// a * sa + m * sm + n * sn + c * sc.
+struct CoreStrides {
+    int sa, sm, sn, sc;
 };
 
 // Byte offsets of every workspace region used by the dense order.
@@ -57,6 +65,35 @@ struct DenseLayout {
     int e_slices[kMaxCores + 1];
 };
 
+// Sweep orders (groups of consecutive cores, activations swept through the
+// groups in sequence).  Each group g (cores s[g] .. e[g]) is treated as a
+// layer of its own whose outer bonds are folded into its outer factors:
+//   right to left:  W'_g [(N_g, ae_g)][(as_g, M_g)]
+//   left to right:  W'_g [(as_g, N_g)][(M_g, ae_g)]
+// where N_g, M_g are the products of the group's input and output factors
+// and as_g, ae_g its left and right (compacted) bond ranks.  The states of
+// both sweeps are stored with the next contraction's index last:
+//   right to left, activation state Z_g (input of step g-1):
+//       [(b, N_<g-1, M_>=g)][(N_{g-1}, ae_{g-1})]
+//   right to left, dY state H_g (input of step g): [(b, N_<g, M_>g)][(as_g, M_g)]
+//   left to right, activation state Z_g (input of step g): [(b, M_<g, N_>g)][(as_g, N_g)]
+//   left to right, dY state H_g (input of step g): [(b, M_<g, N_>g)][(M_g, ae_g)]
+// so the gradient of W'_g is one product A^T B of the two states that meet
+// at group g, with the token-like index (b and the outer factors) as K.
+struct SweepLayout {
+    int G = 0;
+    int dir = 0;                       // COMERA_ORDER_SWEEP_RL or _LR
+    int s[kMaxCores], e[kMaxCores];
+    int64_t N[kMaxCores], M[kMaxCores], as[kMaxCores], ae[kMaxCores];
+    size_t base[kMaxCores];            // workspace offset of each group's own layout
+    size_t z[kMaxCores + 1];           // activation states Z_g, g = 1 .. G-1
+    size_t h[kMaxCores + 1];           // dY states (RL: H_g, g = 1 .. G-1; LR: H_g, g = 0 .. G-2)
+    size_t tin;                        // per-token transposed dY (RL) or X (LR)
+    bool need_t = false;
+    CoreStrides st[kMaxCores];         // placement of each folded core in its group
+    size_t total = 0;
+};
+
 }  // namespace comera
 
 namespace comera {
@@ -79,16 +116,28 @@ struct comera_ttm_plan_s {
     std::vector<comera::Order> orders;
     int chosen = 0;
     comera::DenseLayout dense;
+    comera::SweepLayout sweep;                    // when the chosen order is a sweep
+    std::unique_ptr<comera_ttm_plan_s> sub[comera::kMaxCores];   // one layer per sweep group
     size_t ws_bytes = 0;
     comera::KernelTiming timing;
 };
 
 namespace comera {
 
-// Workspace layout of the dense order for a plan (fills p->dense).
-void layout_dense(comera_ttm_plan_s *p);
+// Workspace layout of the dense order for a plan (fills p->dense).  Without
+// with_dx no region for split partials of dX is reserved.
+void layout_dense(comera_ttm_plan_s *p, bool with_dx = true);
+// Workspace layout of a sweep order: fills L and one layer per group in sub;
+// false when the order cannot run (workspace above the cap or a group
+// outside the kernels' index limits).
+bool layout_sweep(const comera_ttm_plan_s *p, int kind, uint32_t cuts, SweepLayout &L,
+                  std::unique_ptr<comera_ttm_plan_s> *sub);
 
 // Launchers (ttm_kernels.hip).  All return a hipError_t value as int.
+
+// [a][m][n][c], or [a][n][m][c] when swap
+CoreStrides core_strides(int A, int m, int n, int C, bool swap);
+
 struct FoldArgs {
     const float *G[kMaxCores];
     const float *D[kMaxCores];   // D[k] for k < d-1, may be null (= ones)
@@ -101,12 +150,12 @@ struct FoldArgs {
     int d;
     int nfold;                   // cores folded (grid.y); d for a linear layer
     int compacted;
-    int swap;                    // write [a][n][m][c] instead of [a][m][n][c]
+    CoreStrides st[kMaxCores];   // placement of each copy
 };
 int launch_fold(const FoldArgs &a, void *stream);
 
 struct ExpandArgs {
-    const float *part[kMaxCores];   // [splits][rc_{k}, m, n, rc_{k+1}]
+    const float *part[kMaxCores];   // [splits][compacted core placed by st[k]]
     const float *D[kMaxCores];
     float *dG[kMaxCores];
     BondBits act[kMaxCores + 1];
@@ -117,7 +166,7 @@ struct ExpandArgs {
     int splits[kMaxCores];
     int d;
     int compacted;
-    int swap;                       // partials are [a][n][m][c]
+    CoreStrides st[kMaxCores];      // placement of the compacted partials
     int groups[kMaxCores];          // set by launch_expand
     int blk0[kMaxCores];            // set by launch_expand
 };
@@ -237,6 +286,47 @@ int meet_gemm(const float *P, const float *En, float *part, int64_t NI, int64_t 
 int launch_sum_splits(const float *part, float *out, int64_t n, int splits, void *stream);
 int launch_fill_zero(void *ptr, size_t bytes, void *stream);
 int launch_fill_one(float *ptr, void *stream);
+
+// Steps of one (virtual) layer, shared by the dense order and the groups of
+// a sweep order (api_ttm.hip).
+struct DenseBuild {
+    float *gc[kMaxCores];      // folded cores [rho_k][n_k][m_k][rho_{k+1}]
+    float *P[kMaxCores + 1];   // left chains P_k = [I_<k][J_<k][rho_k], k = 1..d-1
+    void *w;                   // W [N_in][N_out] (or W^T) in the activation dtype
+};
+// folded-core pointers of a layer whose workspace starts at ws
+void dense_ptrs(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd);
+// fold the masks into compacted copies of every core of layer p (eq. Wcompress):
+// core k goes to dst[k], placed by st[k]
+int fold_cores(const comera_ttm_plan_s *p, const float *const *G, const float *const *D, float *const *dst,
+               const CoreStrides *st, void *stream);
+// left chains and W (or W^T with transpose) of a layer from its folded cores
+int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, bool transpose, void *stream);
+// dW = A^T B (A [K][N_in] with leading dimension lda, B [K][N_out] with ldb),
+// split over K, written blocked for the projections; *dwp, *splits describe
+// the split partials
+int dw_gemm(const comera_ttm_plan_s *sp, const void *A, int64_t lda, const void *B, int64_t ldb, int64_t K,
+            void *ws, float **dwp, int *splits, void *stream);
+// core gradients (compacted, as split partials part[k] x nsplit[k]) from the
+// partials of dW; want[k] false skips core k
+int project_cores(const comera_ttm_plan_s *sp, const DenseBuild &bd, const float *dwp, int splits,
+                  const bool *want, void *ws, const float **part, int *nsplit, void *stream);
+// sum the partials of every core of layer p, unfold and apply the masks
+int expand_cores(const comera_ttm_plan_s *p, const float *const *part, const int *nsplit, const CoreStrides *st,
+                 const float *const *D, float *const *dG, void *stream);
+// out[t][j][i] = in[t][i][j] for t < b, i < M, j < T (elements of esz bytes)
+int launch_permute_tokens(const void *in, void *out, int64_t b, int64_t M, int64_t T, int esz, void *stream);
+
+// sweep orders (sweep.hip)
+comera_status sweep_forward(const comera_ttm_plan_s *p, int64_t b, const void *X, const float *const *G,
+                            const float *const *D, void *Y, void *ws, void *stream);
+comera_status sweep_backward(const comera_ttm_plan_s *p, int64_t b, const void *X, const void *dY,
+                             const float *const *G, const float *const *D, void *dX, float *const *dG, void *ws,
+                             void *stream);
+
+// record a failed launcher result (hipError_t value e != 0) with the step
+// name for comera_last_hip_error; returns e (api_ttm.hip)
+int note_hip(int e, const char *where);
 
 // timing hooks (api_ttm.hip)
 void timing_begin(comera_ttm_plan_s *p, int kernel, void *stream, void **ev0);

@@ -62,6 +62,31 @@ void describe(Order &o, int d) {
     o.desc = buf;
 }
 
+// Time of one launch: its work at half the dense peak plus its bytes at the
+// HBM rate, and never below the launch cost.
+double launch_time(double flops, double bytes, double peak) {
+    return std::max(kLaunch, flops / (0.5 * peak) + bytes / kHbm);
+}
+
+// Flops of the projections of a group's matrix gradient onto its cores (one
+// environment step and one meet per core but the first; eq. back Gi).
+double proj_flops(const comera_ttm_plan_s *p, int s, int e, double rs, double re) {
+    double I = 1, J = 1;
+    for (int k = s; k <= e; ++k) {
+        I *= double(p->s.n[k]);
+        J *= double(p->s.m[k]);
+    }
+    double f = 0;
+    for (int k = e; k > s; --k) {
+        I /= double(p->s.n[k]);
+        J /= double(p->s.m[k]);
+        const double right = k == e ? re : double(p->rho[k + 1]);
+        f += 4.0 * rs * I * J * double(p->s.n[k]) * double(p->s.m[k]) * right * double(p->rho[k]);
+    }
+    return f;
+}
+
+// Predicted flops, bytes and time of one forward plus one backward call.
 void cost_order(const comera_ttm_plan_s *p, Order &o) {
     const int d = p->d;
     const double b = double(p->batch);
@@ -83,48 +108,58 @@ void cost_order(const comera_ttm_plan_s *p, Order &o) {
             s = k + 1;
         }
     }
-    double build = 0;
+    const int G = int(groups.size());
+    double build = 0, t_build = kLaunch;   // the fold
     std::vector<GroupDims> gd;
     for (auto &g : groups) {
         gd.push_back(group_dims(p, g.first, g.second));
         build += gd.back().build_flops;
+        const int dg = g.second - g.first + 1;
+        const double steps = dg > 1 ? dg - 1 : (p->s.act == COMERA_BF16 || o.kind == COMERA_ORDER_DENSE ? 1 : 0);
+        t_build += steps * kLaunch + gd.back().build_flops / (0.5 * kPeakF32);
     }
     if (o.kind == COMERA_ORDER_DENSE) {
-        // projections of dW onto every core: one adjoint step and one meet
-        // per core, each 2 * |E_{k+1}| * rho_k flops.
-        double proj = 0, Il = Nin, Jl = Nout;
-        for (int k = d - 1; k >= 0; --k) {
-            double Esz = Il * Jl * double(p->rho[k + 1]);
-            proj += (k > 0 ? 4.0 : 0.0) * Esz * double(p->rho[k]);
-            Il /= double(p->s.n[k]);
-            Jl /= double(p->s.m[k]);
-        }
-        o.flops_fwd = build + 2.0 * b * Nin * Nout;
-        o.flops_bwd = build + 4.0 * b * Nin * Nout + proj;
-        o.bytes = b * (Nin + Nout) * esz * 2 + b * (Nin + Nout) * esz * 2 + Nin * Nout * (esz * 3 + 12.0);
-        double launches = double(d) + 1 + double(d) + 3 + 2.0 * d;
-        o.t_pred = (o.flops_fwd + o.flops_bwd - 2 * build) / peak + 2 * build / kPeakF32 + o.bytes / kHbm +
-                   launches * kLaunch;
+        const double proj = proj_flops(p, 0, d - 1, 1.0, 1.0);
+        const double gemm = 2.0 * b * Nin * Nout;
+        o.flops_fwd = build + gemm;
+        o.flops_bwd = build + 2.0 * gemm + proj;
+        const double act = b * (Nin + Nout) * esz, w = Nin * Nout * esz;
+        o.bytes = 3.0 * act + 3.0 * w + Nin * Nout * 4.0;
+        o.t_pred = 2.0 * t_build + 3.0 * launch_time(gemm, act + w, peak) + (d - 1) * kLaunch +
+                   proj / (0.5 * kPeakF32) + kLaunch;
         return;
     }
-    // sweeps
-    const int G = int(groups.size());
-    double sweep = 0, inter_bytes = 0;
+    // sweeps: step g contracts rows x (K = in-side of the group) into C
+    const bool rl = o.kind == COMERA_ORDER_SWEEP_RL;
+    double sweep = 0, t_step = 0, out_step = 0, out_flops = 0, inter_bytes = 0, proj = 0, t_meet = 0;
     for (int gi = 0; gi < G; ++gi) {
         double Ib = 1, Ja = 1, Jb = 1, Ia = 1;  // I before / J after (RL); J before / I after (LR)
         for (int h = 0; h < gi; ++h) { Ib *= gd[h].I; Jb *= gd[h].J; }
         for (int h = gi + 1; h < G; ++h) { Ja *= gd[h].J; Ia *= gd[h].I; }
         const GroupDims &g = gd[gi];
-        double outer = o.kind == COMERA_ORDER_SWEEP_RL ? Ib * Ja : Jb * Ia;
-        sweep += 2.0 * b * outer * g.I * g.re * g.rs * g.J;
-        double state = o.kind == COMERA_ORDER_SWEEP_RL ? b * Ib * g.rs * g.J * Ja : b * Jb * g.J * g.re * Ia;
-        if (gi != (o.kind == COMERA_ORDER_SWEEP_RL ? 0 : G - 1)) inter_bytes += state * 4.0 * 2;
+        const double rows = b * (rl ? Ib * Ja : Jb * Ia);
+        const double K = rl ? g.I * g.re : g.rs * g.I, C = rl ? g.rs * g.J : g.J * g.re;
+        const double f = 2.0 * rows * K * C;
+        sweep += f;
+        const double by = rows * (K + C) * esz + K * C * esz;
+        inter_bytes += rows * (K + C) * esz;
+        t_step += launch_time(f, by, peak);
+        if (gi == (rl ? 0 : G - 1)) {
+            out_step = launch_time(f, by, peak);
+            out_flops = f;
+        }
+        proj += proj_flops(p, groups[gi].first, groups[gi].second, g.rs, g.re);
+        t_meet += launch_time(f, by, peak);
+        t_meet += (groups[gi].second - groups[gi].first) * kLaunch;
     }
+    // backward: the activation states are recomputed (every step but the one
+    // writing Y), then the dY sweep and one meet per group
     o.flops_fwd = build + sweep;
-    o.flops_bwd = build + 2.0 * sweep;
-    o.bytes = b * (Nin + Nout) * esz * 4 + inter_bytes * 3;
-    double launches = 3.0 * G + 2.0 * d;
-    o.t_pred = (3.0 * sweep) / peak + 2 * build / kPeakF32 + o.bytes / kHbm + launches * kLaunch;
+    o.flops_bwd = build + 2.0 * sweep + (sweep - out_flops) + proj;
+    o.bytes = inter_bytes * 4.0;
+    const double t_perm = G > 1 ? 2.0 * kLaunch : 0.0;
+    o.t_pred = 2.0 * t_build + t_step + (t_step - out_step) + t_step + t_meet + proj / (0.5 * kPeakF32) +
+               kLaunch + t_perm;
 }
 
 bool validate(const comera_ttm_shape *s, int64_t batch) {
@@ -146,7 +181,7 @@ bool validate(const comera_ttm_shape *s, int64_t batch) {
 
 }  // namespace
 
-void layout_dense(comera_ttm_plan_s *p) {
+void layout_dense(comera_ttm_plan_s *p, bool with_dx) {
     DenseLayout &L = p->dense;
     std::memset(&L, 0, sizeof(L));
     const int d = p->d;
@@ -184,7 +219,7 @@ void layout_dense(comera_ttm_plan_s *p) {
     // 128 x 128 tiles (the partials are summed in a fixed order)
     L.dx_splits = 1;
     L.dx_kchunk = p->N_out;
-    if (p->s.act == COMERA_F32) {
+    if (with_dx && p->s.act == COMERA_F32) {
         const int64_t xt = ((b + 127) / 128) * ((p->N_in + 127) / 128);
         int64_t sx = std::max<int64_t>(1, (768 + xt / 2) / xt);
         sx = std::min<int64_t>(std::min<int64_t>(sx, 8), std::max<int64_t>(1, p->N_out / 512));
@@ -271,6 +306,152 @@ void layout_dense(comera_ttm_plan_s *p) {
     L.total = off;
 }
 
+namespace {
+constexpr double kSweepCap = 64.0 * 1024 * 1024 * 1024;   // workspace cap of a sweep order (bytes)
+
+// placement of core k (local index j of a group of dg cores, bonds A and C)
+// in the group's layer: right to left the group's left bond joins the output
+// factor of its first core and its right bond the input factor of its last
+// core; left to right (left bond before the first input factor, right bond
+// after the last output factor) the placement is the plain swapped one
+CoreStrides sweep_strides(int dir, int j, int dg, int A, int m, int n, int C) {
+    if (dir == COMERA_ORDER_SWEEP_LR || (j > 0 && j < dg - 1)) return core_strides(A, m, n, C, true);
+    CoreStrides s;
+    if (dg == 1) {           // [1][(n, c)][(a, m)][1]
+        s.sn = C * A * m;
+        s.sc = A * m;
+        s.sa = m;
+        s.sm = 1;
+    } else if (j == 0) {     // [1][n][(a, m)][c]
+        s.sn = A * m * C;
+        s.sa = m * C;
+        s.sm = C;
+        s.sc = 1;
+    } else {                 // [a][(n, c)][m][1]
+        s.sa = n * C * m;
+        s.sn = C * m;
+        s.sc = m;
+        s.sm = 1;
+    }
+    return s;
+}
+}  // namespace
+
+bool layout_sweep(const comera_ttm_plan_s *p, int kind, uint32_t cuts, SweepLayout &L,
+                  std::unique_ptr<comera_ttm_plan_s> *sub) {
+    L = SweepLayout();
+    const int d = p->d;
+    const bool rl = kind == COMERA_ORDER_SWEEP_RL;
+    L.dir = kind;
+    int G = 0, s0 = 0;
+    for (int k = 0; k < d; ++k) {
+        if (k == d - 1 || ((cuts >> k) & 1u)) {
+            L.s[G] = s0;
+            L.e[G] = k;
+            ++G;
+            s0 = k + 1;
+        }
+    }
+    L.G = G;
+    for (int g = 0; g < G; ++g) {
+        L.N[g] = 1;
+        L.M[g] = 1;
+        for (int k = L.s[g]; k <= L.e[g]; ++k) {
+            L.N[g] *= p->s.n[k];
+            L.M[g] *= p->s.m[k];
+        }
+        L.as[g] = p->rho[L.s[g]];
+        L.ae[g] = p->rho[L.e[g] + 1];
+    }
+    auto prod = [&](const int64_t *v, int lo, int hi) {   // product of v[lo .. hi)
+        double x = 1;
+        for (int h = lo; h < hi; ++h) x *= double(v[h]);
+        return x;
+    };
+    const double b = double(std::max<int64_t>(p->batch, 1));
+    const size_t esz = p->s.act == COMERA_BF16 ? 2 : 4;
+    double off = 0;
+    // one layer per group
+    for (int g = 0; g < G; ++g) {
+        const int dg = L.e[g] - L.s[g] + 1;
+        sub[g].reset(new (std::nothrow) comera_ttm_plan_s());
+        comera_ttm_plan_s *sp = sub[g].get();
+        if (!sp) return false;
+        std::memset(&sp->s, 0, sizeof(sp->s));
+        std::memset(sp->act, 0, sizeof(sp->act));
+        sp->s.d = dg;
+        sp->s.act = p->s.act;
+        for (int j = 0; j < dg; ++j) {
+            sp->s.n[j] = p->s.n[L.s[g] + j];
+            sp->s.m[j] = p->s.m[L.s[g] + j];
+            sp->s.r[j] = j == 0 ? 1 : p->rho[L.s[g] + j];
+        }
+        sp->s.r[dg] = 1;
+        if (rl) {
+            sp->s.m[0] *= L.as[g];
+            sp->s.n[dg - 1] *= L.ae[g];
+        } else {
+            sp->s.n[0] *= L.as[g];
+            sp->s.m[dg - 1] *= L.ae[g];
+        }
+        sp->d = dg;
+        sp->N_in = 1;
+        sp->N_out = 1;
+        double nin = 1, nout = 1;
+        for (int j = 0; j < dg; ++j) {
+            nin *= double(sp->s.n[j]);
+            nout *= double(sp->s.m[j]);
+            if (double(sp->s.r[j]) * double(sp->s.m[j]) * double(sp->s.n[j]) * double(sp->s.r[j + 1]) >
+                2147483647.0)
+                return false;
+            sp->N_in *= sp->s.n[j];
+            sp->N_out *= sp->s.m[j];
+        }
+        if (nin > 2147483647.0 || nout > 2147483647.0 || nin * nout * 4.0 > kSweepCap) return false;
+        for (int j = 0; j <= dg; ++j) sp->rho[j] = sp->s.r[j];
+        sp->compacted = false;
+        // K of the product that meets at this group: tokens times the outer factors
+        const double kappa = rl ? b * prod(L.N, 0, g) * prod(L.M, g + 1, G) : b * prod(L.M, 0, g) * prod(L.N, g + 1, G);
+        if (kappa > 4.0e18) return false;
+        sp->batch = int64_t(kappa);
+        layout_dense(sp, false);
+        for (int j = 0; j < dg; ++j) {
+            const int k = L.s[g] + j;
+            L.st[k] = sweep_strides(kind, j, dg, int(p->rho[k]), int(p->s.m[k]), int(p->s.n[k]), int(p->rho[k + 1]));
+        }
+        L.base[g] = size_t(off);
+        off += double(align_up(sp->dense.total));
+    }
+    // states: both sweeps store G-1 intermediate states of equal sizes
+    for (int g = 1; g < G; ++g) {
+        double zs, hs;
+        if (rl) {
+            zs = b * prod(L.N, 0, g) * double(L.ae[g - 1]) * prod(L.M, g, G);   // Z_g
+            hs = zs;                                                                    // H_g
+        } else {
+            zs = b * prod(L.M, 0, g) * double(L.as[g]) * prod(L.N, g, G);       // Z_g
+            hs = b * prod(L.M, 0, g) * double(L.ae[g - 1]) * prod(L.N, g, G);           // H_{g-1}
+        }
+        L.z[g] = size_t(off);
+        off += double(align_up(size_t(zs * double(esz))));
+        if (off > kSweepCap) return false;
+        const int hi = rl ? g : g - 1;
+        L.h[hi] = size_t(off);
+        off += double(align_up(size_t(hs * double(esz))));
+        if (off > kSweepCap) return false;
+    }
+    // per-token transpose of the input whose first-swept factor is not last
+    const double trail = rl ? prod(L.M, 1, G) : prod(L.N, 1, G);
+    L.need_t = G > 1 && trail > 1;
+    if (L.need_t) {
+        L.tin = size_t(off);
+        off += double(align_up(size_t(b * double(rl ? p->N_out : p->N_in) * double(esz))));
+    }
+    if (off > kSweepCap) return false;
+    L.total = size_t(off);
+    return true;
+}
+
 }  // namespace comera
 
 using namespace comera;
@@ -351,7 +532,13 @@ comera_status comera_ttm_plan(const comera_ttm_shape *s, int64_t batch, const ui
             o.executable = true;
         } else {
             cost_order(p, o);
-            o.executable = o.kind == COMERA_ORDER_DENSE;
+            if (o.kind == COMERA_ORDER_DENSE) {
+                o.executable = true;
+            } else {
+                SweepLayout sl;
+                std::unique_ptr<comera_ttm_plan_s> tmp[kMaxCores];
+                o.executable = layout_sweep(p, o.kind, o.cuts, sl, tmp);
+            }
         }
     }
     if (force_order >= 0) {
@@ -372,8 +559,20 @@ comera_status comera_ttm_plan(const comera_ttm_shape *s, int64_t batch, const ui
         }
         p->chosen = best < 0 ? 0 : best;
     }
-    if (!p->zero) layout_dense(p);
-    p->ws_bytes = p->zero ? 0 : p->dense.total;
+    p->ws_bytes = 0;
+    if (!p->zero) {
+        const Order &o = p->orders[p->chosen];
+        if (o.kind == COMERA_ORDER_DENSE) {
+            layout_dense(p);
+            p->ws_bytes = p->dense.total;
+        } else {
+            if (!layout_sweep(p, o.kind, o.cuts, p->sweep, p->sub)) {
+                delete p;
+                return COMERA_ERR_INTERNAL;
+            }
+            p->ws_bytes = p->sweep.total;
+        }
+    }
     *out = p;
     return COMERA_OK;
 }

@@ -56,24 +56,25 @@ __global__ void fold_kernel(FoldArgs a) {
     if (k >= a.nfold) return;
     const int rl = a.rc[k], rr = a.rc[k + 1], m = a.m[k], n = a.n[k];
     const int total = rl * m * n * rr;     // core sizes are far below 2^31 (host checks)
-    const int mn_ = m * n;
     const float *G = a.G[k];
     const float *D = (k < a.d - 1) ? a.D[k] : nullptr;
+    const CoreStrides st = a.st[k];
     for (int o = blockIdx.x * blockDim.x + threadIdx.x; o < total; o += gridDim.x * blockDim.x) {
+        // compacted element o = (al, jm, in, c)
         const int c = o % rr;
-        const int t = o / rr;
-        const int mn = t % mn_;
-        const int al = t / mn_;
+        int t = o / rr;
+        const int in = t % n;
+        t /= n;
+        const int jm = t % m;
+        const int al = t / m;
         int fa = al, fc = c;
         if (a.compacted) {
             fa = (k == 0) ? 0 : select_bit(a.act[k], al);
             fc = (k == a.d - 1) ? 0 : select_bit(a.act[k + 1], c);
         }
-        // output element o = (al, q, c) with q over (m, n), or (n, m) when swapped
-        const int jm = a.swap ? mn % m : mn / n, in = a.swap ? mn / m : mn % n;
         float v = G[((fa * m + jm) * n + in) * a.r[k + 1] + fc];
         if (D) v *= D[fc];
-        a.Gc[k][o] = v;
+        a.Gc[k][al * st.sa + jm * st.sm + in * st.sn + c * st.sc] = v;
     }
 }
 
@@ -112,7 +113,8 @@ __global__ __launch_bounds__(256) void expand_kernel(ExpandArgs a) {
         }
         if (ca >= 0 && cc >= 0) {
             const int jm = mn / n, in = mn % n;
-            ci = (ca * mn_ + (a.swap ? in * m + jm : mn)) * crr + cc;
+            const CoreStrides st = a.st[k];
+            ci = ca * st.sa + jm * st.sm + in * st.sn + cc * st.sc;
         }
     }
     float v = 0.f;
@@ -146,6 +148,32 @@ __global__ void sum_splits_kernel(const float *__restrict__ part, float *__restr
     }
 }
 
+// out[t][j][i] = in[t][i][j] (i < M, j < Tn) through a 32 x 33 LDS tile; the
+// workgroups stride over (token, row tile, column tile).
+template <typename T>
+__global__ __launch_bounds__(256) void permute_kernel(const T *__restrict__ in, T *__restrict__ out, int64_t b, int M,
+                                                      int Tn, int64_t tiles_m, int64_t tiles_t) {
+    __shared__ T tile[32][33];
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    const int64_t per = tiles_m * tiles_t, total = b * per;
+    for (int64_t id = blockIdx.x; id < total; id += gridDim.x) {
+        const int64_t t = id / per, r = id % per;
+        const int i0 = int(r / tiles_t) * 32, j0 = int(r % tiles_t) * 32;
+        const T *src = in + t * int64_t(M) * Tn;
+        T *dst = out + t * int64_t(M) * Tn;
+        for (int y = ty; y < 32; y += 8) {
+            const int i = i0 + y, j = j0 + tx;
+            if (i < M && j < Tn) tile[y][tx] = src[int64_t(i) * Tn + j];
+        }
+        __syncthreads();
+        for (int y = ty; y < 32; y += 8) {
+            const int j = j0 + y, i = i0 + tx;
+            if (i < M && j < Tn) dst[int64_t(j) * M + i] = tile[tx][y];
+        }
+        __syncthreads();
+    }
+}
+
 __global__ void fill_one_kernel(float *p) { *p = 1.0f; }
 
 __global__ void fill_zero_kernel(uint32_t *p, int64_t n) {
@@ -159,6 +187,21 @@ inline int grid_for(int64_t n, int threads = 256, int64_t cap = 65536) {
 }
 
 }  // namespace
+
+CoreStrides core_strides(int A, int m, int n, int C, bool swap) {
+    (void)A;
+    CoreStrides s;
+    s.sc = 1;
+    if (swap) {
+        s.sm = C;
+        s.sn = m * C;
+    } else {
+        s.sn = C;
+        s.sm = n * C;
+    }
+    s.sa = m * n * C;
+    return s;
+}
 
 int launch_fold(const FoldArgs &a, void *stream) {
     int64_t mx = 1;
@@ -188,6 +231,22 @@ int launch_expand(const ExpandArgs &a_in, void *stream) {
 
 int launch_sum_splits(const float *part, float *out, int64_t n, int splits, void *stream) {
     hipLaunchKernelGGL(sum_splits_kernel, dim3(grid_for(n)), dim3(256), 0, hipStream_t(stream), part, out, n, splits);
+    return int(hipGetLastError());
+}
+
+int launch_permute_tokens(const void *in, void *out, int64_t b, int64_t M, int64_t T, int esz, void *stream) {
+    if (b <= 0 || M <= 0 || T <= 0) return 0;
+    const int64_t tm = (M + 31) / 32, tt = (T + 31) / 32;
+    const int64_t total = b * tm * tt;
+    const unsigned grid = unsigned(std::min<int64_t>(total, 16384));
+    if (esz == 2)
+        hipLaunchKernelGGL(permute_kernel<uint16_t>, dim3(grid), dim3(256), 0, hipStream_t(stream),
+                           reinterpret_cast<const uint16_t *>(in), reinterpret_cast<uint16_t *>(out), b, int(M),
+                           int(T), tm, tt);
+    else
+        hipLaunchKernelGGL(permute_kernel<float>, dim3(grid), dim3(256), 0, hipStream_t(stream),
+                           reinterpret_cast<const float *>(in), reinterpret_cast<float *>(out), b, int(M), int(T),
+                           tm, tt);
     return int(hipGetLastError());
 }
 

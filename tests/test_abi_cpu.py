@@ -46,7 +46,9 @@ def test_order_count(d):
     assert p.order_info(0)["kind"] == C.ORDER_DENSE
     kinds = [p.order_info(i)["kind"] for i in range(1, p.num_orders)]
     assert kinds == [C.ORDER_SWEEP_RL, C.ORDER_SWEEP_LR] * (2 ** (d - 1) - 1)
-    assert p.chosen == 0
+    # every order of a small layer can run; the choice is one of them
+    assert all(p.order_info(i)["executable"] for i in range(p.num_orders))
+    assert 0 <= p.chosen < p.num_orders
 
 
 def test_order_descriptions_d3():
