@@ -59,13 +59,13 @@ def layer_inputs(wid, li, act, gen_seed):
 
 
 class Layer:
-    def __init__(self, sh, X, dY, G, D, mask_active, b, act):
+    def __init__(self, sh, X, dY, G, D, mask_active, b, act, force_order=-1):
         import torch
         from paper_2405_14377_amd import comera as C
         self.C = C
         self.sh, self.X, self.dY, self.G, self.D, self.b, self.act = sh, X, dY, G, D, b, act
         self.plan = C.TTMPlan(sh.n, sh.m, sh.r, C.BF16 if act == "bf16" else C.F32, batch=b,
-                              mask_active=mask_active)
+                              mask_active=mask_active, force_order=force_order)
         dev = X.device
         self.ws = torch.empty(self.plan.workspace_bytes, dtype=torch.uint8, device=dev)
         self.Y = torch.empty((b, sh.n_out), dtype=X.dtype, device=dev)
@@ -73,11 +73,16 @@ class Layer:
         self.dG = [torch.empty_like(g) for g in G]
         self.stream = torch.cuda.current_stream().cuda_stream
 
+    def forward(self):
+        self.C.comera_ttm_forward(self.plan.handle, self.b, self.X, self.G, self.D, self.Y, self.ws, self.stream)
+
+    def backward(self):
+        self.C.comera_ttm_backward(self.plan.handle, self.b, self.X, self.dY, self.G, self.D, self.dX, self.dG,
+                                   self.ws, self.stream)
+
     def step(self):
-        C = self.C
-        C.comera_ttm_forward(self.plan.handle, self.b, self.X, self.G, self.D, self.Y, self.ws, self.stream)
-        C.comera_ttm_backward(self.plan.handle, self.b, self.X, self.dY, self.G, self.D, self.dX, self.dG, self.ws,
-                              self.stream)
+        self.forward()
+        self.backward()
 
 
 def time_loop(fn, steps, warmup):
@@ -273,7 +278,7 @@ def other_workloads(steps, warmup):
     from paper_2405_14377_amd import workloads as wl
     res = {}
     # TTM layer workloads
-    for wid, act in ((0, "f32"), (1, "bf16"), (2, "bf16"), (4, "bf16")):
+    for wid, act in ((0, "f32"), (1, "bf16"), (2, "bf16"), (4, "bf16"), (5, "f32"), (5, "bf16")):
         w = wl.WORKLOADS[wid]
         layers, dense = [], []
         for li in range(len(w.layers)):
@@ -284,13 +289,19 @@ def other_workloads(steps, warmup):
         ms, _ = time_loop(lambda: [l.step() for l in layers], k, warmup)
         dms, _ = time_loop(lambda: [f() for f in dense], k, warmup)
         fl = sum(6.0 * l.b * l.sh.n_in * l.sh.n_out for l in layers)
+        fl_alg = 0.0
+        for l in layers:
+            o = l.plan.order_info(l.plan.chosen)
+            fl_alg += o["flops_fwd"] + o["flops_bwd"]
         entry = {"workload": w.name, "dtype": act, "tokens": w.batch, "layers": len(layers),
                  "ms_per_step": round(ms, 4), "tokens_per_s": round(w.batch / (ms * 1e-3), 1),
                  "tflops_gemm_equiv": round(fl / (ms * 1e-3) / 1e12, 2),
+                 "tflops_algorithmic": round(fl_alg / (ms * 1e-3) / 1e12, 2),
                  "dense_ms_per_step": round(dms, 4), "speedup_vs_dense": round(dms / ms, 3)}
         if wid in (1, 2, 4):
             roofs = [kernel_roofline(l, max(2, k // 2), act)[1] for l in layers]
             entry["kernels_ms"] = [{t: round(v["avg_ms"], 4) for t, v in r.items()} for r in roofs]
+        entry["orders"] = [l.plan.order_info(l.plan.chosen)["desc"] for l in layers]
         res[f"w{wid}_{act}"] = entry
         del layers, dense
         torch.cuda.empty_cache()
@@ -336,6 +347,49 @@ def other_workloads(steps, warmup):
     return res
 
 
+def order_timings(wids, steps, warmup):
+    """Every executable contraction order of each layer of the given
+    workloads, timed forward and backward separately, beside the dense
+    torch.matmul step of the same shapes."""
+    import torch
+    from paper_2405_14377_amd import workloads as wl
+    out = []
+    for wid in wids:
+        w = wl.WORKLOADS[wid]
+        for act in w.dtypes:
+            for li in range(len(w.layers)):
+                sh, inp, X, dY, G, D, ma, b = layer_inputs(wid, li, act, 1000 * wid + li)
+                probe = Layer(sh, X, dY, G, D, ma, b, act)
+                chosen = probe.plan.chosen
+                infos = [probe.plan.order_info(i) for i in range(probe.plan.num_orders)]
+                del probe
+                dense = 6.0 * b * sh.n_in * sh.n_out
+                dms, _ = time_loop(dense_step_fn(sh, X, dY), steps, warmup)
+                rec = {"workload": w.name, "layer": sh.name, "dtype": act, "tokens": b, "chosen": chosen,
+                       "dense_gemm_ms": round(dms, 5), "orders": []}
+                for i, o in enumerate(infos):
+                    if not o["executable"]:
+                        rec["orders"].append({"i": i, "desc": o["desc"], "executable": False})
+                        continue
+                    fl = o["flops_fwd"] + o["flops_bwd"]
+                    k = steps if fl < 5 * dense else max(2, steps // 5)
+                    log(f"[orders] {w.name} {sh.name} {act} order {i} {o['desc']}: {k} steps")
+                    lay = Layer(sh, X, dY, G, D, ma, b, act, force_order=i)
+                    fms, _ = time_loop(lay.forward, k, min(warmup, 2))
+                    bms, _ = time_loop(lay.backward, k, min(warmup, 2))
+                    rec["orders"].append({"i": i, "desc": o["desc"], "fwd_ms": round(fms, 5), "bwd_ms": round(bms, 5),
+                                          "step_ms": round(fms + bms, 5),
+                                          "flops_vs_dense": round(fl / dense, 4),
+                                          "tflops": round(fl / ((fms + bms) * 1e-3) / 1e12, 2),
+                                          "speedup_vs_dense_gemm": round(dms / (fms + bms), 3)})
+                    del lay
+                    torch.cuda.empty_cache()
+                out.append(rec)
+                del X, dY, G, D
+                torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -350,6 +404,8 @@ def main():
     ap.add_argument("--traffic-summary", nargs=5, metavar=("FETCH_DIR", "WRITE_DIR", "KERNEL", "GRID", "TAG"),
                     help="write profiles/traffic_<TAG>_<dtype>.md from two counter runs (no GPU); GRID 0 = any")
     ap.add_argument("--commands", nargs="*", default=[], help="commands recorded in a summary")
+    ap.add_argument("--orders", type=int, nargs="*", default=None, metavar="WORKLOAD",
+                    help="time every contraction order of these workloads (default 0 1 5) and exit")
     args = ap.parse_args()
     if args.stats_summary:
         kernel_stats_summary(*args.stats_summary)
@@ -371,6 +427,11 @@ def main():
         sys.exit(1)
     from paper_2405_14377_amd import comera as C
     C.load()
+    if args.orders is not None:
+        wids = args.orders or [0, 1, 5]
+        for rec in order_timings(wids, args.steps, args.warmup):
+            print(json.dumps(rec), flush=True)
+        return
     runs = {}
     for act in ("f32", "bf16"):
         sh, inp, X, dY, G, D, ma, b = layer_inputs(1, 0, act, 1000 + (act == "bf16"))

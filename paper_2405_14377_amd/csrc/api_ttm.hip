@@ -365,6 +365,11 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, 
     g.ldb = p->N_in;
     g.rmap = remap_linear(p->N_out);
     g.cmap = remap_linear(1);
+    if (p->dense.part_elems > 0) {
+        g.scratch = reinterpret_cast<float *>(at(ws, p->dense.part));
+        g.scratch_elems = p->dense.part_elems;
+        g.out_elems = b * p->N_out;
+    }
     e = note_hip(launch_gemm(g, stream), "forward GEMM");
     timing_end(p, COMERA_KERNEL_FWD, stream, ev);
     return e ? COMERA_ERR_HIP : COMERA_OK;
@@ -417,6 +422,11 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
         g.ldb = p->N_out;
         g.rmap = remap_linear(p->N_in);
         g.cmap = remap_linear(1);
+        if (L.dx_splits == 1 && L.part_elems > 0) {
+            g.scratch = reinterpret_cast<float *>(at(ws, L.part));
+            g.scratch_elems = L.part_elems;
+            g.out_elems = b * p->N_in;
+        }
         if (L.dx_splits > 1) {
             g.C = at(ws, L.dx_part);
             g.splits = L.dx_splits;

@@ -661,6 +661,15 @@ bool fast_ok(const GemmArgs &g, int64_t kchunk, int ktb) {
 }
 }  // namespace
 
+int gemm_auto_splits(int64_t M, int64_t N, int64_t K) {
+    const int64_t tiles = ceil_div(M, 64) * ceil_div(N, 64);
+    if (tiles >= 256 || K < 128) return 1;
+    int64_t s = ceil_div(1024, tiles);
+    s = std::min<int64_t>(s, K / 64);
+    s = std::min<int64_t>(s, 32);
+    return int(std::max<int64_t>(s, 1));
+}
+
 Remap remap_linear(int64_t stride) {
     Remap r{};
     r.nd = 1;
@@ -670,6 +679,23 @@ Remap remap_linear(int64_t stride) {
 
 int launch_gemm(const GemmArgs &g, void *stream) {
     if (g.M <= 0 || g.N <= 0) return 0;
+    if (g.splits <= 1 && g.scratch && g.out_elems > 0) {
+        int s = gemm_auto_splits(g.M, g.N, g.K);
+        while (s > 1 && int64_t(s) * g.out_elems > g.scratch_elems) --s;
+        if (s > 1) {
+            GemmArgs h = g;
+            h.scratch = nullptr;
+            h.C = g.scratch;
+            h.out_bf16 = false;
+            h.kchunk = (ceil_div(g.K, s) + 31) / 32 * 32;
+            h.splits = int(ceil_div(g.K, h.kchunk));
+            h.split_stride = g.out_elems;
+            if (int e = launch_gemm(h, stream)) return e;
+            return g.out_bf16 ? launch_sum_splits_bf16(g.scratch, g.C, g.out_elems, h.splits, stream)
+                              : launch_sum_splits(g.scratch, reinterpret_cast<float *>(g.C), g.out_elems, h.splits,
+                                                  stream);
+        }
+    }
     GemmParams p;
     p.A = g.A;
     p.B = g.B;
@@ -711,6 +737,8 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     if (g.dtype == COMERA_BF16) {
         COMERA_GEMM_CASE(uint16_t, true, false, true)
         COMERA_GEMM_CASE(uint16_t, true, true, true)
+        COMERA_GEMM_CASE(uint16_t, true, false, false)
+        COMERA_GEMM_CASE(uint16_t, true, true, false)
         COMERA_GEMM_CASE(uint16_t, false, false, false)
     } else {
         COMERA_GEMM_CASE(float, true, false, false)

@@ -56,6 +56,8 @@ struct DenseLayout {
     size_t dx_part;            // split partials of dX (fp32)
     int adj_splits[kMaxCores];  // split-K of the adjoint step producing E_k
     size_t adj_part;           // shared scratch for adjoint split partials
+    size_t part;               // split partials of the forward / dX products at small batch
+    int64_t part_elems;
     // fused projection route (all ranks within proj_supported): step k reads
     // E_{k+1} as e_slices[k+1] slices and writes E_k as e_slices[k] slices
     // (one per column chunk) and meet_splits[k] meet partials (one per row chunk)
@@ -90,6 +92,8 @@ struct SweepLayout {
     size_t h[kMaxCores + 1];           // dY states (RL: H_g, g = 1 .. G-1; LR: H_g, g = 0 .. G-2)
     size_t tin;                        // per-token transposed dY (RL) or X (LR)
     bool need_t = false;
+    size_t part = 0;                   // split partials of the sweep products
+    int64_t part_elems = 0;
     CoreStrides st[kMaxCores];         // placement of each folded core in its group
     size_t total = 0;
 };
@@ -238,9 +242,18 @@ struct GemmArgs {
     int64_t split_stride = 0;        // elements between split outputs
     int tile = -1;                   // general-kernel tile (-1 = automatic)
     int fast = -1;                   // fast-kernel tile (-1 = automatic, -2 = never)
+    // automatic split over K for products whose output tiles alone leave
+    // the chip idle: the remapped output must cover out_elems consecutive
+    // elements; the fp32 partials go to scratch (at most scratch_elems) and
+    // are summed in a fixed order into C
+    float *scratch = nullptr;
+    int64_t scratch_elems = 0;
+    int64_t out_elems = 0;
 };
 // C[rmap(m) + cmap(n)] = sum_k Aop(m, k) Bop(k, n); see gemm.hip.
 int launch_gemm(const GemmArgs &g, void *stream);
+// split count launch_gemm takes for an M x N x K product given scratch room
+int gemm_auto_splits(int64_t M, int64_t N, int64_t K);
 
 // Core contractions as GEMMs (gemm.hip).  A core copy Gc has layout
 // [A][nx][ny][C]; x runs over the factors of the left index X, y over those
@@ -284,6 +297,8 @@ int meet_gemm(const float *P, const float *En, float *part, int64_t NI, int64_t 
               int splits, void *stream);
 
 int launch_sum_splits(const float *part, float *out, int64_t n, int splits, void *stream);
+// the same sum rounded once to bf16
+int launch_sum_splits_bf16(const float *part, void *out, int64_t n, int splits, void *stream);
 int launch_fill_zero(void *ptr, size_t bytes, void *stream);
 int launch_fill_one(float *ptr, void *stream);
 

@@ -232,6 +232,17 @@ void layout_dense(comera_ttm_plan_s *p, bool with_dx) {
             off = align_up(off + sizeof(float) * size_t(L.dx_splits) * size_t(b) * size_t(p->N_in));
         }
     }
+    // forward and dX products with too few output tiles are split over K
+    if (with_dx) {
+        const int sf = gemm_auto_splits(b, p->N_out, p->N_in);
+        const int sx = L.dx_splits > 1 ? 1 : gemm_auto_splits(b, p->N_in, p->N_out);
+        const int64_t pe = std::max<int64_t>(sf > 1 ? sf * b * p->N_out : 0, sx > 1 ? sx * b * p->N_in : 0);
+        if (pe > 0) {
+            L.part = off;
+            L.part_elems = pe;
+            off = align_up(off + sizeof(float) * size_t(pe));
+        }
+    }
     L.proj = true;
     for (int k = 1; k < d; ++k) L.proj = L.proj && proj_supported(int(p->rho[k]));
     if (L.proj) {
@@ -446,6 +457,22 @@ bool layout_sweep(const comera_ttm_plan_s *p, int kind, uint32_t cuts, SweepLayo
     if (L.need_t) {
         L.tin = size_t(off);
         off += double(align_up(size_t(b * double(rl ? p->N_out : p->N_in) * double(esz))));
+    }
+    // split partials of the sweep products whose output tiles are too few
+    double pe = 0;
+    for (int g = 0; g < G; ++g) {
+        const double R = rl ? b * prod(L.N, 0, g) * prod(L.M, g + 1, G) : b * prod(L.M, 0, g) * prod(L.N, g + 1, G);
+        const double Kx = rl ? double(L.N[g] * L.ae[g]) : double(L.as[g] * L.N[g]);
+        const double Cx = rl ? double(L.as[g] * L.M[g]) : double(L.M[g] * L.ae[g]);
+        const int s1 = gemm_auto_splits(int64_t(R), int64_t(Cx), int64_t(Kx));
+        const int s2 = gemm_auto_splits(int64_t(R), int64_t(Kx), int64_t(Cx));
+        if (s1 > 1) pe = std::max(pe, s1 * R * Cx);
+        if (s2 > 1) pe = std::max(pe, s2 * R * Kx);
+    }
+    if (pe > 0) {
+        L.part = size_t(off);
+        L.part_elems = int64_t(pe);
+        off += double(align_up(size_t(pe * 4.0)));
     }
     if (off > kSweepCap) return false;
     L.total = size_t(off);

@@ -49,9 +49,10 @@ Remap remap2(int64_t r1, int64_t s0, int64_t s1) {
 }
 
 // out[rm(r) + cm(c)] = sum_k A[r][k] W(k, c), W = W'_g [K][C] (b_kc false) or
-// W'_g^T read from [C][K] (b_kc true)
-int step(const comera_ttm_plan_s *p, const void *A, int64_t R, int64_t K, const void *W, bool b_kc, int64_t C,
-         void *out, const Remap &rm, const Remap &cm, void *stream) {
+// W'_g^T read from [C][K] (b_kc true); the output covers R x C consecutive
+// elements, so a split over K can be summed elementwise
+int step(const comera_ttm_plan_s *p, void *ws, const void *A, int64_t R, int64_t K, const void *W, bool b_kc,
+         int64_t C, void *out, const Remap &rm, const Remap &cm, void *stream) {
     GemmArgs g;
     g.dtype = p->s.act;
     g.a_kc = true;
@@ -67,6 +68,11 @@ int step(const comera_ttm_plan_s *p, const void *A, int64_t R, int64_t K, const 
     g.ldb = b_kc ? K : C;
     g.rmap = rm;
     g.cmap = cm;
+    if (p->sweep.part_elems > 0) {
+        g.scratch = reinterpret_cast<float *>(at(ws, p->sweep.part));
+        g.scratch_elems = p->sweep.part_elems;
+        g.out_elems = R * C;
+    }
     return note_hip(launch_gemm(g, stream), b_kc ? "dY sweep GEMM" : "activation sweep GEMM");
 }
 
@@ -111,7 +117,7 @@ int sweep_x(const comera_ttm_plan_s *p, int64_t b, const void *X0, void *Y, void
             // row (q, i, t), column (a, m) -> Z_g [(q, m, t)][(i, a)]
             const Remap rm = remap3(Nn, T, L.M[g] * T * Nn * A, A, Nn * A);
             const Remap cm = remap2(L.M[g], 1, T * Nn * A);
-            if (int e = step(p, in, R, K, gr.bd[g].w, false, C, out, rm, cm, stream)) return e;
+            if (int e = step(p, ws, in, R, K, gr.bd[g].w, false, C, out, rm, cm, stream)) return e;
             in = out;
         }
         return 0;
@@ -126,7 +132,7 @@ int sweep_x(const comera_ttm_plan_s *p, int64_t b, const void *X0, void *Y, void
         // row (q, i, t), column (m, a) -> Z_{g+1} [(q, m, t)][(a, i)]
         const Remap rm = remap3(Nn, T, L.M[g] * T * A * Nn, 1, A * Nn);
         const Remap cm = remap2(A, T * A * Nn, Nn);
-        if (int e = step(p, in, R, K, gr.bd[g].w, false, C, out, rm, cm, stream)) return e;
+        if (int e = step(p, ws, in, R, K, gr.bd[g].w, false, C, out, rm, cm, stream)) return e;
         in = out;
     }
     return 0;
@@ -199,7 +205,7 @@ comera_status sweep_backward(const comera_ttm_plan_s *p, int64_t b, const void *
                 // row (q, m, t), column (i, a) -> H_{g+1} [(q, i, t)][(a, m)]
                 const Remap rm = remap3(Mn, T, L.N[g] * T * A * Mn, 1, A * Mn);
                 const Remap cm = remap2(A, T * A * Mn, Mn);
-                if (int e = step(p, in, R, K, gr.bd[g].w, true, C, out, rm, cm, stream)) return status_of(e);
+                if (int e = step(p, ws, in, R, K, gr.bd[g].w, true, C, out, rm, cm, stream)) return status_of(e);
                 in = out;
             }
         } else {
@@ -215,7 +221,7 @@ comera_status sweep_backward(const comera_ttm_plan_s *p, int64_t b, const void *
                 // row (q, m, t), column (a, i) -> H_{g-1} [(q, i, t)][(m, a)]
                 const Remap rm = remap3(Mp, T, L.N[g] * T * Mp * A, A, Mp * A);
                 const Remap cm = remap2(L.N[g], 1, T * Mp * A);
-                if (int e = step(p, in, R, K, gr.bd[g].w, true, C, out, rm, cm, stream)) return status_of(e);
+                if (int e = step(p, ws, in, R, K, gr.bd[g].w, true, C, out, rm, cm, stream)) return status_of(e);
                 in = out;
             }
         }

@@ -148,6 +148,15 @@ __global__ void sum_splits_kernel(const float *__restrict__ part, float *__restr
     }
 }
 
+__global__ void sum_splits_bf16_kernel(const float *__restrict__ part, uint16_t *__restrict__ out, int64_t n,
+                                       int splits) {
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
+        float v = 0.f;
+        for (int s = 0; s < splits; ++s) v += part[s * n + i];
+        out[i] = f32_to_bf16_rne(v);
+    }
+}
+
 // out[t][j][i] = in[t][i][j] (i < M, j < Tn) through a 32 x 33 LDS tile; the
 // workgroups stride over (token, row tile, column tile).
 template <typename T>
@@ -247,6 +256,12 @@ int launch_permute_tokens(const void *in, void *out, int64_t b, int64_t M, int64
         hipLaunchKernelGGL(permute_kernel<float>, dim3(grid), dim3(256), 0, hipStream_t(stream),
                            reinterpret_cast<const float *>(in), reinterpret_cast<float *>(out), b, int(M), int(T),
                            tm, tt);
+    return int(hipGetLastError());
+}
+
+int launch_sum_splits_bf16(const float *part, void *out, int64_t n, int splits, void *stream) {
+    hipLaunchKernelGGL(sum_splits_bf16_kernel, dim3(grid_for(n)), dim3(256), 0, hipStream_t(stream), part,
+                       reinterpret_cast<uint16_t *>(out), n, splits);
     return int(hipGetLastError());
 }
 

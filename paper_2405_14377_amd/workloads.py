@@ -89,6 +89,13 @@ WORKLOADS = {
                    (TTMLayerShape("up", (4, 8, 4, 8), (8, 8, 8, 8), (1, 64, 64, 64, 1)),
                     TTMLayerShape("down", (8, 8, 8, 8), (4, 8, 4, 8), (1, 64, 64, 64, 1))),
                    65536, ("bf16",), ("bernoulli", 0.7)),
+    # the paper's TT layout (Sec. 4.2): input cores [r, 1, n_k, r] then output
+    # cores [r, m_k, 1, r], i.e. a TTM layer with unit modes and a rank-30
+    # bond between the input and the output half
+    5: TTMWorkload(5, "tt_layout_768x3072_768x768_r30_b4096",
+                   (TTMLayerShape("tt_ffn_up", (8, 8, 12, 1, 1, 1), (1, 1, 1, 16, 16, 12), (1,) + (30,) * 5 + (1,)),
+                    TTMLayerShape("tt_qkvo", (8, 8, 12, 1, 1, 1), (1, 1, 1, 12, 8, 8), (1,) + (30,) * 5 + (1,))),
+                   4096, ("f32", "bf16"), ("bernoulli", 0.8)),
 }
 
 

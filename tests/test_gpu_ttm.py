@@ -149,7 +149,7 @@ def _workload_layer(wid, li, act, rows=None):
     return sh, inp, X, dY, mask_active
 
 
-@pytest.mark.parametrize("wid,act", [(0, "f32"), (1, "f32"), (1, "bf16")])
+@pytest.mark.parametrize("wid,act", [(0, "f32"), (1, "f32"), (1, "bf16"), (5, "f32"), (5, "bf16")])
 def test_workload_full_parity(wid, act):
     sh, inp, X, dY, mask_active = _workload_layer(wid, 0, act)
     errs = _check_layer(sh.n, sh.m, sh.r, inp.cores, inp.masks, X, dY, act, mask_active=mask_active)
