@@ -343,17 +343,18 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
-// KTB = bytes of K per LDS row (64 or 128), FP = KTB + 16 = LDS row pitch
-template <typename T, bool KC, int RT, int KTB>
+// KTB = bytes of K per LDS row (64 or 128), FP = KTB + 16 = LDS row pitch;
+// NT threads share the loads
+template <typename T, bool KC, int RT, int KTB, int NT = 256>
 struct FastLoader {
     static constexpr int FP = KTB + 16;
     static constexpr int E = GemmCfg<T>::E;
     static constexpr int KT = KTB / int(sizeof(T));
     static constexpr int CPR = KTB / 16;
-    static constexpr int NKC = (RT * CPR + 255) / 256;
+    static constexpr int NKC = (RT * CPR + NT - 1) / NT;
     static constexpr int KP = KT / 2;
     static constexpr int MG = sizeof(T) == 2 ? 8 : 4;
-    static constexpr int NMB = (KP * (RT / MG) + 255) / 256;
+    static constexpr int NMB = (KP * (RT / MG) + NT - 1) / NT;
     static constexpr int NV = KC ? NKC : 2 * NMB;
     u32x4 v[NV];
     uint32_t off[NV];
@@ -362,14 +363,14 @@ struct FastLoader {
         if constexpr (KC) {
 #pragma unroll
             for (int j = 0; j < NKC; ++j) {
-                const int c = min(tid + 256 * j, RT * CPR - 1);
+                const int c = min(tid + NT * j, RT * CPR - 1);
                 const int64_t row = min(r0 + c / CPR, R - 1);
                 off[j] = uint32_t((row * ld + (c % CPR) * E) * int64_t(sizeof(T)));
             }
         } else {
 #pragma unroll
             for (int j = 0; j < NMB; ++j) {
-                const int id = min(tid + 256 * j, KP * (RT / MG) - 1);
+                const int id = min(tid + NT * j, KP * (RT / MG) - 1);
                 const int kp = id % KP, mg = id / KP;
                 const int64_t row = min(r0 + MG * mg, R - MG);
                 off[2 * j] = uint32_t(((2 * kp) * ld + row) * int64_t(sizeof(T)));
@@ -385,15 +386,15 @@ struct FastLoader {
         if constexpr (KC) {
 #pragma unroll
             for (int j = 0; j < NKC; ++j) {
-                const int c = tid + 256 * j;
-                if (RT * CPR % 256 == 0 || c < RT * CPR)
+                const int c = tid + NT * j;
+                if (RT * CPR % NT == 0 || c < RT * CPR)
                     *reinterpret_cast<u32x4 *>(lds + (c / CPR) * FP + (c % CPR) * 16) = v[j];
             }
         } else {
 #pragma unroll
             for (int j = 0; j < NMB; ++j) {
-                const int id = tid + 256 * j;
-                if (KP * (RT / MG) % 256 == 0 || id < KP * (RT / MG)) {
+                const int id = tid + NT * j;
+                if (KP * (RT / MG) % NT == 0 || id < KP * (RT / MG)) {
                     const int kp = id % KP, mg = id / KP;
                     if constexpr (sizeof(T) == 2) {
                         // element e of the two k rows -> one dword (k even low, k odd high)
@@ -418,13 +419,13 @@ struct FastLoader {
     }
 };
 
-template <typename T, bool A_KC, bool B_KC, bool OUT_BF16, int BM, int BN, int WM, int WN, int KTB>
-__global__ __launch_bounds__(256) void gemm_fast_kernel(GemmParams p) {
+template <typename T, bool A_KC, bool B_KC, bool OUT_BF16, int BM, int BN, int WM, int WN, int KTB, int NT = 256>
+__global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
     constexpr int FP = KTB + 16;
     constexpr int KT = KTB / int(sizeof(T));
     constexpr int WAVES_N = BN / WN;
     constexpr int TM = WM / 32, TN = WN / 32;
-    static_assert((BM / WM) * (BN / WN) == 4, "four waves per workgroup");
+    static_assert((BM / WM) * (BN / WN) * 64 == NT, "one wave per WM x WN block");
     extern __shared__ __attribute__((aligned(16))) char smem[];
     char *sA0 = smem;
     char *sA1 = smem + BM * FP;
@@ -452,16 +453,16 @@ __global__ __launch_bounds__(256) void gemm_fast_kernel(GemmParams p) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    FastLoader<T, A_KC, BM, KTB> la;
-    FastLoader<T, B_KC, BN, KTB> lb;
+    FastLoader<T, A_KC, BM, KTB, NT> la;
+    FastLoader<T, B_KC, BN, KTB, NT> lb;
     la.setup(p.lda, m0, p.M, tid);
     lb.setup(p.ldb, n0, p.N, tid);
     if (ntiles > 0) {
         la.load(abase);
         lb.load(bbase);
     }
-    for (int i = tid; i < BM; i += 256) roff[i] = m0 + i < p.M ? remap(p.rmap, m0 + i) : int64_t(-1);
-    for (int i = tid; i < BN; i += 256) coff[i] = n0 + i < p.N ? remap(p.cmap, n0 + i) : int64_t(-1);
+    for (int i = tid; i < BM; i += NT) roff[i] = m0 + i < p.M ? remap(p.rmap, m0 + i) : int64_t(-1);
+    for (int i = tid; i < BN; i += NT) coff[i] = n0 + i < p.N ? remap(p.cmap, n0 + i) : int64_t(-1);
     if (ntiles > 0) {
         la.store(sA0, tid);
         lb.store(sB0, tid);
@@ -594,12 +595,16 @@ int pick_tile(int64_t M, int64_t N, int splits) {
 
 
 // Fast-path tiles: {BM, BN, K bytes per LDS row}.
-enum FastId { F128x128_128 = 0, F128x64_128, F64x128_128, F128x128_64, F256x128_64 };
+enum FastId {
+    F128x128_128 = 0, F128x64_128, F64x128_128, F128x128_64, F256x128_64,
+    // bf16 only, eight waves: 256 x 256 (waves of 128 x 64), 256 x 128 (64 x 64)
+    F256x256_128w8, F256x128_128w8
+};
 
-template <typename T, bool AK, bool BK, bool OB, int BM, int BN, int WM, int WN, int KTB>
+template <typename T, bool AK, bool BK, bool OB, int BM, int BN, int WM, int WN, int KTB, int NT = 256>
 int go_fast(const GemmArgs &g, const GemmParams &p, void *stream) {
     constexpr size_t lds = size_t(2) * (BM + BN) * (KTB + 16) + size_t(BM + BN) * sizeof(int64_t);
-    auto kern = gemm_fast_kernel<T, AK, BK, OB, BM, BN, WM, WN, KTB>;
+    auto kern = gemm_fast_kernel<T, AK, BK, OB, BM, BN, WM, WN, KTB, NT>;
     // above the default 64 KB of dynamic LDS: raise the limit once per kernel
     static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                                    hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
@@ -608,7 +613,7 @@ int go_fast(const GemmArgs &g, const GemmParams &p, void *stream) {
     const dim3 grid = tile_grid(g, BM, BN, q);
     if (!grid.x) return int(hipErrorInvalidConfiguration);
     q.gw = choose_gw(g, BM, BN, g.splits);
-    hipLaunchKernelGGL(kern, grid, dim3(256), lds, hipStream_t(stream), q);
+    hipLaunchKernelGGL(kern, grid, dim3(NT), lds, hipStream_t(stream), q);
     return int(hipGetLastError());
 }
 
@@ -621,6 +626,12 @@ int launch_fast(const GemmArgs &g, const GemmParams &p, int id, void *stream) {
         case F128x128_64: return go_fast<T, AK, BK, OB, 128, 128, 64, 64, 64>(g, p, stream);
         case F256x128_64: return go_fast<T, AK, BK, OB, 256, 128, 128, 64, 64>(g, p, stream);
     }
+    if constexpr (sizeof(T) == 2) {
+        switch (id) {
+            case F256x256_128w8: return go_fast<T, AK, BK, OB, 256, 256, 128, 64, 128, 512>(g, p, stream);
+            case F256x128_128w8: return go_fast<T, AK, BK, OB, 256, 128, 64, 64, 128, 512>(g, p, stream);
+        }
+    }
     return int(hipErrorInvalidValue);
 }
 
@@ -630,6 +641,11 @@ int launch_fast(const GemmArgs &g, const GemmParams &p, int id, void *stream) {
 // chip with these tiles (the general kernel's smaller tiles do better).
 int pick_fast(const GemmArgs &g, int splits) {
     const int64_t t128 = ceil_div(g.M, 128) * ceil_div(g.N, 128) * splits;
+    const int64_t t256 = ceil_div(g.M, 256) * ceil_div(g.N, 256) * splits;
+    // bf16: 256 x 256 tiles of eight waves once they give two or more
+    // workgroups per CU (transposed operands, split over K: half a wave of
+    // workgroups is enough)
+    if (g.dtype == COMERA_BF16 && g.a_kc == g.b_kc && t256 >= (g.a_kc ? 512 : 128)) return F256x256_128w8;
     if (g.a_kc && g.b_kc) {
         // fp32 tiles of 128 x 128 fit three workgroups per CU with 64-byte rows
         if (g.dtype == COMERA_F32 && t128 >= 240) return F128x128_64;
@@ -724,6 +740,7 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     GemmParams pf = p;
     if (fast >= 0) {
         const int ktb = (fast == F128x128_64 || fast == F256x128_64) ? 64 : 128;
+        if (fast >= F256x256_128w8 && g.dtype != COMERA_BF16) fast = -1;
         const int64_t kt = ktb / (g.dtype == COMERA_BF16 ? 2 : 4);
         pf.kchunk = ceil_div(p.kchunk, kt) * kt;
         if (!fast_ok(gg, pf.kchunk, ktb)) fast = -1;

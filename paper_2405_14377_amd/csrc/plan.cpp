@@ -22,7 +22,7 @@ namespace {
 constexpr double kPeakF32 = 157.3e12;    // MI355X dense fp32 (vector and MFMA)
 constexpr double kPeakBF16 = 2.5e15;     // MI355X dense bf16 MFMA
 constexpr double kHbm = 8.0e12;          // MI355X HBM3E bytes/s
-constexpr double kLaunch = 2.0e-6;       // cost charged per kernel launch
+constexpr double kLaunch = 6.0e-6;       // cost of one small kernel launch (measured 5-10 us back to back)
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -208,6 +208,24 @@ void layout_dense(comera_ttm_plan_s *p, bool with_dx) {
     int64_t b = std::max<int64_t>(p->batch, 1);
     int64_t splits = std::max<int64_t>(1, (512 + tiles - 1) / tiles);
     if (p->s.act == COMERA_F32) splits = std::max<int64_t>(1, (768 + tiles / 2) / tiles);
+    // bf16 (256 x 256 tiles): the split count minimising a measured model,
+    // waves of tiles x tokens per split x 40 ns plus writing and reading
+    // back the split partials at 4 TB/s
+    if (p->s.act == COMERA_BF16 && p->N_in >= 256 && p->N_out >= 256) {
+        const int64_t t256 = ((p->N_in + 255) / 256) * ((p->N_out + 255) / 256);
+        double best = -1.0;
+        for (int64_t s = 1; s <= 64; ++s) {
+            const int64_t kc = ((b + s - 1) / s + 63) / 64 * 64;
+            const int64_t sp = (b + kc - 1) / kc;
+            if (sp != s) continue;
+            const double rounds = double((t256 * s + 255) / 256);
+            const double t = rounds * double(kc) * 40e-9 + 2.0 * double(s) * double(p->N_in * p->N_out) * 4.0 / 4e12;
+            if (best < 0 || t < best) {
+                best = t;
+                splits = s;
+            }
+        }
+    }
     splits = std::min<int64_t>(splits, std::max<int64_t>(1, b / 256));
     splits = std::min<int64_t>(splits, 64);
     int64_t kchunk = (b + splits - 1) / splits;
