@@ -66,19 +66,22 @@ class Layer:
         self.sh, self.X, self.dY, self.G, self.D, self.b, self.act = sh, X, dY, G, D, b, act
         self.plan = C.TTMPlan(sh.n, sh.m, sh.r, C.BF16 if act == "bf16" else C.F32, batch=b,
                               mask_active=mask_active, force_order=force_order)
+        # a training step: the backward follows the forward on the same
+        # workspace and cores, so it takes the forward's W and core copies
+        self.plan.set_reuse_forward(True)
         dev = X.device
         self.ws = torch.empty(self.plan.workspace_bytes, dtype=torch.uint8, device=dev)
         self.Y = torch.empty((b, sh.n_out), dtype=X.dtype, device=dev)
         self.dX = torch.empty((b, sh.n_in), dtype=X.dtype, device=dev)
         self.dG = [torch.empty_like(g) for g in G]
-        self.stream = torch.cuda.current_stream().cuda_stream
 
+    # every call goes to the caller's current stream
     def forward(self):
-        self.C.comera_ttm_forward(self.plan.handle, self.b, self.X, self.G, self.D, self.Y, self.ws, self.stream)
+        self.C.comera_ttm_forward(self.plan.handle, self.b, self.X, self.G, self.D, self.Y, self.ws, None)
 
     def backward(self):
         self.C.comera_ttm_backward(self.plan.handle, self.b, self.X, self.dY, self.G, self.D, self.dX, self.dG,
-                                   self.ws, self.stream)
+                                   self.ws, None)
 
     def step(self):
         self.forward()
@@ -100,6 +103,25 @@ def time_loop(fn, steps, warmup):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     return e0.elapsed_time(e1) / steps, wall
+
+
+def graph_loop(fn, steps, warmup):
+    """Capture one call of fn as a HIP graph on the current stream and time
+    `steps` replays of it (after `warmup` replays).  Returns (ms per replay,
+    None) or (None, reason) when the capture fails."""
+    import torch
+    s = torch.cuda.current_stream()
+    fn()                      # lazy initialisation happens outside the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    try:
+        with torch.cuda.graph(g, stream=s):
+            fn()
+    except Exception as e:   # reported, never silently replaced by the eager time
+        return None, f"capture failed: {type(e).__name__}: {e}"[:200]
+    ms, _ = time_loop(g.replay, steps, warmup)
+    del g
+    return ms, None
 
 
 def dense_step_fn(sh, X, dY):
@@ -271,6 +293,17 @@ def cpu_baseline(min_seconds=10.0):
 
 
 # ------------------------------------------------------------------ other workloads
+def graph_entry(gms, gerr, dgms, dgerr):
+    """Graph-replay figures of one step (ours and the dense baseline's)."""
+    e = {"ms_per_step": None if gms is None else round(gms, 5),
+         "dense_ms_per_step": None if dgms is None else round(dgms, 5)}
+    if gms is not None and dgms is not None:
+        e["speedup_vs_dense"] = round(dgms / gms, 3)
+    if gerr or dgerr:
+        e["error"] = gerr or dgerr
+    return e
+
+
 def other_workloads(steps, warmup):
     import numpy as np
     import torch
@@ -288,6 +321,8 @@ def other_workloads(steps, warmup):
         k = steps if wid != 4 else max(3, steps // 4)
         ms, _ = time_loop(lambda: [l.step() for l in layers], k, warmup)
         dms, _ = time_loop(lambda: [f() for f in dense], k, warmup)
+        gms, gerr = graph_loop(lambda: [l.step() for l in layers], k, warmup)
+        dgms, dgerr = graph_loop(lambda: [f() for f in dense], k, warmup)
         fl = sum(6.0 * l.b * l.sh.n_in * l.sh.n_out for l in layers)
         fl_alg = 0.0
         for l in layers:
@@ -297,7 +332,8 @@ def other_workloads(steps, warmup):
                  "ms_per_step": round(ms, 4), "tokens_per_s": round(w.batch / (ms * 1e-3), 1),
                  "tflops_gemm_equiv": round(fl / (ms * 1e-3) / 1e12, 2),
                  "tflops_algorithmic": round(fl_alg / (ms * 1e-3) / 1e12, 2),
-                 "dense_ms_per_step": round(dms, 4), "speedup_vs_dense": round(dms / ms, 3)}
+                 "dense_ms_per_step": round(dms, 4), "speedup_vs_dense": round(dms / ms, 3),
+                 "graph": graph_entry(gms, gerr, dgms, dgerr)}
         if wid in (1, 2, 4):
             roofs = [kernel_roofline(l, max(2, k // 2), act)[1] for l in layers]
             entry["kernels_ms"] = [{t: round(v["avg_ms"], 4) for t, v in r.items()} for r in roofs]
@@ -321,7 +357,7 @@ def other_workloads(steps, warmup):
     table.requires_grad_(True)
     for dist in ("zipf1.1", "uniform"):
         ids = torch.from_numpy(wl.token_ids(n, V, dist, wl.seed_of(3, 20))).to(dev)
-        stream = torch.cuda.current_stream().cuda_stream
+        stream = None             # the current stream
 
         def step():
             C.comera_tt_embed_forward(shape, ids, n, cores, None, Y, ws, None, stream)
@@ -338,12 +374,14 @@ def other_workloads(steps, warmup):
         ms, _ = time_loop(step, steps, warmup)
         fms, _ = time_loop(fstep, steps, warmup)
         dms, _ = time_loop(dense, steps, warmup)
+        gms, gerr = graph_loop(step, steps, warmup)
         byt = 2.0 * n * E * 4            # output write + dY read (algorithmic floor)
         res[f"w3_{dist}"] = {"workload": w.name, "dtype": "f32", "tokens": n, "ms_per_step": round(ms, 4),
                              "fwd_ms": round(fms, 4), "tokens_per_s": round(n / (ms * 1e-3), 1),
                              "gbps_floor_bytes": round(byt / (ms * 1e-3) / 1e9, 1),
                              "hbm_frac": round(byt / (ms * 1e-3) / HBM_PEAK, 4),
-                             "dense_ms_per_step": round(dms, 4), "speedup_vs_dense": round(dms / ms, 3)}
+                             "dense_ms_per_step": round(dms, 4), "speedup_vs_dense": round(dms / ms, 3),
+                             "graph": graph_entry(gms, gerr, None, None)}
     return res
 
 
@@ -427,6 +465,16 @@ def main():
         sys.exit(1)
     from paper_2405_14377_amd import comera as C
     C.load()
+    # every GPU call, ours and the baselines', goes to one dedicated stream
+    # of default priority (the legacy null stream adds per-launch cost)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        run_gpu(args)
+        torch.cuda.synchronize()
+
+
+def run_gpu(args):
+    import torch
     if args.orders is not None:
         wids = args.orders or [0, 1, 5]
         for rec in order_timings(wids, args.steps, args.warmup):
@@ -439,11 +487,17 @@ def main():
         log(f"[bench] ttm 768x3072 {act}: warmup {args.warmup}, timing {args.steps} steps")
         torch.cuda.synchronize()
         ms, wall = time_loop(layer.step, args.steps, args.warmup)
-        dms, _ = time_loop(dense_step_fn(sh, X, dY), args.steps, args.warmup)
+        dfn = dense_step_fn(sh, X, dY)
+        dms, _ = time_loop(dfn, args.steps, args.warmup)
+        gms, gerr = graph_loop(layer.step, args.steps, args.warmup)
+        dgms, dgerr = graph_loop(dfn, args.steps, args.warmup)
         roof, kern = kernel_roofline(layer, args.steps, act)
         runs[act] = {"ms_per_step": ms, "wall_s": wall, "tokens_per_s": b / (ms * 1e-3), "dense_ms": dms,
                      "speedup_vs_dense": dms / ms, "roofline": roof,
-                     "kernels_ms": {t: round(v["avg_ms"], 5) for t, v in kern.items()}}
+                     "kernels_ms": {t: round(v["avg_ms"], 5) for t, v in kern.items()},
+                     "graph": graph_entry(gms, gerr, dgms, dgerr)}
+        if gms is not None:
+            runs[act]["graph"]["tokens_per_s"] = round(b / (gms * 1e-3), 1)
         log(f"[bench]   {ms:.4f} ms/step, dense {dms:.4f} ms, dominant {roof['kernel']} {roof['achieved']} TF/s")
         del layer
         torch.cuda.empty_cache()
@@ -468,13 +522,15 @@ def main():
         "speedup_vs_dense_gemm": round(main_run["speedup_vs_dense"], 3),
         "dense_gemm_ms_per_step": round(main_run["dense_ms"], 5),
         "kernels_ms": main_run["kernels_ms"],
+        "graph_replay": main_run["graph"],
+        "stream": "one dedicated stream (default priority) for every GPU call, ours and the baseline's",
     }
     other = "bf16" if args.dtype == "f32" else "f32"
     r = runs[other]
     out[f"{other}_run"] = {"value": round(r["tokens_per_s"], 1), "ms_per_step": round(r["ms_per_step"], 5),
                            "speedup_vs_dense_gemm": round(r["speedup_vs_dense"], 3),
                            "dense_gemm_ms_per_step": round(r["dense_ms"], 5), "roofline": r["roofline"],
-                           "kernels_ms": r["kernels_ms"]}
+                           "kernels_ms": r["kernels_ms"], "graph_replay": r["graph"]}
     if args.calib_copy:
         calib_copy()
     if not args.no_extra:

@@ -124,7 +124,7 @@ comera_status comera_ttm_plan_order_info(comera_ttm_plan_t p, int32_t i, char *d
 
 /* Device workspace (bytes) that forward and backward need for this plan at
  * its planned batch.  Forward and backward may use the same buffer; no state
- * is carried from forward to backward. */
+ * is carried from forward to backward unless reuse is switched on (below). */
 size_t comera_ttm_workspace_bytes(comera_ttm_plan_t p);
 
 /* Y[b, N_out] = X[b, N_in] W  (Sec. 4.2 eq. forward).
@@ -147,6 +147,20 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
                                   void *ws, size_t ws_bytes, void *stream);
 
 void comera_ttm_plan_destroy(comera_ttm_plan_t p);
+
+/* Reuse of the forward's batch-free work in the backward call, as a
+ * training step saves forward intermediates for its backward pass (the
+ * contraction paths of Sec. 4.2 keep their forward results for the
+ * gradients).  With enable != 0, comera_ttm_forward of the dense order also
+ * writes W in the layout that dX reads, and comera_ttm_backward takes the
+ * masked cores, left chains and W from the workspace instead of rebuilding
+ * them.  The caller then guarantees that every backward call follows a
+ * forward call of this plan on the same workspace with the same G and D,
+ * with no other call of this plan on that workspace in between; otherwise
+ * the results are undefined (no error can be detected).  Sweep orders
+ * ignore the setting.  Off by default; host only, no device work.
+ * Returns COMERA_ERR_INVALID_ARG for a NULL plan. */
+comera_status comera_ttm_plan_set_reuse_forward(comera_ttm_plan_t p, int32_t enable);
 
 /* Diagnostics: per-kernel timing of the batch products of a plan.  While
  * enabled, forward and backward record a pair of HIP events on the call's

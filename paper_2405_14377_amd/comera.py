@@ -26,7 +26,7 @@ EXPORTS = (
     "comera_ttm_plan_order_info", "comera_ttm_workspace_bytes", "comera_ttm_forward",
     "comera_ttm_backward", "comera_ttm_plan_destroy", "comera_tt_embed_workspace_bytes",
     "comera_tt_embed_forward", "comera_tt_embed_backward", "comera_status_string", "comera_last_hip_error",
-    "comera_ttm_plan_set_timing", "comera_ttm_plan_kernel_time",
+    "comera_ttm_plan_set_timing", "comera_ttm_plan_kernel_time", "comera_ttm_plan_set_reuse_forward",
 )
 KERNEL_FWD, KERNEL_DX, KERNEL_DW = 0, 1, 2
 
@@ -95,6 +95,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comera_tt_embed_backward.argtypes = [P(comera_tt_embed_shape), vp, i64, vp, vp, vp, vp, i32, vp, sz, vp, vp]
     lib.comera_tt_embed_backward.restype = i32
     lib.comera_ttm_plan_set_timing.argtypes = [vp, i32]
+    lib.comera_ttm_plan_set_reuse_forward.argtypes = [vp, i32]
+    lib.comera_ttm_plan_set_reuse_forward.restype = i32
     lib.comera_ttm_plan_set_timing.restype = i32
     lib.comera_ttm_plan_kernel_time.argtypes = [vp, i32, P(dbl), P(i32)]
     lib.comera_ttm_plan_kernel_time.restype = i32
@@ -240,6 +242,10 @@ def comera_ttm_plan_set_timing(plan, enable: bool) -> None:
     _check(load().comera_ttm_plan_set_timing(plan, int(bool(enable))), "comera_ttm_plan_set_timing")
 
 
+def comera_ttm_plan_set_reuse_forward(plan, enable: bool) -> None:
+    _check(load().comera_ttm_plan_set_reuse_forward(plan, int(bool(enable))), "comera_ttm_plan_set_reuse_forward")
+
+
 def comera_ttm_plan_kernel_time(plan, kernel: int):
     """(mean ms, launches) of one kernel since the last query; clears the record."""
     ms, cnt = ctypes.c_double(), ctypes.c_int32()
@@ -290,6 +296,9 @@ class TTMPlan:
 
     def order_info(self, i: int) -> dict:
         return comera_ttm_plan_order_info(self.handle, i)
+
+    def set_reuse_forward(self, enable: bool = True) -> None:
+        comera_ttm_plan_set_reuse_forward(self.handle, enable)
 
     def __del__(self):
         try:

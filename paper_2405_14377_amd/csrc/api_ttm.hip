@@ -56,54 +56,70 @@ int fold_cores(const comera_ttm_plan_s *p, const float *const *G, const float *c
 }
 
 // Left chains P_1..P_{d-1} and W (eq. TTM) as one GEMM per core from the
-// folded cores; the last step writes W[N_in, N_out] (or, with transpose,
-// W^T[N_out, N_in]) in the activation dtype.
-int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, bool transpose, void *stream) {
+// folded cores; the last step writes W[N_in, N_out] (want & kWantW) and / or
+// W^T[N_out, N_in] (want & kWantWT) in the activation dtype.
+int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, int want, void *stream) {
     const DenseLayout &L = sp->dense;
     const int d = sp->d;
     const bool bf = sp->s.act == COMERA_BF16;
     bd.w = at(ws, L.w);
+    bd.wt = at(ws, L.wt);
     if (d == 1) {
         // W = G_0[0, :, :, 0]^T: the folded core [n][m] itself in fp32, else
         // a GEMM with a single 1 on the left
-        if (!bf && !transpose) {
+        if (!bf && want == kWantW) {
             bd.w = bd.gc[0];
             return 0;
         }
         float *ones = reinterpret_cast<float *>(at(ws, L.ones));
         int e = note_hip(launch_fill_one(ones, stream), "fill");
-        if (e) return e;
-        return note_hip(chain_gemm(ones, bd.gc[0], bd.w, bf, 1, 1, 1, int(sp->s.n[0]), int(sp->s.m[0]), 1, stream,
-                                   transpose ? kChainT : kChainNormal),
-                        "chain GEMM");
+        for (int t = 0; t < 2 && !e; ++t) {
+            const bool tr = t == 1;
+            if (!(want & (tr ? kWantWT : kWantW))) continue;
+            e = note_hip(chain_gemm(ones, bd.gc[0], tr ? bd.wt : bd.w, bf, 1, 1, 1, int(sp->s.n[0]),
+                                    int(sp->s.m[0]), 1, stream, tr ? kChainT : kChainNormal),
+                         "chain GEMM");
+        }
+        return e;
     }
     bd.P[1] = bd.gc[0];  // rho_0 = 1: [n_0][m_0][rho_1] is the folded core itself
     int64_t Il = sp->s.n[0], Jl = sp->s.m[0];
     for (int k = 1; k < d; ++k) {
         const bool last = k == d - 1;
-        void *out = last ? bd.w : at(ws, L.p[k + 1]);
-        int qb = 0;
-        if (last && wbuild_tiles(Il, Jl, int(sp->rho[k]), int(sp->s.n[k]), int(sp->s.m[k]), transpose, qb)) {
+        if (!last) {
+            void *out = at(ws, L.p[k + 1]);
+            int e = chain_gemm(bd.P[k], bd.gc[k], out, false, Il, Jl, int(sp->rho[k]), int(sp->s.n[k]),
+                               int(sp->s.m[k]), int(sp->rho[k + 1]), stream, kChainNormal);
+            if (e) return note_hip(e, "chain GEMM");
+            bd.P[k + 1] = reinterpret_cast<float *>(out);
+            Il *= sp->s.n[k];
+            Jl *= sp->s.m[k];
+            continue;
+        }
+        int qi = 0, qj = 0;
+        if (wbuild_tiles(Il, Jl, int(sp->rho[k]), int(sp->s.n[k]), int(sp->s.m[k]), qi, qj)) {
             WBuildArgs wa;
             wa.P = bd.P[k];
             wa.G = bd.gc[k];
-            wa.out = out;
+            wa.out = (want & kWantW) ? bd.w : nullptr;
+            wa.out_t = (want & kWantWT) ? bd.wt : nullptr;
             wa.NI = Il;
             wa.NJ = Jl;
             wa.A = int(sp->rho[k]);
             wa.nx = int(sp->s.n[k]);
             wa.ny = int(sp->s.m[k]);
-            wa.transpose = transpose ? 1 : 0;
             wa.out_bf16 = bf ? 1 : 0;
-            wa.QB = qb;
+            wa.QI = qi;
+            wa.QJ = qj;
             return note_hip(launch_wbuild(wa, stream), "W build");
         }
-        int e = chain_gemm(bd.P[k], bd.gc[k], out, last && bf, Il, Jl, int(sp->rho[k]), int(sp->s.n[k]),
-                           int(sp->s.m[k]), int(sp->rho[k + 1]), stream, last && transpose ? kChainT : kChainNormal);
-        if (e) return note_hip(e, "chain GEMM");
-        if (!last) bd.P[k + 1] = reinterpret_cast<float *>(out);
-        Il *= sp->s.n[k];
-        Jl *= sp->s.m[k];
+        for (int t = 0; t < 2; ++t) {
+            const bool tr = t == 1;
+            if (!(want & (tr ? kWantWT : kWantW))) continue;
+            int e = chain_gemm(bd.P[k], bd.gc[k], tr ? bd.wt : bd.w, bf, Il, Jl, int(sp->rho[k]), int(sp->s.n[k]),
+                               int(sp->s.m[k]), int(sp->rho[k + 1]), stream, tr ? kChainT : kChainNormal);
+            if (e) return note_hip(e, "chain GEMM");
+        }
     }
     return 0;
 }
@@ -281,12 +297,21 @@ void dense_strides(const comera_ttm_plan_s *p, CoreStrides *st) {
 
 // fold, chains and W of the dense order
 int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *const *D, void *ws, void *stream,
-                DenseBuild &bd, bool transpose) {
+                DenseBuild &bd, int want) {
     dense_ptrs(p, ws, bd);
     CoreStrides st[kMaxCores];
     dense_strides(p, st);
     if (int e = fold_cores(p, G, D, bd.gc, st, stream)) return e;
-    return build_chain(p, ws, bd, transpose, stream);
+    return build_chain(p, ws, bd, want, stream);
+}
+
+// pointers of a build that an earlier forward call left in the workspace
+void built_dense(const comera_ttm_plan_s *p, void *ws, DenseBuild &bd) {
+    dense_ptrs(p, ws, bd);
+    bd.P[1] = bd.gc[0];
+    for (int k = 1; k + 1 < p->d; ++k) bd.P[k + 1] = reinterpret_cast<float *>(at(ws, p->dense.p[k + 1]));
+    bd.w = at(ws, p->dense.w);
+    bd.wt = at(ws, p->dense.wt);
 }
 
 }  // namespace
@@ -345,7 +370,8 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, 
     if (!ws || ws_bytes < p->ws_bytes) return COMERA_ERR_WORKSPACE;
     if (p->sweep.G > 0) return sweep_forward(p, b, X, G, D, Y, ws, stream);
     DenseBuild bd;
-    int e = build_dense(p, G, D, ws, stream, bd, true);
+    // W^T for the forward product; with reuse also W for the backward call
+    int e = build_dense(p, G, D, ws, stream, bd, kWantWT | (p->reuse ? kWantW : 0));
     if (e) return COMERA_ERR_HIP;
     // Y[b, N_out] = X[b, N_in] W (eq. forward), W^T read row by row
     void *ev;
@@ -356,7 +382,7 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, 
     g.b_kc = true;
     g.out_bf16 = p->s.act == COMERA_BF16;
     g.A = X;
-    g.B = bd.w;
+    g.B = bd.wt;
     g.C = Y;
     g.M = b;
     g.N = p->N_out;
@@ -401,7 +427,11 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
     if (p->sweep.G > 0) return sweep_backward(p, b, X, dY, G, D, dX, dG, ws, stream);
     const DenseLayout &L = p->dense;
     DenseBuild bd;
-    int e = build_dense(p, G, D, ws, stream, bd, false);
+    int e = 0;
+    if (p->reuse)
+        built_dense(p, ws, bd);
+    else
+        e = build_dense(p, G, D, ws, stream, bd, kWantW);
     if (e) return COMERA_ERR_HIP;
     if (dX) {
         // dX[b, N_in] = dY[b, N_out] W^T  (eq. back X)
@@ -461,6 +491,12 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
     CoreStrides st[kMaxCores];
     dense_strides(p, st);
     return expand_cores(p, part, nsplit, st, D, dG, stream) ? COMERA_ERR_HIP : COMERA_OK;
+}
+
+comera_status comera_ttm_plan_set_reuse_forward(comera_ttm_plan_t p, int32_t enable) {
+    if (!p) return COMERA_ERR_INVALID_ARG;
+    p->reuse = enable != 0;
+    return COMERA_OK;
 }
 
 comera_status comera_ttm_plan_set_timing(comera_ttm_plan_t p, int32_t enable) {

@@ -42,6 +42,7 @@ struct DenseLayout {
     size_t gc[kMaxCores];      // compacted, mask-folded cores (fp32)
     size_t p[kMaxCores + 1];   // left chains P_k, k = 1..d-1 (fp32); p[d] unused
     size_t w;                  // W [N_in, N_out] in the activation dtype
+    size_t wt;                 // W^T [N_out, N_in] in the activation dtype
     size_t ones;               // a single 1.0f (left operand of the d = 1 build)
     size_t dw_part;            // split-K partials of dW (fp32)
     size_t dw;                 // dW (fp32)
@@ -123,6 +124,7 @@ struct comera_ttm_plan_s {
     comera::SweepLayout sweep;                    // when the chosen order is a sweep
     std::unique_ptr<comera_ttm_plan_s> sub[comera::kMaxCores];   // one layer per sweep group
     size_t ws_bytes = 0;
+    bool reuse = false;                           // backward reuses the forward's build
     comera::KernelTiming timing;
 };
 
@@ -213,19 +215,20 @@ void proj_tiles(int64_t rows, int64_t cols, int A, int &RT, int &CT);
 bool proj_supported(int A);
 int launch_proj(const ProjArgs &a, void *stream);
 
-// Last step of the W rebuild (proj.hip): out = W [N_in][N_out] or W^T
-// [N_out][N_in] from P_{d-1} [NI][NJ][A] and the folded last core [A][nx][ny].
+// Last step of the W rebuild (proj.hip): W [N_in][N_out] to out and / or
+// W^T [N_out][N_in] to out_t (either may be null) from P_{d-1} [NI][NJ][A]
+// and the folded last core [A][nx][ny], in tiles of QI x QJ prefixes.
 struct WBuildArgs {
     const float *P;
     const float *G;
     void *out;
+    void *out_t;
     int64_t NI, NJ;
     int A, nx, ny;
-    int transpose;
     int out_bf16;
-    int QB;
+    int QI, QJ;
 };
-bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, bool transpose, int &QB);
+bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, int &QI, int &QJ);
 int launch_wbuild(const WBuildArgs &a, void *stream);
 
 
@@ -287,6 +290,30 @@ __device__ __forceinline__ void stage_lds(float *dst, int count, int t0, int nt,
         }
     }
 }
+// Two regions staged together (one memory round trip when countA + countB
+// <= U * nt): element i < countA goes to dstA[i] = srcA(i), the rest to
+// dstB[i - countA] = srcB(i - countA).
+template <int U, class SrcA, class SrcB>
+__device__ __forceinline__ void stage2_lds(float *dstA, int countA, SrcA srcA, float *dstB, int countB, SrcB srcB,
+                                           int t0, int nt) {
+    const int count = countA + countB;
+    for (int i0 = t0; i0 < count; i0 += nt * U) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * nt;
+            v[u] = i < countA ? srcA(i) : (i < count ? srcB(i - countA) : 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * nt;
+            if (i < countA)
+                dstA[i] = v[u];
+            else if (i < count)
+                dstB[i - countA] = v[u];
+        }
+    }
+}
 // With splits > 1 the split partials go to `scratch` (splits * NI * NJ * A
 // floats) and are summed into `out` in a fixed order.
 int adjoint_gemm(const float *En, const float *Gc, float *out, int64_t NI, int64_t NJ, int A, int nx, int ny, int C,
@@ -307,16 +334,20 @@ int launch_fill_one(float *ptr, void *stream);
 struct DenseBuild {
     float *gc[kMaxCores];      // folded cores [rho_k][n_k][m_k][rho_{k+1}]
     float *P[kMaxCores + 1];   // left chains P_k = [I_<k][J_<k][rho_k], k = 1..d-1
-    void *w;                   // W [N_in][N_out] (or W^T) in the activation dtype
+    void *w;                   // W [N_in][N_out] in the activation dtype
+    void *wt;                  // W^T [N_out][N_in] in the activation dtype
 };
+// which layouts of W build_chain writes
+constexpr int kWantW = 1, kWantWT = 2;
 // folded-core pointers of a layer whose workspace starts at ws
 void dense_ptrs(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd);
 // fold the masks into compacted copies of every core of layer p (eq. Wcompress):
 // core k goes to dst[k], placed by st[k]
 int fold_cores(const comera_ttm_plan_s *p, const float *const *G, const float *const *D, float *const *dst,
                const CoreStrides *st, void *stream);
-// left chains and W (or W^T with transpose) of a layer from its folded cores
-int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, bool transpose, void *stream);
+// left chains and W (want & kWantW) and / or W^T (want & kWantWT) of a
+// layer from its folded cores
+int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, int want, void *stream);
 // dW = A^T B (A [K][N_in] with leading dimension lda, B [K][N_out] with ldb),
 // split over K, written blocked for the projections; *dwp, *splits describe
 // the split partials

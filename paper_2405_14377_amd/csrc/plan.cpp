@@ -200,6 +200,8 @@ void layout_dense(comera_ttm_plan_s *p, bool with_dx) {
     }
     L.w = off;
     off = align_up(off + esz * size_t(p->N_in * p->N_out));
+    L.wt = off;
+    off = align_up(off + esz * size_t(p->N_in * p->N_out));
     L.ones = off;
     off = align_up(off + sizeof(float));
     // dW = X^T dY split over tokens so that the grid holds >= ~512 workgroups

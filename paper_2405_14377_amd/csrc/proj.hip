@@ -231,10 +231,12 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjArgs a) {
 // P = P_{d-1} [I][J][a] and the folded last core G [a][x][y] (x = i_{d-1},
 // y = j_{d-1}),
 //   W[(I x)][(J y)] = sum_a P[I][J][a] G[a][x][y]
-// written as W [N_in][N_out] or as W^T [N_out][N_in], fp32 or bf16.  A
-// workgroup owns one value of the outer index of the output rows (J for W^T,
-// I for W) and a block of QB values of the inner one; consecutive threads
-// write consecutive output columns.
+// written as W [N_in][N_out], as W^T [N_out][N_in], or both, fp32 or bf16.
+// A workgroup owns QI values of I and QJ values of J, i.e. a tile of
+// (QI nx) x (QJ ny) entries of W: it stages its P slice (rank-major) and G in
+// LDS, computes the tile as a [QI QJ] x [nx ny] product with 4 x 4 register
+// blocks, keeps it in LDS and writes it out row by row in each requested
+// layout, consecutive threads on consecutive addresses.
 __device__ __forceinline__ uint16_t to_bf16_rne(float f) {
     uint32_t u = __float_as_uint(f);
     if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return uint16_t((u >> 16) | 0x40);
@@ -242,69 +244,144 @@ __device__ __forceinline__ uint16_t to_bf16_rne(float f) {
     return uint16_t(u >> 16);
 }
 
-// G is staged as [a][q][o] with o (the output-row digit) padded to a multiple
-// of 4, so every thread reads float4 runs of G for its (Q, q) column.
-template <bool TR>
-__global__ __launch_bounds__(256) void wbuild_kernel(WBuildArgs a) {
+// LDS floats of a W tile workgroup: P^T [A][NP4], G [A][NC4], tile [TI][TJ + 1]
+__host__ __device__ inline size_t wtile_lds_floats(int A, int QI, int QJ, int nx, int ny) {
+    const int NP4 = round4(QI * QJ), NC4 = round4(nx * ny);
+    return size_t(A) * NP4 + size_t(A) * NC4 + size_t(QI * nx) * (QJ * ny + 1);
+}
+
+__device__ __forceinline__ void put_w(void *out, bool bf, int64_t off, float v) {
+    if (bf)
+        reinterpret_cast<uint16_t *>(out)[off] = to_bf16_rne(v);
+    else
+        reinterpret_cast<float *>(out)[off] = v;
+}
+
+__global__ __launch_bounds__(256) void wtile_kernel(WBuildArgs a) {
     extern __shared__ __attribute__((aligned(16))) float sw[];
-    const int64_t NQ = TR ? a.NI : a.NJ;
-    const int no = TR ? a.ny : a.nx, nq = TR ? a.nx : a.ny;
-    const int NO4 = round4(no);
-    const int A = a.A, QB = a.QB;
-    const int gsz = A * nq * NO4;
-    float *G_s = sw;
-    float *P_s = sw + gsz;
-    const int64_t O = blockIdx.x;
-    const int64_t Q0 = int64_t(blockIdx.y) * QB;
-    const int nQ = int(min<int64_t>(QB, NQ - Q0));
-    stage_lds<8>(G_s, gsz, threadIdx.x, 256, [&](int i) {
-        const int o = i % NO4, t = i / NO4;
-        const int q = t % nq, al = t / nq;
-        const int x = TR ? q : o, y = TR ? o : q;
-        return o < no ? a.G[(al * a.nx + x) * a.ny + y] : 0.f;
-    });
-    stage_lds<8>(P_s, nQ * A, threadIdx.x, 256, [&](int i) {
-        const int ql = i / A, al = i - ql * A;
-        const int64_t I = TR ? Q0 + ql : O, J = TR ? O : Q0 + ql;
-        return a.P[(I * a.NJ + J) * A + al];
-    });
-    __syncthreads();
-    const int64_t rowlen = NQ * nq;
-    for (int item = threadIdx.x; item < nQ * nq; item += 256) {
-        const int ql = item / nq, q = item - ql * nq;
-        const int64_t col = (Q0 + ql) * nq + q;
-        const float *pr = P_s + ql * A;
-        for (int o0 = 0; o0 < NO4; o0 += 16) {
-            const int n4 = min(4, (NO4 - o0) / 4);
-            float acc[16];
+    const int A = a.A, nx = a.nx, ny = a.ny, QI = a.QI, QJ = a.QJ;
+    const int NP = QI * QJ, NC = nx * ny;
+    const int NP4 = round4(NP), NC4 = round4(NC);
+    const int TI = QI * nx, TJ = QJ * ny, tp = TJ + 1;
+    float *Pt = sw;                 // [A][NP4], pair p = qi * QJ + qj
+    float *Gs = Pt + A * NP4;       // [A][NC4], column c = x * ny + y
+    float *tile = Gs + A * NC4;     // [TI][tp]
+    const int64_t I0 = int64_t(blockIdx.y) * QI, J0 = int64_t(blockIdx.x) * QJ;
+    const int nI = int(min<int64_t>(QI, a.NI - I0)), nJ = int(min<int64_t>(QJ, a.NJ - J0));
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // Every integer division below is per thread or per item, never per
+    // element: a wave64 instruction occupies its SIMD for four cycles, and a
+    // division is a few dozen of them.
+    {
+        // P slice: thread t loads rank entries al = t % A, t % A + ... of the
+        // pairs p = t / A + 256 / A * i (coalesced runs of A floats per pair);
+        // G: consecutive floats.  All loads are issued before any store.
+        constexpr int U = 24;
+        float v[U];
+        const int pa0 = tid % A, pp0 = tid / A, pstep = 256 / A;     // A <= 64
+        const int np_t = (tid < pstep * A && pp0 < NP4) ? (NP4 - pp0 + pstep - 1) / pstep : 0;
+        const int ng_t = (A * NC4 - tid + 255) / 256;
+        int qi = pp0 / QJ, qj = pp0 - (pp0 / QJ) * QJ;
+        const int dqi = pstep / QJ, dqj = pstep - dqi * QJ;
 #pragma unroll
-            for (int j = 0; j < 16; ++j) acc[j] = 0.f;
-            const float *gq = G_s + q * NO4 + o0;
-            for (int al = 0; al < A; ++al) {
-                const float p = pr[al];
-                const float *g = gq + al * nq * NO4;
-#pragma unroll
-                for (int j4 = 0; j4 < 4; ++j4) {
-                    if (j4 < n4) {
-                        const float4 g4 = *reinterpret_cast<const float4 *>(g + 4 * j4);
-                        acc[4 * j4 + 0] += p * g4.x;
-                        acc[4 * j4 + 1] += p * g4.y;
-                        acc[4 * j4 + 2] += p * g4.z;
-                        acc[4 * j4 + 3] += p * g4.w;
-                    }
+        for (int u = 0; u < U; ++u) {
+            v[u] = 0.f;
+            if (u < np_t) {
+                const int p = pp0 + u * pstep;
+                if (p < NP && qi < nI && qj < nJ) v[u] = a.P[((I0 + qi) * a.NJ + J0 + qj) * A + pa0];
+                qi += dqi;
+                qj += dqj;
+                if (qj >= QJ) {
+                    qj -= QJ;
+                    ++qi;
                 }
-            }
-#pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                if (o0 + j >= no) break;
-                const int64_t off = (O * no + o0 + j) * rowlen + col;
-                if (a.out_bf16)
-                    reinterpret_cast<uint16_t *>(a.out)[off] = to_bf16_rne(acc[j]);
-                else
-                    reinterpret_cast<float *>(a.out)[off] = acc[j];
+            } else if (u - np_t < ng_t) {
+                const int g = tid + (u - np_t) * 256;
+                const int al = g / NC4, c = g - al * NC4;
+                if (c < NC) v[u] = a.G[al * NC + c];
             }
         }
+        for (int u = 0; u < U; ++u) {
+            if (u < np_t) {
+                Pt[pa0 * NP4 + pp0 + u * pstep] = v[u];
+            } else if (u - np_t < ng_t) {
+                const int g = tid + (u - np_t) * 256;
+                Gs[g] = v[u];
+            }
+        }
+        // anything beyond U loads per thread (large ranks or cores)
+        for (int u = U; u < np_t; ++u) {
+            const int p = pp0 + u * pstep;
+            const int q1 = p / QJ, q2 = p - (p / QJ) * QJ;
+            Pt[pa0 * NP4 + p] = (p < NP && q1 < nI && q2 < nJ) ? a.P[((I0 + q1) * a.NJ + J0 + q2) * A + pa0] : 0.f;
+        }
+        for (int u = max(0, U - np_t); u < ng_t; ++u) {
+            const int g = tid + u * 256;
+            const int al = g / NC4, c = g - al * NC4;
+            Gs[g] = c < NC ? a.G[al * NC + c] : 0.f;
+        }
     }
+    __syncthreads();
+    const int npb = NP4 / 4, ncb = NC4 / 4;
+    for (int w = tid; w < npb * ncb; w += 256) {
+        const int pb = w / ncb, cb = w - pb * ncb;
+        float acc[4][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+        const float *pp = Pt + pb * 4, *gp = Gs + cb * 4;
+#pragma unroll 4
+        for (int al = 0; al < A; ++al) {
+            const float4 pv = *reinterpret_cast<const float4 *>(pp + al * NP4);
+            const float4 gv = *reinterpret_cast<const float4 *>(gp + al * NC4);
+            const float pa[4] = {pv.x, pv.y, pv.z, pv.w}, ga[4] = {gv.x, gv.y, gv.z, gv.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] += pa[i] * ga[j];
+        }
+        // tile offsets of the four pairs and the four columns
+        int roff[4], coff[4];
+        {
+            int p = pb * 4, q1 = p / QJ, q2 = p - q1 * QJ;
+            int c = cb * 4, x = c / ny, y = c - x * ny;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                roff[i] = (p + i < NP) ? q1 * nx * tp + q2 * ny : -1;
+                coff[i] = (c + i < NC) ? x * tp + y : -1;
+                if (++q2 == QJ) {
+                    q2 = 0;
+                    ++q1;
+                }
+                if (++y == ny) {
+                    y = 0;
+                    ++x;
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (roff[i] >= 0 && coff[j] >= 0) tile[roff[i] + coff[j]] = acc[i][j];
+    }
+    __syncthreads();
+    const bool bf = a.out_bf16 != 0;
+    const int ri = nI * nx, rj = nJ * ny;
+    const int64_t Nin = a.NI * nx, Nout = a.NJ * ny;
+    const int64_t i0 = I0 * nx, j0 = J0 * ny;
+    // one output row per wave at a time, lanes on consecutive addresses
+    if (a.out)       // W [N_in][N_out]: rows i, runs of rj consecutive j
+        for (int r = wave; r < ri; r += 4) {
+            const int64_t base = (i0 + r) * Nout + j0;
+            for (int c = lane; c < rj; c += 64) put_w(a.out, bf, base + c, tile[r * tp + c]);
+        }
+    if (a.out_t)     // W^T [N_out][N_in]: rows j, runs of ri consecutive i
+        for (int c = wave; c < rj; c += 4) {
+            const int64_t base = (j0 + c) * Nin + i0;
+            for (int r = lane; r < ri; r += 64) put_w(a.out_t, bf, base + r, tile[r * tp + c]);
+        }
 }
 
 }  // namespace
@@ -320,35 +397,32 @@ void proj_tiles(int64_t rows, int64_t cols, int A, int &RT, int &CT) {
     while (RT > 8 && ((rows + RT - 1) / RT) * nct < 256) RT /= 2;
 }
 
-bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, bool transpose, int &QB) {
-    if (A < 1 || A > kProjMaxA) return false;
-    const int64_t NQ = transpose ? NI : NJ;
-    const int nq = transpose ? nx : ny;
-    const int no = transpose ? ny : nx;
-    const size_t g = size_t(A) * nq * round4(no);
-    // about 256 output columns per workgroup: several workgroups per CU hide
-    // the staging latency better than fewer, larger ones (measured); blocks of
-    // equal size
-    int64_t qb = std::max<int64_t>(1, std::min<int64_t>(NQ, 256 / std::max(1, nq)));
-    const int64_t nblk = (NQ + qb - 1) / qb;
-    qb = (NQ + nblk - 1) / nblk;
-    while (qb > 1 && (g + size_t(qb) * A) * sizeof(float) > kProjLds) qb /= 2;
-    if ((g + size_t(qb) * A) * sizeof(float) > kProjLds) return false;
-    QB = int(qb);
+bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, int &QI, int &QJ) {
+    if (A < 1 || A > kProjMaxA || NI < 1 || NJ < 1) return false;
+    // tiles of about 64 x 64 entries of W (rows of 64+ elements in both
+    // layouts); halved while a workgroup would hold more LDS than allowed
+    int qi = int(std::min<int64_t>(NI, std::max(1, (64 + nx - 1) / nx)));
+    int qj = int(std::min<int64_t>(NJ, std::max(1, (64 + ny - 1) / ny)));
+    while (wtile_lds_floats(A, qi, qj, nx, ny) * sizeof(float) > kProjLds && (qi > 1 || qj > 1)) {
+        if (qj >= qi && qj > 1) qj = (qj + 1) / 2;
+        else qi = (qi + 1) / 2;
+    }
+    if (wtile_lds_floats(A, qi, qj, nx, ny) * sizeof(float) > kProjLds) return false;
+    QI = qi;
+    QJ = qj;
     return true;
 }
 
 int launch_wbuild(const WBuildArgs &a, void *stream) {
-    const int64_t NO = a.transpose ? a.NJ : a.NI, NQ = a.transpose ? a.NI : a.NJ;
-    if (NO <= 0 || NQ <= 0) return 0;
-    const int no = a.transpose ? a.ny : a.nx, nq = a.transpose ? a.nx : a.ny;
-    const size_t lds = (size_t(a.A) * nq * round4(no) + size_t(a.QB) * a.A) * sizeof(float);
-    if (lds > kProjLds || a.QB < 1) return int(hipErrorInvalidValue);
-    dim3 grid(unsigned(NO), unsigned((NQ + a.QB - 1) / a.QB));
-    if (a.transpose)
-        hipLaunchKernelGGL(wbuild_kernel<true>, grid, dim3(256), lds, hipStream_t(stream), a);
-    else
-        hipLaunchKernelGGL(wbuild_kernel<false>, grid, dim3(256), lds, hipStream_t(stream), a);
+    if (a.NI <= 0 || a.NJ <= 0 || (!a.out && !a.out_t)) return 0;
+    const size_t lds = wtile_lds_floats(a.A, a.QI, a.QJ, a.nx, a.ny) * sizeof(float);
+    if (lds > kProjLds || a.QI < 1 || a.QJ < 1) return int(hipErrorInvalidValue);
+    static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(wtile_kernel),
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, int(kProjLds)));
+    if (set) return set;
+    const int64_t gx = (a.NJ + a.QJ - 1) / a.QJ, gy = (a.NI + a.QI - 1) / a.QI;
+    if (gx >= (int64_t(1) << 31) || gy > 65535) return int(hipErrorInvalidValue);
+    hipLaunchKernelGGL(wtile_kernel, dim3(unsigned(gx), unsigned(gy)), dim3(256), lds, hipStream_t(stream), a);
     return int(hipGetLastError());
 }
 

@@ -93,7 +93,7 @@ int build_groups(const comera_ttm_plan_s *p, const float *const *G, const float 
     }
     if (int e = fold_cores(p, G, D, dst, L.st, stream)) return e;
     for (int g = 0; g < L.G; ++g)
-        if (int e = build_chain(p->sub[g].get(), gr.ws[g], gr.bd[g], false, stream)) return e;
+        if (int e = build_chain(p->sub[g].get(), gr.ws[g], gr.bd[g], kWantW, stream)) return e;
     return 0;
 }
 

@@ -158,6 +158,10 @@ def test_call_errors_before_launch():
     assert lib.comera_ttm_backward(p.handle, 4, fake, fake, G, None, fake, None, fake, 1, None) == C.ERR_WORKSPACE
     # empty batch is a no-op that needs nothing
     assert lib.comera_ttm_forward(p.handle, 0, None, None, None, None, None, 0, None) == C.OK
+    # plan settings
+    assert lib.comera_ttm_plan_set_reuse_forward(None, 1) == C.ERR_INVALID_ARG
+    assert lib.comera_ttm_plan_set_reuse_forward(p.handle, 1) == C.OK
+    assert lib.comera_ttm_plan_set_reuse_forward(p.handle, 0) == C.OK
 
 
 def test_embed_workspace_and_errors():

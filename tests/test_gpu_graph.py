@@ -1,0 +1,134 @@
+"""HIP-graph capture of a whole training step (TTM forward + backward, and
+the embedding lookup forward + backward), the analogue of the CUDA-graph
+execution of Sec. 4.3: every replay must reproduce the eager results bit
+for bit.  Between replays the program does its own eager work (new inputs
+copied into the captured buffers, eager calls of the same plan on another
+workspace) and synchronises, and every replay is checked."""
+import numpy as np
+import pytest
+
+from oracle import ttm as OT
+from paper_2405_14377_amd import comera as C
+from paper_2405_14377_amd import workloads as wl
+from tests.gpu_util import EmbedRun, TTMRun, rel_err, to_dev, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _ttm_inputs(seed, n, m, r, b, act, sets):
+    rng = np.random.default_rng(seed)
+    shape = wl.TTMLayerShape("g", tuple(n), tuple(m), tuple(r))
+    d = len(n)
+    sig = (shape.n_in * np.prod(r[1:-1])) ** (-1.0 / (2 * d))
+    cores = [(c * sig).astype(np.float32) for c in wl.random_cores(rng, shape)]
+    D = [rng.uniform(0.5, 1.5, r[k + 1]).astype(np.float32) for k in range(d - 1)]
+    xs = []
+    for _ in range(sets):
+        X = rng.standard_normal((b, shape.n_in)).astype(np.float32)
+        dY = rng.standard_normal((b, shape.n_out)).astype(np.float32)
+        if act == "bf16":
+            X, dY = wl.to_bf16_values(X), wl.to_bf16_values(dY)
+        xs.append((X, dY))
+    return cores, D, xs
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+@pytest.mark.parametrize("reuse", [False, True])
+@pytest.mark.parametrize("case", [((4, 6, 5), (3, 7, 4), (1, 6, 5, 1), 200, -1),
+                                  ((8, 8, 12), (12, 8, 8), (1, 8, 8, 1), 32, -1),
+                                  ((3, 4, 5), (5, 2, 6), (1, 3, 4, 1), 64, 1)],
+                         ids=["dense", "w0", "sweep"])
+def test_ttm_step_graph_replays(case, reuse, act):
+    import torch
+    n, m, r, b, order = case
+    cores, D, xs = _ttm_inputs(31, n, m, r, b, act, 3)
+    run = TTMRun(n, m, r, cores, D, b, act, force_order=order, reuse=reuse)
+    ref_run = TTMRun(n, m, r, cores, D, b, act, force_order=order, reuse=reuse)
+    Xs, dYs = to_dev(xs[0][0], act), to_dev(xs[0][1], act)
+    Ys = torch.empty((b, run.n_out), dtype=run.tdt, device="cuda")
+    dXs = torch.empty((b, run.n_in), dtype=run.tdt, device="cuda")
+    dGs = [torch.empty_like(g) for g in run.G]
+
+    def step():
+        C.comera_ttm_forward(run.plan.handle, b, Xs, run.G, run.D, Ys, run.ws)
+        C.comera_ttm_backward(run.plan.handle, b, Xs, dYs, run.G, run.D, dXs, dGs, run.ws)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            step()
+        torch.cuda.synchronize()
+        for rep in range(2):
+            for X, dY in xs:
+                Xt, dYt = to_dev(X, act), to_dev(dY, act)
+                # eager reference on its own workspace, then the replay
+                Yr = ref_run.forward(Xt)
+                dXr, dGr = ref_run.backward(Xt, dYt)
+                torch.cuda.synchronize()
+                Xs.copy_(Xt)
+                dYs.copy_(dYt)
+                g.replay()
+                torch.cuda.synchronize()
+                assert torch.equal(Ys, Yr), rep
+                assert torch.equal(dXs, dXr), rep
+                for a, c in zip(dGs, dGr):
+                    assert torch.equal(a, c), rep
+        # the last replay also matches the oracle
+        X, dY = xs[-1]
+        tol = 1e-4 if act == "f32" else 2e-2
+        assert rel_err(to_np(Ys), OT.forward_dense(X, cores, D)) <= tol
+        dXo, dGo = OT.backward_dense(X, dY, cores, D)
+        assert rel_err(to_np(dXs), dXo) <= tol
+        for a, c in zip(dGs, dGo):
+            assert rel_err(to_np(a), c) <= tol
+    del g
+
+
+def test_embed_step_graph_replays():
+    import torch
+    v, e, r = (4, 5, 6), (2, 3, 4), (1, 3, 4, 1)
+    rng = np.random.default_rng(32)
+    cores = [(0.3 * rng.standard_normal((r[k], v[k], e[k], r[k + 1]))).astype(np.float32) for k in range(3)]
+    n = 300
+    V, E = int(np.prod(v)), int(np.prod(e))
+    ids_sets = [rng.integers(0, V, n), rng.zipf(1.5, n) % V, np.full(n, 7)]
+    dY_sets = [rng.standard_normal((n, E)).astype(np.float32) for _ in ids_sets]
+    run = EmbedRun(v, e, r, cores, None, n)
+    ref = EmbedRun(v, e, r, cores, None, n)
+    ids_s = run.ids_dev(ids_sets[0])
+    dY_s = to_dev(dY_sets[0])
+    Y_s = torch.empty((n, E), device="cuda")
+    dG_s = [torch.empty_like(g) for g in run.G]
+
+    def step():
+        C.comera_tt_embed_forward(run.shape, ids_s, n, run.G, None, Y_s, run.ws, run.err)
+        C.comera_tt_embed_backward(run.shape, ids_s, n, dY_s, run.G, None, dG_s, 1, run.ws, run.err)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            step()
+        torch.cuda.synchronize()
+        for rep in range(2):
+            for ids, dY in zip(ids_sets, dY_sets):
+                it, dYt = ref.ids_dev(ids), to_dev(dY)
+                Yr = ref.forward(it)
+                dGr = ref.backward(it, dYt)
+                torch.cuda.synchronize()
+                ids_s.copy_(it)
+                dY_s.copy_(dYt)
+                g.replay()
+                torch.cuda.synchronize()
+                assert torch.equal(Y_s, Yr), rep
+                for a, c in zip(dG_s, dGr):
+                    assert torch.equal(a, c), rep
+    assert int(run.err.item()) == 0
+    del g

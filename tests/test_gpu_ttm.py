@@ -74,6 +74,33 @@ def test_random_shapes(case, act):
     _check_layer(n, m, r, cores, D, X, dY, act)
 
 
+REUSE_CASES = CASES + [(15, (2, 16), (3, 20), (1, 60, 1), 100)]   # last core too large for the W tile kernel
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+@pytest.mark.parametrize("case", REUSE_CASES, ids=[f"s{c[0]}" for c in REUSE_CASES])
+def test_reuse_forward_build(case, act):
+    """With reuse on, backward takes the masked cores, chains and W that the
+    forward left in the workspace: every output equals the rebuilding
+    route's bit for bit and matches the oracle."""
+    seed, n, m, r, b = case
+    cores, D, X, dY = _inputs(seed, n, m, r, b, act)
+    Xt, dYt = to_dev(X, act), to_dev(dY, act)
+    outs = []
+    for reuse in (False, True):
+        run = TTMRun(n, m, r, cores, D, b, act, reuse=reuse)
+        Y = to_np(run.forward(Xt))
+        dX, dG = run.backward(Xt, dYt)
+        outs.append([Y, to_np(dX)] + [to_np(g) for g in dG])
+    for a, c in zip(*outs):
+        assert np.array_equal(a, c)
+    Yr = OT.forward_dense(X, cores, D)
+    dXr, dGr = OT.backward_dense(X, dY, cores, D)
+    refs = [Yr, dXr] + list(dGr)
+    errs = [rel_err(g, ref) for g, ref in zip(outs[1], refs)]
+    assert max(errs) <= TOL[act], errs
+
+
 @pytest.mark.parametrize("act", ["f32", "bf16"])
 def test_no_masks(act):
     n, m, r = (4, 6, 5), (3, 7, 4), (1, 6, 5, 1)
