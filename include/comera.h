@@ -154,11 +154,12 @@ void comera_ttm_plan_destroy(comera_ttm_plan_t p);
  * gradients).  With enable != 0, comera_ttm_forward of the dense order also
  * writes W in the layout that dX reads, and comera_ttm_backward takes the
  * masked cores, left chains and W from the workspace instead of rebuilding
- * them.  The caller then guarantees that every backward call follows a
- * forward call of this plan on the same workspace with the same G and D,
- * with no other call of this plan on that workspace in between; otherwise
- * the results are undefined (no error can be detected).  Sweep orders
- * ignore the setting.  Off by default; host only, no device work.
+ * them; under a sweep order it likewise takes the group matrices and the
+ * activation states of the forward sweep.  The caller then guarantees that
+ * every backward call follows a forward call of this plan on the same
+ * workspace with the same G, D and X, with no other call of this plan on
+ * that workspace in between; otherwise the results are undefined (no error
+ * can be detected).  Off by default; host only, no device work.
  * Returns COMERA_ERR_INVALID_ARG for a NULL plan. */
 comera_status comera_ttm_plan_set_reuse_forward(comera_ttm_plan_t p, int32_t enable);
 

@@ -124,6 +124,16 @@ int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, int want,
     return 0;
 }
 
+void built_dense(const comera_ttm_plan_s *p, void *ws, DenseBuild &bd, int want) {
+    dense_ptrs(p, ws, bd);
+    bd.P[1] = bd.gc[0];
+    for (int k = 1; k + 1 < p->d; ++k) bd.P[k + 1] = reinterpret_cast<float *>(at(ws, p->dense.p[k + 1]));
+    bd.w = at(ws, p->dense.w);
+    bd.wt = at(ws, p->dense.wt);
+    // build_chain keeps a single fp32 core as W itself
+    if (p->d == 1 && p->s.act != COMERA_BF16 && want == kWantW) bd.w = bd.gc[0];
+}
+
 int dw_gemm(const comera_ttm_plan_s *sp, const void *A, int64_t lda, const void *B, int64_t ldb, int64_t K,
             void *ws, float **dwp, int *splits_out, void *stream) {
     const DenseLayout &L = sp->dense;
@@ -305,15 +315,6 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
     return build_chain(p, ws, bd, want, stream);
 }
 
-// pointers of a build that an earlier forward call left in the workspace
-void built_dense(const comera_ttm_plan_s *p, void *ws, DenseBuild &bd) {
-    dense_ptrs(p, ws, bd);
-    bd.P[1] = bd.gc[0];
-    for (int k = 1; k + 1 < p->d; ++k) bd.P[k + 1] = reinterpret_cast<float *>(at(ws, p->dense.p[k + 1]));
-    bd.w = at(ws, p->dense.w);
-    bd.wt = at(ws, p->dense.wt);
-}
-
 }  // namespace
 
 namespace comera {
@@ -429,7 +430,7 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
     DenseBuild bd;
     int e = 0;
     if (p->reuse)
-        built_dense(p, ws, bd);
+        built_dense(p, ws, bd, kWantWT | kWantW);
     else
         e = build_dense(p, G, D, ws, stream, bd, kWantW);
     if (e) return COMERA_ERR_HIP;

@@ -348,6 +348,9 @@ int fold_cores(const comera_ttm_plan_s *p, const float *const *G, const float *c
 // left chains and W (want & kWantW) and / or W^T (want & kWantWT) of a
 // layer from its folded cores
 int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, int want, void *stream);
+// pointers of the build that build_chain(want) left in the workspace of an
+// earlier call (no device work)
+void built_dense(const comera_ttm_plan_s *p, void *ws, DenseBuild &bd, int want);
 // dW = A^T B (A [K][N_in] with leading dimension lda, B [K][N_out] with ldb),
 // split over K, written blocked for the projections; *dwp, *splits describe
 // the split partials

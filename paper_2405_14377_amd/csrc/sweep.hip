@@ -7,7 +7,9 @@
 //   dG        the gradient of W'_g is the meet of the activation state and
 //             the dY state at group g (eq. back Gi); it is projected onto the
 //             group's own cores as for a dense layer.
-// The activation states are recomputed in the backward call.  Every product
+// The backward call recomputes the group matrices and the activation states,
+// or, when the plan reuses the forward's work, takes them from the workspace
+// the forward call left.  Every product
 // writes its output already permuted for the next one (mixed-radix epilogue).
 #include <hip/hip_runtime.h>
 
@@ -97,6 +99,15 @@ int build_groups(const comera_ttm_plan_s *p, const float *const *G, const float 
     return 0;
 }
 
+// pointers of the groups an earlier forward call built (reuse)
+void built_groups(const comera_ttm_plan_s *p, void *ws, Groups &gr) {
+    const SweepLayout &L = p->sweep;
+    for (int g = 0; g < L.G; ++g) {
+        gr.ws[g] = at(ws, L.base[g]);
+        built_dense(p->sub[g].get(), gr.ws[g], gr.bd[g], kWantW);
+    }
+}
+
 // Activation sweep.  Right to left, step g maps Z_{g+1} (X for the last
 // group) to Z_g (Y for g = 0); left to right, step g maps Z_g (X, or its
 // per-token transpose, for g = 0) to Z_{g+1} (Y for the last group).  With
@@ -169,8 +180,13 @@ comera_status sweep_backward(const comera_ttm_plan_s *p, int64_t b, const void *
     const bool rl = L.dir == COMERA_ORDER_SWEEP_RL;
     bool want_dg = false;
     for (int k = 0; k < d; ++k) want_dg = want_dg || (dG && dG[k]);
+    // with reuse, the group layers, the transposed X (left to right) and the
+    // activation states are the ones the forward call left in the workspace
     Groups gr;
-    if (int e = build_groups(p, G, D, ws, gr, stream)) return status_of(e);
+    if (p->reuse)
+        built_groups(p, ws, gr);
+    else if (int e = build_groups(p, G, D, ws, gr, stream))
+        return status_of(e);
     // inputs of the first step of each sweep (per-token transposes where the
     // first-swept factor is not the last one)
     const void *X0 = X, *H0 = dY;
@@ -180,13 +196,14 @@ comera_status sweep_backward(const comera_ttm_plan_s *p, int64_t b, const void *
                 return status_of(note_hip(e, "transpose"));
             H0 = at(ws, L.tin);
         } else if (want_dg) {
-            if (int e = launch_permute_tokens(X, at(ws, L.tin), b, L.N[0], prod(L.N, 1, NG), esz, stream))
-                return status_of(note_hip(e, "transpose"));
+            if (!p->reuse)
+                if (int e = launch_permute_tokens(X, at(ws, L.tin), b, L.N[0], prod(L.N, 1, NG), esz, stream))
+                    return status_of(note_hip(e, "transpose"));
             X0 = at(ws, L.tin);
         }
     }
     // activation states for the meets
-    if (want_dg)
+    if (want_dg && !p->reuse)
         if (int e = sweep_x(p, b, X0, nullptr, ws, gr, false, stream)) return status_of(e);
     // dY sweep (the mirror direction); its last step writes dX
     {

@@ -21,7 +21,7 @@ from tests.test_gpu_ttm import TOL, _inputs
 pytestmark = pytest.mark.gpu
 
 
-def _all_orders(n, m, r, cores, D, X, dY, act, mask_active=None, b_run=None, orders=None):
+def _all_orders(n, m, r, cores, D, X, dY, act, mask_active=None, b_run=None, orders=None, reuse=False):
     b_plan = X.shape[0]
     b = b_plan if b_run is None else b_run
     Xb, dYb = X[:b], dY[:b]
@@ -36,7 +36,7 @@ def _all_orders(n, m, r, cores, D, X, dY, act, mask_active=None, b_run=None, ord
             continue
         seen += 1
         print(f"order {i} {info['desc']} b={b} act={act}", flush=True)
-        run = TTMRun(n, m, r, cores, D, b_plan, act, mask_active=mask_active, force_order=i)
+        run = TTMRun(n, m, r, cores, D, b_plan, act, mask_active=mask_active, force_order=i, reuse=reuse)
         Xt, dYt = to_dev(Xb, act), to_dev(dYb, act)
         Y = to_np(run.forward(Xt, b=b))
         dX, dG = run.backward(Xt, dYt, b=b)
@@ -66,6 +66,30 @@ def test_every_order(case, act):
     seed, n, m, r, b = case
     cores, D, X, dY = _inputs(seed, n, m, r, b, act)
     _all_orders(n, m, r, cores, D, X, dY, act)
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+@pytest.mark.parametrize("case", SHAPES, ids=[f"s{c[0]}" for c in SHAPES])
+def test_every_order_reusing_forward(case, act):
+    """Backward calls that take the group matrices and activation states the
+    forward left in the workspace: the oracle's results for every order, and
+    bit for bit the rebuilding route's."""
+    seed, n, m, r, b = case
+    cores, D, X, dY = _inputs(seed, n, m, r, b, act)
+    _all_orders(n, m, r, cores, D, X, dY, act, reuse=True)
+    probe = C.TTMPlan(n, m, r, C.BF16 if act == "bf16" else C.F32, batch=b)
+    Xt, dYt = to_dev(X, act), to_dev(dY, act)
+    for i in range(probe.num_orders):
+        if not probe.order_info(i)["executable"]:
+            continue
+        outs = []
+        for reuse in (False, True):
+            run = TTMRun(n, m, r, cores, D, b, act, force_order=i, reuse=reuse)
+            Y = run.forward(Xt)
+            dX, dG = run.backward(Xt, dYt)
+            outs.append([Y, dX] + dG)
+        for a, c in zip(*outs):
+            assert np.array_equal(to_np(a), to_np(c)), i
 
 
 def test_every_order_compacted_masks_smaller_batch():
