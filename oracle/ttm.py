@@ -194,6 +194,47 @@ def backward_direct(X, dY, cores, masks=None) -> Tuple[np.ndarray, List[np.ndarr
     return dX, dG
 
 
+# ----------------------------------------------------------------------------- mask gradients
+def _mask_list(cores, masks) -> List[np.ndarray]:
+    d = len(cores)
+    return [np.ones(cores[k].shape[3]) if masks is None else _f64(masks[k]) for k in range(d - 1)]
+
+
+def mask_grads_dense(X, dY, cores, masks=None) -> List[np.ndarray]:
+    """dD_k[c] = <dW, dW/dD_k[c]> for every bond k = 0..d-2 (chain rule through
+    eq. Wcompress).  W is linear in D_k, so dW/dD_k[c] is the layer rebuilt
+    with D_k replaced by the unit vector e_c and the other masks kept."""
+    _check(cores)
+    dW = _f64(X).T @ _f64(dY)
+    base = _mask_list(cores, masks)
+    out = []
+    for k in range(len(cores) - 1):
+        g = np.zeros(base[k].shape[0])
+        for c in range(g.shape[0]):
+            mk = [m.copy() for m in base]
+            mk[k] = np.zeros_like(mk[k])
+            mk[k][c] = 1.0
+            g[c] = float(np.sum(dW * dense_weight(cores, mk)))
+        out.append(g)
+    return out
+
+
+def mask_grads_direct(X, dY, cores, masks=None) -> List[np.ndarray]:
+    """dD_k[c] = sum_{a, j, i} dG~_k[a, j, i, c] G_k[a, j, i, c], where dG~_k is
+    the gradient with respect to the masked core G~_k = G_k D_k: the meet of
+    the forward and the backward sweep at core k (as in backward_direct,
+    before the mask factor)."""
+    _check(cores)
+    Gt = masked_cores(cores, masks)
+    _, F = sweep_right_to_left(X, Gt)
+    _, H = sweep_left_to_right(dY, Gt)
+    out = []
+    for k in range(len(cores) - 1):
+        g = np.einsum("bNajM,bNicM->ajic", H[k], F[k], optimize=True)
+        out.append(np.einsum("ajic,ajic->c", g, _f64(cores[k])))
+    return out
+
+
 # ----------------------------------------------------------------------------- helpers
 def transpose_cores(cores) -> List[np.ndarray]:
     """Cores of W^T: swap each core's output and input mode."""

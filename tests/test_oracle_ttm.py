@@ -6,7 +6,11 @@
 * zeroing rank-mask entries equals deleting those bond slices;
 * inner-product identities <dG_k, G_k> = <dX, X> = <Y, dY> at workload size;
 * the paper's large-batch path (Alg. path; eq. path-T1 .. path-gGi<d) on the
-  unit-mode TT layout of Sec. 4.2.
+  unit-mode TT layout of Sec. 4.2;
+* mask gradients dD_k: explicit sums, central finite differences in D, the
+  identity sum_c dD_k[c] D_k[c] = <Y, dY> (W is linear in each D_k), and the
+  closed form diag((X A)^T (dY B^T)) of the two-core bottleneck
+  W = A diag(D) B.
 """
 import itertools
 
@@ -44,6 +48,7 @@ def _brute(shape, cores, D, X, dY):
     Y = np.zeros((b, shape.n_out))
     dX = np.zeros((b, shape.n_in))
     dG = [np.zeros(g.shape) for g in G]
+    dD = [np.zeros(m.shape) for m in Dm]
     XtdY = X.T @ dY                           # only used as sum_b X[b,i] dY[b,j]; a plain product
     iranges = [range(x) for x in shape.n]
     jranges = [range(x) for x in shape.m]
@@ -66,16 +71,24 @@ def _brute(shape, cores, D, X, dY):
                 for k in range(d):
                     rest = np.prod([fac[l] for l in range(d) if l != k]) * np.prod(msk)
                     dG[k][a[k], jt[k], it[k], a[k + 1]] += XtdY[i, j] * rest
+                for k in range(d - 1):
+                    rest = np.prod(fac) * np.prod([msk[l] for l in range(d - 1) if l != k])
+                    dD[k][a[k + 1]] += XtdY[i, j] * rest
             Y[:, j] += X[:, i] * w
             dX[:, i] += dY[:, j] * w
-    return Y, dX, dG
+    return Y, dX, dG, dD
 
 
 @pytest.mark.parametrize("seed,d", [(s, d) for d in (1, 2, 3) for s in range(4)] + [(11, 4), (12, 4)])
 def test_brute_force(seed, d):
     shape, cores, D, X, dY = _rand_problem(seed, d, max_factor=3 if d < 4 else 2,
                                             max_rank=3 if d < 4 else 2)
-    Yb, dXb, dGb = _brute(shape, cores, D, X, dY)
+    Yb, dXb, dGb, dDb = _brute(shape, cores, D, X, dY)
+    for route in (ttm.mask_grads_dense, ttm.mask_grads_direct):
+        dD = route(X, dY, cores, D)
+        assert len(dD) == d - 1
+        for k in range(d - 1):
+            np.testing.assert_allclose(dD[k], dDb[k], rtol=1e-12, atol=1e-12)
     for route_f, route_b in ((ttm.forward_dense, ttm.backward_dense), (ttm.forward_direct, ttm.backward_direct)):
         Y = route_f(X, cores, D)
         dX, dG = route_b(X, dY, cores, D)
@@ -136,6 +149,54 @@ def test_finite_differences(seed, d):
                 cm[k] = Gk.copy(); cm[k][idx] -= h
                 fd = (loss(X, cp) - loss(X, cm)) / (2 * h)
                 assert abs(fd - dG[k][idx]) < 1e-6 * max(1.0, abs(fd)), (k, idx, fd, dG[k][idx])
+
+
+@pytest.mark.parametrize("seed,d", [(24, 2), (25, 3), (26, 4)])
+def test_mask_grad_finite_differences(seed, d):
+    shape, cores, D, X, dY = _rand_problem(seed, d, b=2, max_factor=2 if d == 4 else 3,
+                                            max_rank=2 if d == 4 else 3)
+    h = 1e-6
+
+    def loss(Ds):
+        return float(np.sum(ttm.forward_direct(X, cores, Ds) * dY))
+
+    for route in (ttm.mask_grads_dense, ttm.mask_grads_direct):
+        dD = route(X, dY, cores, D)
+        for k in range(d - 1):
+            for c in range(shape.r[k + 1]):
+                Dp = [np.asarray(x, np.float64).copy() for x in D]
+                Dm = [np.asarray(x, np.float64).copy() for x in D]
+                Dp[k][c] += h
+                Dm[k][c] -= h
+                fd = (loss(Dp) - loss(Dm)) / (2 * h)
+                assert abs(fd - dD[k][c]) < 1e-6 * max(1.0, abs(fd)), (k, c, fd, dD[k][c])
+
+
+@pytest.mark.parametrize("seed,d", [(27, 3), (28, 4)])
+def test_mask_grad_homogeneity(seed, d):
+    """W is linear in each D_k, so sum_c dD_k[c] D_k[c] = <dW, W> = <Y, dY>."""
+    shape, cores, D, X, dY = _rand_problem(seed, d, b=4)
+    ydy = float(np.sum(ttm.forward_dense(X, cores, D) * dY))
+    for k, g in enumerate(ttm.mask_grads_direct(X, dY, cores, D)):
+        assert abs(float(g @ np.asarray(D[k], np.float64)) - ydy) < 1e-10 * max(1.0, abs(ydy))
+
+
+def test_mask_grad_bottleneck_closed_form():
+    """Two cores with unit modes (input core [1, 1, N, r], output core
+    [r, M, 1, 1]) give W = A diag(D) B with A = G_0[0, 0, :, :] and
+    B = G_1[:, :, 0, 0]; then dD = diag((X A)^T (dY B^T))."""
+    rng = np.random.default_rng(29)
+    N, M, r, b = 7, 5, 4, 6
+    G0 = rng.standard_normal((1, 1, N, r))
+    G1 = rng.standard_normal((r, M, 1, 1))
+    D = [rng.standard_normal(r)]
+    X = rng.standard_normal((b, N))
+    dY = rng.standard_normal((b, M))
+    A, B = G0[0, 0], G1[:, :, 0, 0]
+    np.testing.assert_allclose(ttm.dense_weight([G0, G1], D), A @ np.diag(D[0]) @ B, rtol=1e-13)
+    want = np.diag((X @ A).T @ (dY @ B.T))
+    for route in (ttm.mask_grads_dense, ttm.mask_grads_direct):
+        np.testing.assert_allclose(route(X, dY, [G0, G1], D)[0], want, rtol=1e-12)
 
 
 def _delete_slice(cores, k, a):
