@@ -146,6 +146,22 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
                                   const float *const *D, void *dX, float *const *dG,
                                   void *ws, size_t ws_bytes, void *stream);
 
+/* comera_ttm_backward plus the gradients of the rank masks (chain rule
+ * through eq. Wcompress, the quantity the rank-adaptive training of Sec. 3
+ * updates D_k with): dD is NULL or a host array of d-1 device pointers
+ * (entries may be NULL = not computed); dD_k receives r[k+1] fp32 values,
+ *   dD_k[c] = <dW, dW/dD_k[c]> = sum_{a,m,n} dG~_k[a,m,n,c] G_k[a,m,n,c],
+ * dG~_k being the gradient of the masked core G_k D_k.  Entries declared
+ * inactive in the plan's mask_active (pruned slices, dropped from every
+ * contraction) receive 0; with mask_active NULL every entry gets its exact
+ * gradient, also where D_k[c] == 0.  Sums run in a fixed order (bitwise
+ * repeatable).  Other arguments and errors as for comera_ttm_backward. */
+comera_status comera_ttm_backward_masks(comera_ttm_plan_t p, int64_t b, const void *X,
+                                        const void *dY, const float *const *G,
+                                        const float *const *D, void *dX, float *const *dG,
+                                        float *const *dD, void *ws, size_t ws_bytes,
+                                        void *stream);
+
 void comera_ttm_plan_destroy(comera_ttm_plan_t p);
 
 /* Reuse of the forward's batch-free work in the backward call, as a

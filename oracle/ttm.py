@@ -235,6 +235,22 @@ def mask_grads_direct(X, dY, cores, masks=None) -> List[np.ndarray]:
     return out
 
 
+def mask_grad_term_scale(X, dY, cores, masks=None) -> List[np.ndarray]:
+    """sum_{a, j, i} |dG~_k[a, j, i, c] G_k[a, j, i, c]| per entry c: the
+    scale of the terms whose sum is dD_k[c].  A perturbation of relative size
+    e in every dG~_k changes dD_k[c] by at most e times this, however much
+    the terms cancel (the error scale for gradients from rounded states)."""
+    _check(cores)
+    Gt = masked_cores(cores, masks)
+    _, F = sweep_right_to_left(X, Gt)
+    _, H = sweep_left_to_right(dY, Gt)
+    out = []
+    for k in range(len(cores) - 1):
+        g = np.einsum("bNajM,bNicM->ajic", H[k], F[k], optimize=True)
+        out.append(np.einsum("ajic->c", np.abs(g * _f64(cores[k]))))
+    return out
+
+
 # ----------------------------------------------------------------------------- helpers
 def transpose_cores(cores) -> List[np.ndarray]:
     """Cores of W^T: swap each core's output and input mode."""

@@ -27,6 +27,7 @@ EXPORTS = (
     "comera_ttm_backward", "comera_ttm_plan_destroy", "comera_tt_embed_workspace_bytes",
     "comera_tt_embed_forward", "comera_tt_embed_backward", "comera_status_string", "comera_last_hip_error",
     "comera_ttm_plan_set_timing", "comera_ttm_plan_kernel_time", "comera_ttm_plan_set_reuse_forward",
+    "comera_ttm_backward_masks",
 )
 KERNEL_FWD, KERNEL_DX, KERNEL_DW = 0, 1, 2
 
@@ -86,6 +87,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comera_ttm_forward.restype = i32
     lib.comera_ttm_backward.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.comera_ttm_backward.restype = i32
+    lib.comera_ttm_backward_masks.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.comera_ttm_backward_masks.restype = i32
     lib.comera_ttm_plan_destroy.argtypes = [vp]
     lib.comera_ttm_plan_destroy.restype = None
     lib.comera_tt_embed_workspace_bytes.argtypes = [P(comera_tt_embed_shape), i64]
@@ -230,6 +233,13 @@ def comera_ttm_backward(plan, b: int, X, dY, G, D, dX, dG, ws, stream=None) -> i
     st = load().comera_ttm_backward(plan, int(b), _ptr(X), _ptr(dY), _ptr_array(G), _ptr_array(D), _ptr(dX),
                                     _ptr_array(dG), _ptr(ws), _nbytes(ws), _stream(stream))
     _check(st, "comera_ttm_backward")
+    return st
+
+
+def comera_ttm_backward_masks(plan, b: int, X, dY, G, D, dX, dG, dD, ws, stream=None) -> int:
+    st = load().comera_ttm_backward_masks(plan, int(b), _ptr(X), _ptr(dY), _ptr_array(G), _ptr_array(D), _ptr(dX),
+                                          _ptr_array(dG), _ptr_array(dD), _ptr(ws), _nbytes(ws), _stream(stream))
+    _check(st, "comera_ttm_backward_masks")
     return st
 
 

@@ -295,6 +295,31 @@ int expand_cores(const comera_ttm_plan_s *p, const float *const *part, const int
     return note_hip(launch_expand(xa, stream), "expand");
 }
 
+int mask_grads(const comera_ttm_plan_s *p, const float *const *part, const int *nsplit, const CoreStrides *st,
+               const float *const *G, float *const *dD, void *stream) {
+    if (!dD) return 0;
+    const int d = p->d;
+    MaskGradArgs ma;
+    std::memset(&ma, 0, sizeof(ma));
+    ma.d = d;
+    ma.compacted = p->compacted ? 1 : 0;
+    for (int k = 0; k < d; ++k) {
+        ma.part[k] = part[k];
+        ma.splits[k] = nsplit[k];
+        ma.st[k] = st[k];
+        ma.G[k] = G[k];
+        ma.dD[k] = k < d - 1 ? dD[k] : nullptr;
+        ma.m[k] = int(p->s.m[k]);
+        ma.n[k] = int(p->s.n[k]);
+    }
+    for (int k = 0; k <= d; ++k) {
+        ma.r[k] = int(p->s.r[k]);
+        ma.rc[k] = int(p->rho[k]);
+        ma.act[k] = p->act[k];
+    }
+    return note_hip(launch_mask_grad(ma, stream), "mask gradients");
+}
+
 }  // namespace comera
 
 namespace {
@@ -402,16 +427,25 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, 
     return e ? COMERA_ERR_HIP : COMERA_OK;
 }
 
-comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X, const void *dY,
-                                  const float *const *G, const float *const *D, void *dX, float *const *dG,
-                                  void *ws, size_t ws_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+comera_status backward_impl(comera_ttm_plan_t p, int64_t b, const void *X, const void *dY, const float *const *G,
+                            const float *const *D, void *dX, float *const *dG, float *const *dD, void *ws,
+                            size_t ws_bytes, void *stream) {
     if (!p || b < 0 || b > p->batch) return COMERA_ERR_INVALID_ARG;
     const int d = p->d;
     const size_t esz = p->s.act == COMERA_BF16 ? 2 : 4;
-    bool want_dg = false;
+    bool want_dg = false, want_dd = false;
     if (dG)
         for (int k = 0; k < d; ++k) want_dg = want_dg || dG[k];
-    // nothing flows when the batch is empty or a bond is fully masked
+    if (dD)
+        for (int k = 0; k + 1 < d; ++k) want_dd = want_dd || dD[k];
+    if (!want_dd) dD = nullptr;
+    // nothing flows when the batch is empty or a bond is fully masked (every
+    // mask gradient is then zero too: an entry of the empty bond is declared
+    // inactive, and any other entry's derivative is a layer with that bond)
     if (b == 0 || p->zero) {
         int e = 0;
         if (dX && b > 0) e = launch_fill_zero(dX, size_t(b) * size_t(p->N_in) * esz, stream);
@@ -419,13 +453,16 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
             if (dG[k])
                 e = launch_fill_zero(dG[k], sizeof(float) * size_t(p->s.r[k] * p->s.m[k] * p->s.n[k] * p->s.r[k + 1]),
                                      stream);
+        for (int k = 0; want_dd && k + 1 < d && !e; ++k)
+            if (dD[k]) e = launch_fill_zero(dD[k], sizeof(float) * size_t(p->s.r[k + 1]), stream);
         return note_hip(e, "fill") ? COMERA_ERR_HIP : COMERA_OK;
     }
-    if (!dY || !G || (want_dg && !X)) return COMERA_ERR_INVALID_ARG;
+    const bool want_grad = want_dg || want_dd;
+    if (!dY || !G || (want_grad && !X)) return COMERA_ERR_INVALID_ARG;
     for (int k = 0; k < d; ++k)
         if (!G[k]) return COMERA_ERR_INVALID_ARG;
     if (!ws || ws_bytes < p->ws_bytes) return COMERA_ERR_WORKSPACE;
-    if (p->sweep.G > 0) return sweep_backward(p, b, X, dY, G, D, dX, dG, ws, stream);
+    if (p->sweep.G > 0) return sweep_backward(p, b, X, dY, G, D, dX, want_dg ? dG : nullptr, dD, ws, stream);
     const DenseLayout &L = p->dense;
     DenseBuild bd;
     int e = 0;
@@ -472,7 +509,7 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
         timing_end(p, COMERA_KERNEL_DX, stream, ev);
         if (e) return COMERA_ERR_HIP;
     }
-    if (!want_dg) return COMERA_OK;
+    if (!want_grad) return COMERA_OK;
     // dW = X^T dY (split over tokens, fixed-order split sums)
     float *dwp = nullptr;
     int splits = 0;
@@ -484,14 +521,31 @@ comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X,
         if (e) return COMERA_ERR_HIP;
     }
     bool want[kMaxCores];
-    for (int k = 0; k < d; ++k) want[k] = dG[k] != nullptr;
+    for (int k = 0; k < d; ++k) want[k] = (want_dg && dG[k]) || (dD && k + 1 < d && dD[k]);
     const float *part[kMaxCores];
     int nsplit[kMaxCores];
     e = project_cores(p, bd, dwp, splits, want, ws, part, nsplit, stream);
     if (e) return COMERA_ERR_HIP;
     CoreStrides st[kMaxCores];
     dense_strides(p, st);
-    return expand_cores(p, part, nsplit, st, D, dG, stream) ? COMERA_ERR_HIP : COMERA_OK;
+    if (want_dg && expand_cores(p, part, nsplit, st, D, dG, stream)) return COMERA_ERR_HIP;
+    return mask_grads(p, part, nsplit, st, G, dD, stream) ? COMERA_ERR_HIP : COMERA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+comera_status comera_ttm_backward(comera_ttm_plan_t p, int64_t b, const void *X, const void *dY,
+                                  const float *const *G, const float *const *D, void *dX, float *const *dG,
+                                  void *ws, size_t ws_bytes, void *stream) {
+    return backward_impl(p, b, X, dY, G, D, dX, dG, nullptr, ws, ws_bytes, stream);
+}
+
+comera_status comera_ttm_backward_masks(comera_ttm_plan_t p, int64_t b, const void *X, const void *dY,
+                                        const float *const *G, const float *const *D, void *dX, float *const *dG,
+                                        float *const *dD, void *ws, size_t ws_bytes, void *stream) {
+    return backward_impl(p, b, X, dY, G, D, dX, dG, dD, ws, ws_bytes, stream);
 }
 
 comera_status comera_ttm_plan_set_reuse_forward(comera_ttm_plan_t p, int32_t enable) {

@@ -178,6 +178,26 @@ struct ExpandArgs {
 };
 int launch_expand(const ExpandArgs &a, void *stream);
 
+// dD_k (k = 0..d-2, r_{k+1} floats each, null = skip) from the compacted
+// split partials of the masked-core gradients (as for expand) and the raw
+// cores G_k
+struct MaskGradArgs {
+    const float *part[kMaxCores];
+    int splits[kMaxCores];
+    CoreStrides st[kMaxCores];
+    const float *G[kMaxCores];
+    float *dD[kMaxCores];
+    BondBits act[kMaxCores + 1];
+    int r[kMaxCores + 1];
+    int rc[kMaxCores + 1];
+    int m[kMaxCores];
+    int n[kMaxCores];
+    int d;
+    int compacted;
+    int blk0[kMaxCores];            // set by launch_mask_grad
+};
+int launch_mask_grad(const MaskGradArgs &a, void *stream);
+
 // Output index remap of a GEMM: write idx in mixed radix (digit 0 most
 // significant and unbounded, digit t < nd has radix radix[t] for t >= 1) and
 // return sum_t digit_t * stride[t].
@@ -363,6 +383,9 @@ int project_cores(const comera_ttm_plan_s *sp, const DenseBuild &bd, const float
 // sum the partials of every core of layer p, unfold and apply the masks
 int expand_cores(const comera_ttm_plan_s *p, const float *const *part, const int *nsplit, const CoreStrides *st,
                  const float *const *D, float *const *dG, void *stream);
+// mask gradients dD_k of layer p from the same partials (dD null: nothing)
+int mask_grads(const comera_ttm_plan_s *p, const float *const *part, const int *nsplit, const CoreStrides *st,
+               const float *const *G, float *const *dD, void *stream);
 // out[t][j][i] = in[t][i][j] for t < b, i < M, j < T (elements of esz bytes)
 int launch_permute_tokens(const void *in, void *out, int64_t b, int64_t M, int64_t T, int esz, void *stream);
 
@@ -370,8 +393,8 @@ int launch_permute_tokens(const void *in, void *out, int64_t b, int64_t M, int64
 comera_status sweep_forward(const comera_ttm_plan_s *p, int64_t b, const void *X, const float *const *G,
                             const float *const *D, void *Y, void *ws, void *stream);
 comera_status sweep_backward(const comera_ttm_plan_s *p, int64_t b, const void *X, const void *dY,
-                             const float *const *G, const float *const *D, void *dX, float *const *dG, void *ws,
-                             void *stream);
+                             const float *const *G, const float *const *D, void *dX, float *const *dG,
+                             float *const *dD, void *ws, void *stream);
 
 // record a failed launcher result (hipError_t value e != 0) with the step
 // name for comera_last_hip_error; returns e (api_ttm.hip)

@@ -171,15 +171,16 @@ comera_status sweep_forward(const comera_ttm_plan_s *p, int64_t b, const void *X
 }
 
 comera_status sweep_backward(const comera_ttm_plan_s *p, int64_t b, const void *X, const void *dY,
-                             const float *const *G, const float *const *D, void *dX, float *const *dG, void *ws,
-                             void *stream) {
+                             const float *const *G, const float *const *D, void *dX, float *const *dG,
+                             float *const *dD, void *ws, void *stream) {
     const SweepLayout &L = p->sweep;
     const int NG = L.G;
     const int d = p->d;
     const int esz = p->s.act == COMERA_BF16 ? 2 : 4;
     const bool rl = L.dir == COMERA_ORDER_SWEEP_RL;
+    // want_dg: some core or mask gradient is asked for (both come from the meets)
     bool want_dg = false;
-    for (int k = 0; k < d; ++k) want_dg = want_dg || (dG && dG[k]);
+    for (int k = 0; k < d; ++k) want_dg = want_dg || (dG && dG[k]) || (dD && k + 1 < d && dD[k]);
     // with reuse, the group layers, the transposed X (left to right) and the
     // activation states are the ones the forward call left in the workspace
     Groups gr;
@@ -268,12 +269,16 @@ comera_status sweep_backward(const comera_ttm_plan_s *p, int64_t b, const void *
         if (int e = dw_gemm(sp, Za, sp->N_in, Hb, sp->N_out, K, gr.ws[g], &dwp, &splits, stream))
             return status_of(e);
         bool want[kMaxCores];
-        for (int j = 0; j < sp->d; ++j) want[j] = dG[L.s[g] + j] != nullptr;
+        for (int j = 0; j < sp->d; ++j) {
+            const int k = L.s[g] + j;
+            want[j] = (dG && dG[k]) || (dD && k + 1 < d && dD[k]);
+        }
         if (int e = project_cores(sp, gr.bd[g], dwp, splits, want, gr.ws[g], part + L.s[g], nsplit + L.s[g], stream))
             return status_of(e);
     }
     timing_end(const_cast<comera_ttm_plan_s *>(p), COMERA_KERNEL_DW, stream, ev);
-    return status_of(expand_cores(p, part, nsplit, L.st, D, dG, stream));
+    if (dG && expand_cores(p, part, nsplit, L.st, D, dG, stream)) return COMERA_ERR_HIP;
+    return status_of(mask_grads(p, part, nsplit, L.st, G, dD, stream));
 }
 
 }  // namespace comera

@@ -140,6 +140,52 @@ __global__ __launch_bounds__(256) void expand_kernel(ExpandArgs a) {
     }
 }
 
+// Mask gradients (chain rule through eq. Wcompress): with dG~_k the gradient
+// of the masked core G~_k = G_k D_k (the sum of the compacted partials),
+//   dD_k[c] = sum_{a, m, n} dG~_k[a, m, n, c] G_k[a, m, n, c].
+// One workgroup per (bond k, entry c): thread t sums the elements t, t + 256,
+// ... in that order (each from its split partials in split order), then a
+// fixed-shape tree adds the 256 thread sums, so the result is bitwise
+// reproducible.  Entries dropped by the compaction (declared inactive) get 0.
+__global__ __launch_bounds__(256) void mask_grad_kernel(MaskGradArgs a) {
+    __shared__ float red[256];
+    int k = 0;
+    while (k + 1 < a.d - 1 && int(blockIdx.x) >= a.blk0[k + 1]) ++k;
+    float *out = a.dD[k];
+    if (!out) return;
+    const int c = int(blockIdx.x) - a.blk0[k];
+    const int rl = a.r[k], rr = a.r[k + 1], m = a.m[k], n = a.n[k];
+    const int cc = a.compacted ? rank_bit(a.act[k + 1], c) : c;
+    if (cc < 0) {
+        if (threadIdx.x == 0) out[c] = 0.f;
+        return;
+    }
+    const int64_t csize = int64_t(a.rc[k]) * m * n * a.rc[k + 1];
+    const CoreStrides st = a.st[k];
+    const float *part = a.part[k];
+    const float *G = a.G[k];
+    const int S = a.splits[k];
+    const int mn_ = m * n;
+    float v = 0.f;
+    for (int e = threadIdx.x; e < rl * mn_; e += 256) {
+        const int al = e / mn_, mn = e - al * mn_;
+        const int ca = (a.compacted && k > 0) ? rank_bit(a.act[k], al) : al;
+        if (ca < 0) continue;   // inactive left slice: G~_{k-1} is zero there, so is dG~_k
+        const int jm = mn / n, in = mn - jm * n;
+        const int64_t ci = int64_t(ca) * st.sa + jm * st.sm + in * st.sn + int64_t(cc) * st.sc;
+        float g = 0.f;
+        for (int s = 0; s < S; ++s) g += part[s * csize + ci];
+        v += g * G[int64_t(e) * rr + c];
+    }
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (int(threadIdx.x) < w) red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) out[c] = red[0];
+}
+
 __global__ void sum_splits_kernel(const float *__restrict__ part, float *__restrict__ out, int64_t n, int splits) {
     for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
         float v = 0.f;
@@ -235,6 +281,19 @@ int launch_expand(const ExpandArgs &a_in, void *stream) {
     for (int k = a.d; k < kMaxCores; ++k) a.blk0[k] = blocks;
     if (blocks == 0) return 0;
     hipLaunchKernelGGL(expand_kernel, dim3(unsigned(blocks)), dim3(256), 0, hipStream_t(stream), a);
+    return int(hipGetLastError());
+}
+
+int launch_mask_grad(const MaskGradArgs &a_in, void *stream) {
+    MaskGradArgs a = a_in;
+    int blocks = 0;
+    for (int k = 0; k + 1 < a.d; ++k) {
+        a.blk0[k] = blocks;
+        blocks += a.dD[k] ? a.r[k + 1] : 0;
+    }
+    for (int k = std::max(0, a.d - 1); k < kMaxCores; ++k) a.blk0[k] = blocks;
+    if (blocks == 0) return 0;
+    hipLaunchKernelGGL(mask_grad_kernel, dim3(unsigned(blocks)), dim3(256), 0, hipStream_t(stream), a);
     return int(hipGetLastError());
 }
 

@@ -71,6 +71,16 @@ class TTMRun:
         return dX, dG
 
 
+    def backward_masks(self, X, dY, b=None, want_dx=True, want_dg=True):
+        torch, dev = torch_dev()
+        b = self.b if b is None else b
+        dX = torch.empty((b, self.n_in), dtype=self.tdt, device=dev) if want_dx else None
+        dG = [torch.empty_like(g) for g in self.G] if want_dg else None
+        dD = [torch.empty(self.G[k].shape[3], dtype=torch.float32, device=dev) for k in range(len(self.G) - 1)]
+        C.comera_ttm_backward_masks(self.plan.handle, b, X, dY, self.G, self.D, dX, dG, dD, self.ws)
+        return dX, dG, dD
+
+
 class EmbedRun:
     def __init__(self, v, e, r, cores, masks, n_tokens):
         torch, dev = torch_dev()

@@ -158,6 +158,14 @@ def test_call_errors_before_launch():
     assert lib.comera_ttm_backward(p.handle, 4, fake, fake, G, None, fake, None, fake, 1, None) == C.ERR_WORKSPACE
     # empty batch is a no-op that needs nothing
     assert lib.comera_ttm_forward(p.handle, 0, None, None, None, None, None, 0, None) == C.OK
+    # the mask-gradient variant checks the same arguments
+    dD = C._ptr_array([fake])
+    assert lib.comera_ttm_backward_masks(p.handle, 4, fake, None, G, None, fake, None, dD, fake, 1 << 20,
+                                         None) == C.ERR_INVALID_ARG
+    assert lib.comera_ttm_backward_masks(p.handle, 4, None, fake, G, None, None, None, dD, fake, 1 << 20,
+                                         None) == C.ERR_INVALID_ARG      # dD needs X
+    assert lib.comera_ttm_backward_masks(p.handle, 4, fake, fake, G, None, None, None, dD, fake, 1,
+                                         None) == C.ERR_WORKSPACE
     # plan settings
     assert lib.comera_ttm_plan_set_reuse_forward(None, 1) == C.ERR_INVALID_ARG
     assert lib.comera_ttm_plan_set_reuse_forward(p.handle, 1) == C.OK

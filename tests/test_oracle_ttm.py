@@ -181,6 +181,19 @@ def test_mask_grad_homogeneity(seed, d):
         assert abs(float(g @ np.asarray(D[k], np.float64)) - ydy) < 1e-10 * max(1.0, abs(ydy))
 
 
+def test_mask_grad_term_scale_bounds():
+    """|dD_k[c]| <= sum |terms| (triangle inequality), with equality when
+    every term has one sign (all-positive data)."""
+    shape, cores, D, X, dY = _rand_problem(30, 3, b=4)
+    for g, sc in zip(ttm.mask_grads_direct(X, dY, cores, D), ttm.mask_grad_term_scale(X, dY, cores, D)):
+        assert np.all(np.abs(g) <= sc * (1 + 1e-12) + 1e-15)
+    pos = [np.abs(np.asarray(c, np.float64)) for c in cores]
+    Dp = [np.abs(np.asarray(x, np.float64)) + 0.1 for x in D]
+    Xp, dYp = np.abs(X), np.abs(dY)
+    for g, sc in zip(ttm.mask_grads_direct(Xp, dYp, pos, Dp), ttm.mask_grad_term_scale(Xp, dYp, pos, Dp)):
+        np.testing.assert_allclose(g, sc, rtol=1e-12)
+
+
 def test_mask_grad_bottleneck_closed_form():
     """Two cores with unit modes (input core [1, 1, N, r], output core
     [r, M, 1, 1]) give W = A diag(D) B with A = G_0[0, 0, :, :] and
