@@ -360,8 +360,9 @@ def other_workloads(steps, warmup):
         stream = None             # the current stream
 
         def step():
+            # a training step: the backward takes the forward's prefix table
             C.comera_tt_embed_forward(shape, ids, n, cores, None, Y, ws, None, stream)
-            C.comera_tt_embed_backward(shape, ids, n, dYe, cores, None, dG, 1, ws, None, stream)
+            C.comera_tt_embed_backward_ex(shape, ids, n, dYe, cores, None, dG, C.EMBED_REUSE_FORWARD, ws, None, stream)
 
         def fstep():
             C.comera_tt_embed_forward(shape, ids, n, cores, None, Y, ws, None, stream)

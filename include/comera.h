@@ -234,6 +234,20 @@ comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int
                                        float *const *dG, int32_t deterministic, void *ws,
                                        size_t ws_bytes, int32_t *err_flag, void *stream);
 
+/* comera_tt_embed_backward with options.  flags: bitwise OR of
+ *   COMERA_EMBED_REUSE_FORWARD  take the masked prefix cores and the prefix
+ *       table from the workspace, where the last comera_tt_embed_forward
+ *       call with this workspace, the same shape, n_tokens, G and D left
+ *       them (a training step's forward then backward); otherwise the
+ *       results are undefined (no error can be detected).
+ * Unknown flag bits are an error (COMERA_ERR_INVALID_ARG). */
+#define COMERA_EMBED_REUSE_FORWARD 1
+comera_status comera_tt_embed_backward_ex(const comera_tt_embed_shape *s, const int64_t *ids,
+                                          int64_t n_tokens, const float *dY,
+                                          const float *const *G, const float *const *D,
+                                          float *const *dG, int32_t flags, void *ws,
+                                          size_t ws_bytes, int32_t *err_flag, void *stream);
+
 /* Static English text for a status code. */
 const char *comera_status_string(comera_status s);
 

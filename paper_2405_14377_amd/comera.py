@@ -27,7 +27,7 @@ EXPORTS = (
     "comera_ttm_backward", "comera_ttm_plan_destroy", "comera_tt_embed_workspace_bytes",
     "comera_tt_embed_forward", "comera_tt_embed_backward", "comera_status_string", "comera_last_hip_error",
     "comera_ttm_plan_set_timing", "comera_ttm_plan_kernel_time", "comera_ttm_plan_set_reuse_forward",
-    "comera_ttm_backward_masks",
+    "comera_ttm_backward_masks", "comera_tt_embed_backward_ex",
 )
 KERNEL_FWD, KERNEL_DX, KERNEL_DW = 0, 1, 2
 
@@ -97,6 +97,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comera_tt_embed_forward.restype = i32
     lib.comera_tt_embed_backward.argtypes = [P(comera_tt_embed_shape), vp, i64, vp, vp, vp, vp, i32, vp, sz, vp, vp]
     lib.comera_tt_embed_backward.restype = i32
+    lib.comera_tt_embed_backward_ex.argtypes = [P(comera_tt_embed_shape), vp, i64, vp, vp, vp, vp, i32, vp, sz, vp,
+                                                vp]
+    lib.comera_tt_embed_backward_ex.restype = i32
     lib.comera_ttm_plan_set_timing.argtypes = [vp, i32]
     lib.comera_ttm_plan_set_reuse_forward.argtypes = [vp, i32]
     lib.comera_ttm_plan_set_reuse_forward.restype = i32
@@ -281,6 +284,18 @@ def comera_tt_embed_backward(shape, ids, n_tokens: int, dY, G, D, dG, determinis
                                          _ptr_array(D), _ptr_array(dG), int(deterministic), _ptr(ws), _nbytes(ws),
                                          _ptr(err_flag), _stream(stream))
     _check(st, "comera_tt_embed_backward")
+    return st
+
+
+EMBED_REUSE_FORWARD = 1
+
+
+def comera_tt_embed_backward_ex(shape, ids, n_tokens: int, dY, G, D, dG, flags: int, ws, err_flag=None,
+                                stream=None) -> int:
+    st = load().comera_tt_embed_backward_ex(ctypes.byref(shape), _ptr(ids), int(n_tokens), _ptr(dY), _ptr_array(G),
+                                            _ptr_array(D), _ptr_array(dG), int(flags), _ptr(ws), _nbytes(ws),
+                                            _ptr(err_flag), _stream(stream))
+    _check(st, "comera_tt_embed_backward_ex")
     return st
 
 

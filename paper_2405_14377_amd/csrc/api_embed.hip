@@ -155,6 +155,16 @@ int build_prefix(const comera_tt_embed_shape *s, const EmbedLayout &L, const flo
     return 0;
 }
 
+// pointers of the folded prefix cores and chains that build_prefix wrote
+int prefix_ptrs(const comera_tt_embed_shape *s, const EmbedLayout &L, void *ws, float **gc, float **P) {
+    const int d = s->d;
+    if (d == 1) return 0;
+    for (int k = 0; k < d - 1; ++k) gc[k] = reinterpret_cast<float *>(at(ws, L.gc[k]));
+    P[1] = gc[0];
+    for (int k = 1; k < d - 1; ++k) P[k + 1] = reinterpret_cast<float *>(at(ws, L.p[k + 1]));
+    return 0;
+}
+
 EmbedWs embed_ws(const EmbedLayout &L, void *ws) {
     EmbedWs w;
     w.keysA = reinterpret_cast<uint32_t *>(at(ws, L.keysA));
@@ -221,6 +231,14 @@ comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int
                                        float *const *dG, int32_t deterministic, void *ws, size_t ws_bytes,
                                        int32_t *err_flag, void *stream) {
     (void)deterministic;
+    return comera_tt_embed_backward_ex(s, ids, n_tokens, dY, G, D, dG, 0, ws, ws_bytes, err_flag, stream);
+}
+
+comera_status comera_tt_embed_backward_ex(const comera_tt_embed_shape *s, const int64_t *ids, int64_t n_tokens,
+                                          const float *dY, const float *const *G, const float *const *D,
+                                          float *const *dG, int32_t flags, void *ws, size_t ws_bytes,
+                                          int32_t *err_flag, void *stream) {
+    if (flags & ~int32_t(COMERA_EMBED_REUSE_FORWARD)) return COMERA_ERR_INVALID_ARG;
     EmbedDims dm;
     if (!embed_dims(s, dm) || n_tokens < 0 || n_tokens >= 2147483647) return COMERA_ERR_INVALID_ARG;
     if (!embed_supported(dm) || !embed_proj_ok(s)) return COMERA_ERR_UNSUPPORTED;
@@ -241,7 +259,8 @@ comera_status comera_tt_embed_backward(const comera_tt_embed_shape *s, const int
     if (!ws || ws_bytes < L.total) return COMERA_ERR_WORKSPACE;
     float *gc[kMaxCores] = {};
     float *P[kMaxCores + 1] = {};
-    int e = build_prefix(s, L, G, D, ws, stream, gc, P);
+    int e = (flags & COMERA_EMBED_REUSE_FORWARD) ? prefix_ptrs(s, L, ws, gc, P)
+                                                 : build_prefix(s, L, G, D, ws, stream, gc, P);
     if (e) return COMERA_ERR_HIP;
     const float *Apre = d > 1 ? P[d - 1] : nullptr;
     EmbedWs w = embed_ws(L, ws);

@@ -141,6 +141,72 @@ __global__ __launch_bounds__(256) void embed_rows_kernel(const int64_t *__restri
     }
 }
 
+// Rows on MFMA (v_mfma_f32_16x16x4f32), one wave per token: the row is the
+// product out[ep][es] = sum_a A[vp, ep, a] G_last[a, vs, es], an
+// (Ep x R) x (R x Es) product with Ep = 16 NT, R <= 4 NS, Es <= 16.  Lane
+// l = 16 q + r supplies A[16 t + r][4 s + q] and B[4 s + q][r] and receives
+// rows 4 q + v, column r of each 16 x 16 output tile t; the tile goes
+// through the wave's LDS region so that the row is written with 16-byte
+// stores.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int NT, int NS>
+__global__ __launch_bounds__(256) void embed_rows_mfma_kernel(const int64_t *__restrict__ ids, int64_t n_tokens,
+                                                              int64_t V, const float *__restrict__ Apre,
+                                                              const float *__restrict__ Gs, float *__restrict__ Y,
+                                                              int R, int Vs, int Es, int sE, int sR,
+                                                              int *__restrict__ err_flag) {
+    constexpr int Ep = 16 * NT;
+    __shared__ __attribute__((aligned(16))) float rowbuf[4][Ep * 16];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t t = int64_t(blockIdx.x) * 4 + wave;
+    if (t >= n_tokens) return;
+    const int64_t id = wave_uniform64(ids[t]);
+    const int E = Ep * Es;
+    float *yrow = Y + t * E;
+    if (id < 0 || id >= V) {
+        if (lane == 0 && err_flag) *err_flag = 1;
+        for (int o = lane; o < E; o += 64) yrow[o] = 0.f;
+        return;
+    }
+    const uint32_t vp = uint32_t(id) / uint32_t(Vs);        // ids are below 2^31
+    const int vs = int(uint32_t(id) - vp * uint32_t(Vs));
+    const int r = lane & 15, q = lane >> 4;
+    // operands, every load issued before the first product
+    float av[NT][NS], bv[NS];
+    const float *ar = Apre ? Apre + int64_t(vp) * Ep * R : nullptr;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const int a = 4 * s + q;
+        const bool ok = a < R;
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+            av[tt][s] = ok ? (ar ? ar[int64_t(16 * tt + r) * sE + int64_t(a) * sR] : 1.f) : 0.f;
+        bv[s] = (ok && r < Es) ? Gs[(int64_t(a) * Vs + vs) * Es + r] : 0.f;
+    }
+    f32x4 acc[NT];
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+        acc[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s) acc[tt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[tt][s], bv[s], acc[tt], 0, 0, 0);
+    }
+    // tile -> LDS as out[ep][es] (pitch Es), then whole-row stores
+    float *rb = rowbuf[wave];
+    if (r < Es)
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) rb[(16 * tt + 4 * q + v) * Es + r] = acc[tt][v];
+    wave_sync_lds();
+    if ((E & 3) == 0 && (reinterpret_cast<uintptr_t>(yrow) & 15) == 0) {
+        for (int o = 4 * lane; o < E; o += 256)
+            *reinterpret_cast<float4 *>(yrow + o) = *reinterpret_cast<const float4 *>(rb + o);
+    } else {
+        for (int o = lane; o < E; o += 64) yrow[o] = rb[o];
+    }
+}
+
 // ---------------------------------------------------------------- radix sort
 // Stable LSD radix sort of (key, token) pairs, 8-bit digits, kBlk keys per
 // workgroup.  Keys are the ids; out-of-range ids get the key V and sort last.
@@ -624,6 +690,179 @@ __global__ __launch_bounds__(256) void embed_dglast_kernel(const int *__restrict
     }
 }
 
+// MFMA forms of the two per-id contractions (v_mfma_f32_16x16x4f32; lane
+// l = 16 q + r supplies A[row 16 t + r][k 4 s + q], B[k 4 s + q][col 16 c + r]
+// and receives rows 4 q + v, column r of each 16 x 16 tile).  One wave owns
+// one accumulator set and walks its ids in id order, so every sum keeps the
+// fixed order of the LDS kernels above.
+//
+// dA: one workgroup per prefix vp (Ep = 16 NT, R <= 32, Es <= 4 NKS); its
+// ids, in id order, are cut into four contiguous quarters, wave w sums
+// quarter w, and the four partial sums are added in wave order:
+//   dA[vp][ep][a] = sum_u sum_es S_u[ep][es] G_last[a][vs_u][es]
+// The contraction index es runs in the order es = NKS q + k (k-th product,
+// lane group q), so each lane reads NKS consecutive floats of S_u and of
+// G_last.
+template <int NT, int NKS>
+__global__ __launch_bounds__(256) void embed_dapre_mfma_kernel(const int *__restrict__ headpos,
+                                                               const float *__restrict__ S,
+                                                               const float *__restrict__ Gs, int64_t Vp, int R,
+                                                               int Vs, int Es, int vq, int eq,
+                                                               float *__restrict__ dA) {
+    constexpr int Ep = 16 * NT;
+    __shared__ int vsl[1024], hpl[1024];
+    __shared__ int nid;
+    __shared__ float red[3][Ep][33];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t vp = blockIdx.x;
+    const int r = lane & 15, q = lane >> 4;
+    const int E = Ep * Es;
+    if (wave == 0) {
+        int cnt = 0;
+        for (int j0 = 0; j0 < Vs; j0 += 64) {
+            const int j = j0 + lane;
+            const int hp = j < Vs ? headpos[vp * Vs + j] : -1;
+            const uint64_t m = __ballot(hp >= 0);
+            if (hp >= 0) {
+                const int slot = cnt + __popcll(m & lanemask_lt());
+                vsl[slot] = j;
+                hpl[slot] = hp;
+            }
+            cnt += __popcll(m);
+        }
+        if (lane == 0) nid = cnt;
+    }
+    __syncthreads();
+    const int ni = nid;
+    if (ni == 0) return;               // no ids under this prefix: dA stays as cleared (0)
+    const int u0 = (ni * wave) / 4, u1 = (ni * (wave + 1)) / 4;
+    f32x4 acc[NT][2];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) acc[t][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int u = u0; u < u1; ++u) {
+        const int vs = vsl[u];
+        const float *su = S + int64_t(hpl[u]) * E;
+        float sa[NT][NKS], gb[2][NKS];
+#pragma unroll
+        for (int k = 0; k < NKS; ++k) {
+            const int es = NKS * q + k;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) sa[t][k] = es < Es ? su[(16 * t + r) * Es + es] : 0.f;
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const int a = 16 * c + r;
+                gb[c][k] = (es < Es && a < R) ? Gs[(int64_t(a) * Vs + vs) * Es + es] : 0.f;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < NKS; ++k)
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int c = 0; c < 2; ++c)
+                    acc[t][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(sa[t][k], gb[c][k], acc[t][c], 0, 0, 0);
+    }
+    // waves 1..3 hand their sums to wave 0, which adds them in wave order
+    for (int w = 1; w < 4; ++w) {
+        if (wave == w)
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+#pragma unroll
+                    for (int c = 0; c < 2; ++c) red[w - 1][16 * t + 4 * q + v][16 * c + r] = acc[t][c][v];
+    }
+    __syncthreads();
+    if (wave != 0) return;
+    // dA[vp] written blocked for the prefix-core projections
+    const int Vh = int(vp / vq), x = int(vp - int64_t(Vh) * vq);
+    const int NEq = Ep / eq;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int ep = 16 * t + 4 * q + v;
+            const int Eh = ep / eq, y = ep - Eh * eq;
+            float *dst = dA + (((int64_t(Vh) * NEq + Eh) * vq + x) * eq + y) * R;
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const int a = 16 * c + r;
+                const float sum = ((acc[t][c][v] + red[0][ep][a]) + red[1][ep][a]) + red[2][ep][a];
+                if (a < R) dst[a] = sum;
+            }
+        }
+}
+
+// dG_last: one wave per (vs, chunk of kGlVp prefixes) (Ep = 4 NKE, R <= 32,
+// Es <= 16), over the ids vp Vs + vs of the chunk in vp order:
+//   part[chunk][a][vs][es] = sum_u sum_ep A[vp_u, ep, a] S_u[ep][es]
+template <int NKE>
+__global__ __launch_bounds__(256) void embed_dglast_mfma_kernel(const int *__restrict__ headpos,
+                                                                const float *__restrict__ S,
+                                                                const float *__restrict__ Apre, int sE, int sR,
+                                                                int64_t Vp, int R, int Vs, int Es, int nchunk,
+                                                                float *__restrict__ part) {
+    constexpr int Ep = 4 * NKE;
+    const int lane = threadIdx.x & 63;
+    const int wv = int(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    if (wv >= Vs * nchunk) return;
+    const int vs = wv % Vs, chunk = wv / Vs;
+    const int r = lane & 15, q = lane >> 4;
+    const int E = Ep * Es;
+    f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+    const int64_t vp0 = int64_t(chunk) * kGlVp;
+    const int hp_l = (lane < kGlVp && vp0 + lane < Vp) ? headpos[(vp0 + lane) * Vs + vs] : -1;
+    uint64_t m = __ballot(hp_l >= 0);
+    while (m) {
+        const int bit = __builtin_ctzll(m);
+        m &= m - 1;
+        const int64_t vp = vp0 + bit;
+        const int hp = __shfl(hp_l, bit, 64);
+        const float *su = S + int64_t(hp) * E;
+        const float *ar = Apre ? Apre + vp * Ep * R : nullptr;
+        // contraction index ep = NKE q + k for the k-th product: lane group q
+        // reads NKE consecutive prefix-table entries per rank (16-byte loads
+        // when the table is rank-major)
+        float aa[2][NKE], sb[NKE];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const int a = 16 * c + r;
+            if (a < R && ar && sE == 1 && (NKE & 3) == 0) {
+                const float4 *p4 = reinterpret_cast<const float4 *>(ar + int64_t(a) * sR + NKE * q);
+#pragma unroll
+                for (int k4 = 0; k4 < NKE / 4; ++k4) {
+                    const float4 v = p4[k4];
+                    aa[c][4 * k4] = v.x;
+                    aa[c][4 * k4 + 1] = v.y;
+                    aa[c][4 * k4 + 2] = v.z;
+                    aa[c][4 * k4 + 3] = v.w;
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < NKE; ++k)
+                    aa[c][k] = a < R ? (ar ? ar[int64_t(NKE * q + k) * sE + int64_t(a) * sR] : 1.f) : 0.f;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < NKE; ++k) sb[k] = r < Es ? su[(NKE * q + k) * Es + r] : 0.f;
+#pragma unroll
+        for (int k = 0; k < NKE; ++k)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(aa[c][k], sb[k], acc[c], 0, 0, 0);
+    }
+    float *dst = part + int64_t(chunk) * R * Vs * Es;
+    if (r < Es)
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int a = 16 * c + 4 * q + v;
+                if (a < R) dst[(int64_t(a) * Vs + vs) * Es + r] = acc[c][v];
+            }
+}
+
 // d = 1: the table is the core itself; dG_0[0, v, e, 0] = S[headpos[v]][e].
 __global__ __launch_bounds__(256) void embed_gather_kernel(const int *__restrict__ headpos,
                                                            const float *__restrict__ S, int64_t V, int E,
@@ -685,12 +924,39 @@ void launch_rows_nj(int nj4, dim3 grid, void *stream, const int64_t *ids, int64_
     }
 }
 
+template <int NT>
+void launch_rows_mfma(int ns, dim3 grid, void *stream, const int64_t *ids, int64_t n, int64_t V, const float *Apre,
+                      const float *Gs, float *Y, int R, int Vs, int Es, int sE, int sR, int *err_flag) {
+    switch (ns) {
+        case 1: hipLaunchKernelGGL((embed_rows_mfma_kernel<NT, 1>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+        case 2: hipLaunchKernelGGL((embed_rows_mfma_kernel<NT, 2>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+        case 4: hipLaunchKernelGGL((embed_rows_mfma_kernel<NT, 4>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+        default: hipLaunchKernelGGL((embed_rows_mfma_kernel<NT, 8>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+    }
+}
+
 int launch_embed_rows(const int64_t *ids, int64_t n, int64_t V, const float *Apre, bool rank_major, const float *Gs,
                       float *Y, int Ep, int R, int Vs, int Es, int *err_flag, void *stream) {
     if (n <= 0) return 0;
     const dim3 grid(unsigned((n + 3) / 4));
     const int nj4 = (Es + 3) / 4;
     const int sE = rank_major ? 1 : R, sR = rank_major ? Ep : 1;
+    // MFMA rows when the product fits 16 x 16 tiles: Ep a multiple of 16 up
+    // to 128, Es <= 16, R <= 32
+    if (Ep % 16 == 0 && Ep <= 128 && Es <= 16 && R <= 32) {
+        const int ns = (R + 3) / 4 <= 1 ? 1 : ((R + 3) / 4 <= 2 ? 2 : ((R + 3) / 4 <= 4 ? 4 : 8));
+        switch (Ep / 16) {
+            case 1: launch_rows_mfma<1>(ns, grid, stream, ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+            case 2: launch_rows_mfma<2>(ns, grid, stream, ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+            case 3: launch_rows_mfma<3>(ns, grid, stream, ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+            case 4: launch_rows_mfma<4>(ns, grid, stream, ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+            case 5: launch_rows_mfma<5>(ns, grid, stream, ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+            case 6: launch_rows_mfma<6>(ns, grid, stream, ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+            case 7: launch_rows_mfma<7>(ns, grid, stream, ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+            default: launch_rows_mfma<8>(ns, grid, stream, ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+        }
+        return int(hipGetLastError());
+    }
     if (R <= 8) launch_rows_nj<8>(nj4, grid, stream, ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag);
     else if (R <= 16) launch_rows_nj<16>(nj4, grid, stream, ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag);
     else if (R <= 32) launch_rows_nj<32>(nj4, grid, stream, ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag);
@@ -737,6 +1003,21 @@ int launch_embed_segsum(const float *dY, int E, int n, int passes, const EmbedWs
 
 int launch_embed_dapre(const EmbedWs &w, const float *Gs, int64_t Vp, int Ep, int R, int Vs, int Es, int vq, int eq,
                        void *stream) {
+    if (Ep % 16 == 0 && Ep <= 64 && R <= 32 && Es <= 16 && Vs <= 1024) {
+        const dim3 grid(static_cast<unsigned>(Vp), 1, 1);
+#define COMERA_DAPRE(NT, NK)                                                                                     \
+    hipLaunchKernelGGL((embed_dapre_mfma_kernel<NT, NK>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, \
+                       Gs, Vp, R, Vs, Es, vq, eq, w.dA)
+        const int nk = (Es + 3) / 4;
+        switch (Ep / 16) {
+            case 1: if (nk <= 2) COMERA_DAPRE(1, 2); else COMERA_DAPRE(1, 4); break;
+            case 2: if (nk <= 2) COMERA_DAPRE(2, 2); else COMERA_DAPRE(2, 4); break;
+            case 3: if (nk <= 2) COMERA_DAPRE(3, 2); else if (nk == 3) COMERA_DAPRE(3, 3); else COMERA_DAPRE(3, 4); break;
+            default: if (nk <= 2) COMERA_DAPRE(4, 2); else if (nk == 3) COMERA_DAPRE(4, 3); else COMERA_DAPRE(4, 4); break;
+        }
+#undef COMERA_DAPRE
+        return int(hipGetLastError());
+    }
     const int nb = dapre_batch(Ep, R, Vs, Es);
     if (nb <= 0) return int(hipErrorInvalidValue);
     const size_t lds = dapre_lds_bytes(Ep, R, Vs, Es, nb);
@@ -755,6 +1036,17 @@ int embed_dglast_chunks(int64_t Vp) { return int((Vp + kGlVp - 1) / kGlVp); }
 int launch_embed_dglast(const EmbedWs &w, const float *Apre, bool rank_major, int64_t Vp, int Ep, int R, int Vs,
                         int Es, void *stream) {
     const int sE = rank_major ? 1 : R, sR = rank_major ? Ep : 1;
+    if (Ep % 16 == 0 && Ep <= 64 && R <= 32 && Es <= 16) {
+        const int nchunk = embed_dglast_chunks(Vp);
+        const dim3 grid(unsigned((int64_t(Vs) * nchunk + 3) / 4));
+        switch (Ep / 16) {
+            case 1: hipLaunchKernelGGL((embed_dglast_mfma_kernel<4>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
+            case 2: hipLaunchKernelGGL((embed_dglast_mfma_kernel<8>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
+            case 3: hipLaunchKernelGGL((embed_dglast_mfma_kernel<12>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
+            default: hipLaunchKernelGGL((embed_dglast_mfma_kernel<16>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
+        }
+        return int(hipGetLastError());
+    }
     const int nb = dglast_batch(Ep, R, Es);
     if (nb <= 0) return int(hipErrorInvalidValue);
     const size_t lds = dglast_lds_bytes(Ep, R, Es, nb);

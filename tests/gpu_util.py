@@ -103,6 +103,11 @@ class EmbedRun:
         C.comera_tt_embed_forward(self.shape, ids_t, self.n, self.G, self.D, Y, self.ws, self.err)
         return Y
 
+    def backward_ex(self, ids_t, dY_t, flags):
+        dG = [torch_dev()[0].empty_like(g) for g in self.G]
+        C.comera_tt_embed_backward_ex(self.shape, ids_t, self.n, dY_t, self.G, self.D, dG, flags, self.ws, self.err)
+        return dG
+
     def backward(self, ids_t, dY_t, deterministic=1):
         dG = [torch_dev()[0].empty_like(g) for g in self.G]
         C.comera_tt_embed_backward(self.shape, ids_t, self.n, dY_t, self.G, self.D, dG, deterministic, self.ws,

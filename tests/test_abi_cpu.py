@@ -186,6 +186,10 @@ def test_embed_workspace_and_errors():
     dG = C._ptr_array([fake, None, fake])
     assert lib.comera_tt_embed_backward(s, fake, 4, fake, G, None, dG, 1, fake, 1 << 30, None,
                                         None) == C.ERR_INVALID_ARG
+    # unknown option bits are refused before any device work
+    G3 = C._ptr_array([fake, fake, fake])
+    assert lib.comera_tt_embed_backward_ex(s, fake, 4, fake, G3, None, G3, 2, fake, 1 << 30, None,
+                                           None) == C.ERR_INVALID_ARG
     # too large for the kernels' LDS staging: refused, not run
     big = C.tt_embed_shape((4, 4), (4096, 64), (1, 64, 1))
     assert lib.comera_tt_embed_forward(big, fake, 4, C._ptr_array([fake, fake]), None, fake, fake, 1 << 40, None,
