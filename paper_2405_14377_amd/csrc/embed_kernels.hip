@@ -296,15 +296,47 @@ __global__ __launch_bounds__(1024) void radix_scan_kernel(int *hist, int nblk, c
     }
 }
 
+// With scan != 0 (few blocks) the workgroup derives its own digit offsets
+// from the raw histograms: offs[dg][b] = sum of all counts of digits below
+// dg plus the counts of digit dg in blocks below b (and block 0 writes
+// meta[0] = n - out-of-range ids when bad != null), so no scan kernel runs.
 __global__ __launch_bounds__(256) void radix_scatter_kernel(const int64_t *__restrict__ ids, const uint32_t *kin,
                                                             const uint32_t *vin, int n, int64_t V, int shift, int nblk,
                                                             const int *__restrict__ offs, uint32_t *kout,
-                                                            uint32_t *vout) {
+                                                            uint32_t *vout, int scan, const int *bad, int *meta) {
     __shared__ int wcount[kSub * 4][256];
+    __shared__ int dbase[256];
+    __shared__ int wsum[4];
     const int tid = threadIdx.x, w = tid >> 6;
     for (int i = tid; i < kSub * 4 * 256; i += 256) (&wcount[0][0])[i] = 0;
-    __syncthreads();
     const int b = blockIdx.x;
+    if (scan) {
+        // thread tid = digit: its total and its count in the blocks below b
+        int tot = 0, below = 0;
+        for (int bb = 0; bb < nblk; ++bb) {
+            const int h = offs[tid * nblk + bb];
+            tot += h;
+            below += bb < b ? h : 0;
+        }
+        // exclusive scan of the digit totals (wave scans, then the four waves)
+        const int lane = tid & 63;
+        int x = tot;
+        for (int off = 1; off < 64; off <<= 1) {
+            const int y = __shfl_up(x, off, 64);
+            if (lane >= off) x += y;
+        }
+        if (lane == 63) wsum[w] = x;
+        __syncthreads();
+        int pre = 0;
+        for (int ww = 0; ww < w; ++ww) pre += wsum[ww];
+        dbase[tid] = pre + x - tot + below;
+        if (b == 0 && tid == 0 && bad) {
+            int nb = 0;
+            for (int bb = 0; bb < nblk; ++bb) nb += bad[bb];
+            meta[0] = n - nb;
+        }
+    }
+    __syncthreads();
     uint32_t key[kSub], val[kSub], dg[kSub];
     int rank[kSub];
     bool valid[kSub];
@@ -346,7 +378,7 @@ __global__ __launch_bounds__(256) void radix_scatter_kernel(const int64_t *__res
 #pragma unroll
     for (int j = 0; j < kSub; ++j) {
         if (!valid[j]) continue;
-        const int pos = offs[dg[j] * nblk + b] + wcount[j * 4 + w][dg[j]] + rank[j];
+        const int pos = (scan ? dbase[dg[j]] : offs[dg[j] * nblk + b]) + wcount[j * 4 + w][dg[j]] + rank[j];
         kout[pos] = key[j];
         vout[pos] = val[j];
     }
@@ -978,10 +1010,13 @@ int launch_embed_sort(const int64_t *ids, int n, int64_t V, int passes, const Em
         hipLaunchKernelGGL(radix_hist_kernel, dim3(nblk + nclr), dim3(256), 0, hipStream_t(stream), ids, kin, n, V,
                            8 * p, nblk, w.hist, p == 0 ? bad : nullptr, err_flag, w.headpos, p == 0 ? nclear : 0,
                            zero, p == 0 ? nzero : 0);
-        hipLaunchKernelGGL(radix_scan_kernel, dim3(1), dim3(1024), 0, hipStream_t(stream), w.hist, nblk,
-                           p == 0 ? bad : nullptr, n, w.meta);
+        // up to 64 blocks, each scatter workgroup scans the histograms itself
+        const int self_scan = nblk <= 64 ? 1 : 0;
+        if (!self_scan)
+            hipLaunchKernelGGL(radix_scan_kernel, dim3(1), dim3(1024), 0, hipStream_t(stream), w.hist, nblk,
+                               p == 0 ? bad : nullptr, n, w.meta);
         hipLaunchKernelGGL(radix_scatter_kernel, dim3(nblk), dim3(256), 0, hipStream_t(stream), ids, kin, vin, n, V,
-                           8 * p, nblk, w.hist, kout, vout);
+                           8 * p, nblk, w.hist, kout, vout, self_scan, p == 0 ? bad : nullptr, w.meta);
         kin = kout;
         vin = vout;
         kout = (kout == w.keysA) ? w.keysB : w.keysA;
