@@ -13,8 +13,10 @@ same on the GPU side):
   (mantissa LSB 0), magnitudes above 448 saturate to 448;
 * scaling: one power of two per tensor, s = 2^e with e the largest integer
   such that amax * s <= 448 (amax = max |x| of the fp32 values; s = 1 when
-  amax = 0).  x * s is then exact in fp32, so the only rounding decision is
-  the FP8 one, taken on the fp32 value x * s.
+  amax = 0), e clamped to [-60, 60] so that s and the product scales
+  1 / (s s') of two tensors stay finite normal fp32 numbers.  x * s is then
+  exact in fp32, so the only rounding decision is the FP8 one, taken on the
+  fp32 value x * s.
 
 Written from the format's definition with numpy; pinned against an
 independent implementation (torch.float8_e4m3fn casts) and the format's
@@ -70,14 +72,18 @@ def encode(x) -> np.ndarray:
     return (code | np.where(np.signbit(x), 0x80, 0)).astype(np.uint8)
 
 
+E_MIN, E_MAX = -60, 60
+
+
 def pow2_scale(amax: float) -> float:
-    """Largest power of two s with amax * s <= 448 (1 when amax is 0)."""
+    """Largest power of two s = 2^e with amax * s <= 448, e clamped to
+    [E_MIN, E_MAX] (1 when amax is 0)."""
     amax = float(amax)
     if amax == 0.0 or not math.isfinite(amax):
         return 1.0
     f, k = math.frexp(amax)                      # amax = f 2^k, 0.5 <= f < 1
     e = 9 - k if f <= 0.875 else 8 - k           # 448 = 0.875 2^9
-    return math.ldexp(1.0, e)
+    return math.ldexp(1.0, min(max(e, E_MIN), E_MAX))
 
 
 def quantize(x) -> tuple:

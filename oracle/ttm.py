@@ -202,10 +202,16 @@ def _mask_list(cores, masks) -> List[np.ndarray]:
 
 def mask_grads_dense(X, dY, cores, masks=None) -> List[np.ndarray]:
     """dD_k[c] = <dW, dW/dD_k[c]> for every bond k = 0..d-2 (chain rule through
-    eq. Wcompress).  W is linear in D_k, so dW/dD_k[c] is the layer rebuilt
-    with D_k replaced by the unit vector e_c and the other masks kept."""
+    eq. Wcompress), dW = X^T dY."""
+    return mask_grads_from_dW(_f64(X).T @ _f64(dY), cores, masks)
+
+
+def mask_grads_from_dW(dW, cores, masks=None) -> List[np.ndarray]:
+    """dD_k[c] = <dW, dW/dD_k[c]> for a given dW [N_in, N_out].  W is linear in
+    D_k, so dW/dD_k[c] is the layer rebuilt with D_k replaced by the unit
+    vector e_c and the other masks kept."""
     _check(cores)
-    dW = _f64(X).T @ _f64(dY)
+    dW = _f64(dW)
     base = _mask_list(cores, masks)
     out = []
     for k in range(len(cores) - 1):

@@ -49,12 +49,30 @@ def test_saturation_and_signed_zero():
     assert fp8.encode(np.array([-1e-6]))[0] == 0x80 and fp8.encode(np.array([1e-6]))[0] == 0x00
 
 
-@pytest.mark.parametrize("amax", [1.0, 448.0, 449.0, 3.5, 0.001, 1e-30, 7e4])
+@pytest.mark.parametrize("amax", [1.0, 448.0, 449.0, 3.5, 0.001, 1e-15, 7e4, 1e18, 2.0 ** -52, 2.0 ** 68])
 def test_pow2_scale(amax):
     s = fp8.pow2_scale(amax)
     assert math.log2(s) == int(math.log2(s))                 # a power of two
     assert amax * s <= 448.0 < amax * s * 2                  # the largest one
     assert fp8.pow2_scale(0.0) == 1.0
+
+
+def test_pow2_scale_clamp():
+    # exponents outside [-60, 60] are clamped, so that s and the inverse of a
+    # product of two scales, 1 / (s s'), stay finite normal fp32 numbers
+    assert fp8.pow2_scale(2.0 ** -52) == 2.0 ** 60          # 2^-52 2^60 = 256 <= 448 < 512: not clamped
+    assert fp8.pow2_scale(2.0 ** -53) == 2.0 ** 60          # would be 2^61: clamped
+    assert fp8.pow2_scale(1e-30) == 2.0 ** 60
+    assert fp8.pow2_scale(2.0 ** 68) == 2.0 ** -60          # 2^68 2^-60 = 256: not clamped
+    assert fp8.pow2_scale(2.0 ** 69) == 2.0 ** -60          # would be 2^-61: clamped
+    assert fp8.pow2_scale(1e30) == 2.0 ** -60
+    tiny = np.finfo(np.float32).tiny
+    for s1, s2 in [(2.0 ** 60, 2.0 ** 60), (2.0 ** -60, 2.0 ** -60)]:
+        inv = np.float32(1.0) / (np.float32(s1) * np.float32(s2))
+        assert np.isfinite(inv) and inv >= tiny
+    # at the lower clamp the codes saturate instead of overflowing
+    codes, s = fp8.quantize(np.array([1e30, -1e30, 1.0], dtype=np.float32))
+    assert s == 2.0 ** -60 and list(codes[:2]) == [0x7E, 0xFE]
 
 
 def test_quantize_exact_scaling():
