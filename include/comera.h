@@ -179,6 +179,41 @@ void comera_ttm_plan_destroy(comera_ttm_plan_t p);
  * Returns COMERA_ERR_INVALID_ARG for a NULL plan. */
 comera_status comera_ttm_plan_set_reuse_forward(comera_ttm_plan_t p, int32_t enable);
 
+/* Mixed-precision layer (appendix on mixed-precision CoMERA: contractions
+ * that carry the batch index run in a low precision, the batch-free ones in
+ * full precision).  With enable != 0 the three batch products of the dense
+ * order -- Y = X W, dX = dY W^T, dW = X^T dY -- read OCP FP8 E4M3 codes of
+ * X, dY and W in the format and scaling of comera_fp8_quantize (one scale
+ * per tensor and call), accumulate in fp32 and multiply by the inverse
+ * scales.  W is rebuilt from the cores in fp32; the projections of dW onto
+ * the cores, the mask gradients and every other batch-free step stay fp32.
+ * X, Y, dY and dX keep the plan's activation dtype.  K of each product is
+ * padded with zero codes to a multiple of 128.  Changes the workspace size:
+ * query comera_ttm_workspace_bytes afterwards.  Combines with reuse (the
+ * backward call then also takes the codes of W and X^T and their scales
+ * from the forward call).  Host only, no device work.  Returns
+ * COMERA_ERR_UNSUPPORTED if the plan's order is not the dense order (plan
+ * with force_order = 0) or a code buffer would exceed 2^32 bytes,
+ * COMERA_ERR_INVALID_ARG for a NULL plan.  Off by default. */
+comera_status comera_ttm_plan_set_fp8(comera_ttm_plan_t p, int32_t enable);
+
+/* OCP FP8 E4M3 codes of a row-major tensor x [rows, cols] (fp32 or bf16 by
+ * dtype) with one power-of-two scale: s = 2^e, e the largest integer with
+ * max|x| * s <= 448, clamped to [-60, 60] (s = 1 if x is all zeros); each
+ * code is x * s (exact in fp32) rounded to the nearest E4M3 value, ties to
+ * the even code, magnitudes above 448 saturated to 448, the sign bit kept
+ * (also where the value rounds to zero).  Inputs must be finite.
+ *   q      device [rows, ldq] codes of x, or NULL; columns cols..ldq-1 get 0.
+ *   qt     device [cols, ldt] codes of x^T, or NULL; columns rows..ldt-1 get 0.
+ *   scale  device float[1], receives s (x ~ value(code) / s).
+ *   ws     device scratch of ws_bytes >= COMERA_FP8_QUANTIZE_WS_BYTES.
+ * At least one of q, qt; ldq >= cols, ldt >= rows.  rows or cols == 0:
+ * nothing is written.  Asynchronous on stream. */
+#define COMERA_FP8_QUANTIZE_WS_BYTES 2048
+comera_status comera_fp8_quantize(const void *x, int32_t dtype, int64_t rows, int64_t cols,
+                                  uint8_t *q, int64_t ldq, uint8_t *qt, int64_t ldt,
+                                  float *scale, void *ws, size_t ws_bytes, void *stream);
+
 /* Diagnostics: per-kernel timing of the batch products of a plan.  While
  * enabled, forward and backward record a pair of HIP events on the call's
  * stream around each launch of the kernels below; comera_ttm_plan_kernel_time

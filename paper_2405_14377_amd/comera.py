@@ -27,8 +27,9 @@ EXPORTS = (
     "comera_ttm_backward", "comera_ttm_plan_destroy", "comera_tt_embed_workspace_bytes",
     "comera_tt_embed_forward", "comera_tt_embed_backward", "comera_status_string", "comera_last_hip_error",
     "comera_ttm_plan_set_timing", "comera_ttm_plan_kernel_time", "comera_ttm_plan_set_reuse_forward",
-    "comera_ttm_backward_masks", "comera_tt_embed_backward_ex",
+    "comera_ttm_backward_masks", "comera_tt_embed_backward_ex", "comera_ttm_plan_set_fp8", "comera_fp8_quantize",
 )
+FP8_QUANTIZE_WS_BYTES = 2048
 KERNEL_FWD, KERNEL_DX, KERNEL_DW = 0, 1, 2
 
 
@@ -103,6 +104,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comera_ttm_plan_set_timing.argtypes = [vp, i32]
     lib.comera_ttm_plan_set_reuse_forward.argtypes = [vp, i32]
     lib.comera_ttm_plan_set_reuse_forward.restype = i32
+    lib.comera_ttm_plan_set_fp8.argtypes = [vp, i32]
+    lib.comera_ttm_plan_set_fp8.restype = i32
+    lib.comera_fp8_quantize.argtypes = [vp, i32, i64, i64, vp, i64, vp, i64, vp, vp, sz, vp]
+    lib.comera_fp8_quantize.restype = i32
     lib.comera_ttm_plan_set_timing.restype = i32
     lib.comera_ttm_plan_kernel_time.argtypes = [vp, i32, P(dbl), P(i32)]
     lib.comera_ttm_plan_kernel_time.restype = i32
@@ -259,6 +264,18 @@ def comera_ttm_plan_set_reuse_forward(plan, enable: bool) -> None:
     _check(load().comera_ttm_plan_set_reuse_forward(plan, int(bool(enable))), "comera_ttm_plan_set_reuse_forward")
 
 
+def comera_ttm_plan_set_fp8(plan, enable: bool) -> None:
+    _check(load().comera_ttm_plan_set_fp8(plan, int(bool(enable))), "comera_ttm_plan_set_fp8")
+
+
+def comera_fp8_quantize(x, dtype: int, rows: int, cols: int, q, ldq: int, qt, ldt: int, scale, ws,
+                        stream=None) -> int:
+    st = load().comera_fp8_quantize(_ptr(x), int(dtype), int(rows), int(cols), _ptr(q), int(ldq), _ptr(qt), int(ldt),
+                                    _ptr(scale), _ptr(ws), _nbytes(ws), _stream(stream))
+    _check(st, "comera_fp8_quantize")
+    return st
+
+
 def comera_ttm_plan_kernel_time(plan, kernel: int):
     """(mean ms, launches) of one kernel since the last query; clears the record."""
     ms, cnt = ctypes.c_double(), ctypes.c_int32()
@@ -324,6 +341,9 @@ class TTMPlan:
 
     def set_reuse_forward(self, enable: bool = True) -> None:
         comera_ttm_plan_set_reuse_forward(self.handle, enable)
+
+    def set_fp8(self, enable: bool = True) -> None:
+        comera_ttm_plan_set_fp8(self.handle, enable)
 
     def __del__(self):
         try:

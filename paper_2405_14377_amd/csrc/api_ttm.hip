@@ -61,7 +61,7 @@ int fold_cores(const comera_ttm_plan_s *p, const float *const *G, const float *c
 int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, int want, void *stream) {
     const DenseLayout &L = sp->dense;
     const int d = sp->d;
-    const bool bf = sp->s.act == COMERA_BF16;
+    const bool bf = sp->s.act == COMERA_BF16 && !sp->fp8;   // FP8 layers build W in fp32
     bd.w = at(ws, L.w);
     bd.wt = at(ws, L.wt);
     if (d == 1) {
@@ -131,11 +131,11 @@ void built_dense(const comera_ttm_plan_s *p, void *ws, DenseBuild &bd, int want)
     bd.w = at(ws, p->dense.w);
     bd.wt = at(ws, p->dense.wt);
     // build_chain keeps a single fp32 core as W itself
-    if (p->d == 1 && p->s.act != COMERA_BF16 && want == kWantW) bd.w = bd.gc[0];
+    if (p->d == 1 && (p->s.act != COMERA_BF16 || p->fp8) && want == kWantW) bd.w = bd.gc[0];
 }
 
 int dw_gemm(const comera_ttm_plan_s *sp, const void *A, int64_t lda, const void *B, int64_t ldb, int64_t K,
-            void *ws, float **dwp, int *splits_out, void *stream) {
+            void *ws, float **dwp, int *splits_out, void *stream, const float *oscale) {
     const DenseLayout &L = sp->dense;
     const int d = sp->d;
     // written blocked as E_d[(I_<, J_<)][(x, y)] with x = i_{d-1}, y = j_{d-1}
@@ -145,10 +145,11 @@ int dw_gemm(const comera_ttm_plan_s *sp, const void *A, int64_t lda, const void 
     float *dw = reinterpret_cast<float *>(at(ws, L.dw));
     float *part = (splits > 1 || L.proj) ? reinterpret_cast<float *>(at(ws, L.dw_part)) : dw;
     GemmArgs g;
-    g.dtype = sp->s.act;
-    g.a_kc = false;
-    g.b_kc = false;
+    g.dtype = oscale ? kDtypeFp8 : sp->s.act;
+    g.a_kc = oscale != nullptr;
+    g.b_kc = oscale != nullptr;
     g.out_bf16 = false;
+    g.oscale = oscale;
     g.A = A;
     g.B = B;
     g.C = part;
@@ -340,6 +341,51 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
     return build_chain(p, ws, bd, want, stream);
 }
 
+inline uint8_t *codes(void *ws, size_t off) { return reinterpret_cast<uint8_t *>(at(ws, off)); }
+
+// Mixed-precision forward (the batch product on FP8 codes, the batch-free
+// build of W in fp32): W -> W^T codes (and W codes for a backward call that
+// reuses them), X -> X codes (and X^T codes likewise), Y = X8 W8 / (sX sW).
+comera_status fp8_forward(comera_ttm_plan_t p, int64_t b, const void *X, const float *const *G,
+                          const float *const *D, void *Y, void *ws, void *stream) {
+    const Fp8Layout &F = p->f8;
+    DenseBuild bd;
+    if (build_dense(p, G, D, ws, stream, bd, kWantW)) return COMERA_ERR_HIP;
+    float *sc = reinterpret_cast<float *>(at(ws, F.sc));
+    float *pmax = reinterpret_cast<float *>(at(ws, F.pmax));
+    int e = note_hip(launch_fp8_quant(bd.w, COMERA_F32, p->N_in, p->N_out, pmax, p->reuse ? codes(ws, F.w8) : nullptr,
+                                      F.nout_p, codes(ws, F.w8t), F.nin_p, sc + kScW, nullptr, nullptr, nullptr,
+                                      nullptr, stream),
+                     "FP8 codes of W");
+    if (!e)
+        e = note_hip(launch_fp8_quant(X, p->s.act, b, p->N_in, pmax, codes(ws, F.x8), F.nin_p,
+                                      p->reuse ? codes(ws, F.x8t) : nullptr, F.b_p, sc + kScX, sc + kScW,
+                                      sc + kScFwd, nullptr, nullptr, stream),
+                     "FP8 codes of X");
+    if (e) return COMERA_ERR_HIP;
+    void *ev;
+    timing_begin(p, COMERA_KERNEL_FWD, stream, &ev);
+    GemmArgs g;
+    g.dtype = kDtypeFp8;
+    g.a_kc = true;
+    g.b_kc = true;
+    g.out_bf16 = p->s.act == COMERA_BF16;
+    g.A = codes(ws, F.x8);
+    g.B = codes(ws, F.w8t);
+    g.C = Y;
+    g.M = b;
+    g.N = p->N_out;
+    g.K = F.nin_p;
+    g.lda = F.nin_p;
+    g.ldb = F.nin_p;
+    g.rmap = remap_linear(p->N_out);
+    g.cmap = remap_linear(1);
+    g.oscale = sc + kScFwd;
+    e = note_hip(launch_gemm(g, stream), "forward GEMM (FP8)");
+    timing_end(p, COMERA_KERNEL_FWD, stream, ev);
+    return e ? COMERA_ERR_HIP : COMERA_OK;
+}
+
 }  // namespace
 
 namespace comera {
@@ -395,6 +441,7 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, 
         if (!G[k]) return COMERA_ERR_INVALID_ARG;
     if (!ws || ws_bytes < p->ws_bytes) return COMERA_ERR_WORKSPACE;
     if (p->sweep.G > 0) return sweep_forward(p, b, X, G, D, Y, ws, stream);
+    if (p->fp8) return fp8_forward(p, b, X, G, D, Y, ws, stream);
     DenseBuild bd;
     // W^T for the forward product; with reuse also W for the backward call
     int e = build_dense(p, G, D, ws, stream, bd, kWantWT | (p->reuse ? kWantW : 0));
@@ -430,6 +477,55 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, 
 }  // extern "C"
 
 namespace {
+
+// Mixed-precision backward, up to dW: the codes of W (unless a forward call
+// left them), of X^T (for dW, likewise) and of dY / dY^T, then dX =
+// dY8 W8^T / (sdY sW).  Returns a HIP error code.
+int fp8_backward(comera_ttm_plan_t p, int64_t b, const void *X, const void *dY, const DenseBuild &bd, void *dX,
+                 bool want_grad, void *ws, void *stream) {
+    const Fp8Layout &F = p->f8;
+    float *sc = reinterpret_cast<float *>(at(ws, F.sc));
+    float *pmax = reinterpret_cast<float *>(at(ws, F.pmax));
+    int e = 0;
+    if (!p->reuse) {
+        if (dX)
+            e = note_hip(launch_fp8_quant(bd.w, COMERA_F32, p->N_in, p->N_out, pmax, codes(ws, F.w8), F.nout_p,
+                                          nullptr, 0, sc + kScW, nullptr, nullptr, nullptr, nullptr, stream),
+                         "FP8 codes of W");
+        if (!e && want_grad)
+            e = note_hip(launch_fp8_quant(X, p->s.act, b, p->N_in, pmax, nullptr, 0, codes(ws, F.x8t), F.b_p,
+                                          sc + kScX, nullptr, nullptr, nullptr, nullptr, stream),
+                         "FP8 codes of X");
+    }
+    if (!e)
+        e = note_hip(launch_fp8_quant(dY, p->s.act, b, p->N_out, pmax, dX ? codes(ws, F.dy8) : nullptr, F.nout_p,
+                                      want_grad ? codes(ws, F.dy8t) : nullptr, F.b_p, sc + kScDY,
+                                      dX ? sc + kScW : nullptr, sc + kScDX, want_grad ? sc + kScX : nullptr,
+                                      sc + kScDW, stream),
+                     "FP8 codes of dY");
+    if (e || !dX) return e;
+    void *ev;
+    timing_begin(p, COMERA_KERNEL_DX, stream, &ev);
+    GemmArgs g;
+    g.dtype = kDtypeFp8;
+    g.a_kc = true;
+    g.b_kc = true;
+    g.out_bf16 = p->s.act == COMERA_BF16;
+    g.A = codes(ws, F.dy8);
+    g.B = codes(ws, F.w8);
+    g.C = dX;
+    g.M = b;
+    g.N = p->N_in;
+    g.K = F.nout_p;
+    g.lda = F.nout_p;
+    g.ldb = F.nout_p;
+    g.rmap = remap_linear(p->N_in);
+    g.cmap = remap_linear(1);
+    g.oscale = sc + kScDX;
+    e = note_hip(launch_gemm(g, stream), "dX GEMM (FP8)");
+    timing_end(p, COMERA_KERNEL_DX, stream, ev);
+    return e;
+}
 
 comera_status backward_impl(comera_ttm_plan_t p, int64_t b, const void *X, const void *dY, const float *const *G,
                             const float *const *D, void *dX, float *const *dG, float *const *dD, void *ws,
@@ -467,11 +563,15 @@ comera_status backward_impl(comera_ttm_plan_t p, int64_t b, const void *X, const
     DenseBuild bd;
     int e = 0;
     if (p->reuse)
-        built_dense(p, ws, bd, kWantWT | kWantW);
+        built_dense(p, ws, bd, p->fp8 ? kWantW : kWantWT | kWantW);
     else
         e = build_dense(p, G, D, ws, stream, bd, kWantW);
     if (e) return COMERA_ERR_HIP;
-    if (dX) {
+    if (p->fp8) {
+        e = fp8_backward(p, b, X, dY, bd, dX, want_grad, ws, stream);
+        if (e) return COMERA_ERR_HIP;
+    }
+    if (dX && !p->fp8) {
         // dX[b, N_in] = dY[b, N_out] W^T  (eq. back X)
         void *ev;
         timing_begin(p, COMERA_KERNEL_DX, stream, &ev);
@@ -510,13 +610,20 @@ comera_status backward_impl(comera_ttm_plan_t p, int64_t b, const void *X, const
         if (e) return COMERA_ERR_HIP;
     }
     if (!want_grad) return COMERA_OK;
-    // dW = X^T dY (split over tokens, fixed-order split sums)
+    // dW = X^T dY (split over tokens, fixed-order split sums); FP8: on the
+    // transposed codes, K padded to whole 128-token tiles with zero codes
     float *dwp = nullptr;
     int splits = 0;
     {
         void *ev;
         timing_begin(p, COMERA_KERNEL_DW, stream, &ev);
-        e = dw_gemm(p, X, p->N_in, dY, p->N_out, b, ws, &dwp, &splits, stream);
+        if (p->fp8) {
+            const Fp8Layout &F = p->f8;
+            e = dw_gemm(p, codes(ws, F.x8t), F.b_p, codes(ws, F.dy8t), F.b_p, (b + 127) / 128 * 128, ws, &dwp,
+                        &splits, stream, reinterpret_cast<const float *>(at(ws, F.sc)) + kScDW);
+        } else {
+            e = dw_gemm(p, X, p->N_in, dY, p->N_out, b, ws, &dwp, &splits, stream);
+        }
         timing_end(p, COMERA_KERNEL_DW, stream, ev);
         if (e) return COMERA_ERR_HIP;
     }

@@ -1,0 +1,175 @@
+// FP8 (OCP E4M3) operands for the batch products of the mixed-precision
+// layer (the contractions with the batch dimension run in FP8, the batch-free
+// core contractions in fp32).  Per tensor: a power-of-two scale s = 2^e, e
+// the largest integer with amax * s <= 448, clamped to [-60, 60] (s = 1 for
+// amax == 0), then x * s rounded to E4M3 (nearest, ties to the even code,
+// saturating at 448).  x * s is exact in fp32, so the codes depend only on
+// the fp32 values; the clamp keeps s and 1 / (s s') finite and nonzero in
+// fp32.
+//
+//   amax_partial_kernel   max |x| per workgroup (no atomics, no clearing)
+//   quant_kernel          max of the partials -> s; codes of x (row-major,
+//                         rows padded with zero codes to ldq) and / or of
+//                         x^T (rows padded with zero codes to ldt); workgroup
+//                         0 also writes s and the products 1 / (s * s_partner)
+//                         that scale GEMM results
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+
+#include "internal.h"
+
+namespace comera {
+namespace {
+
+constexpr int kAmaxBlocks = 512;   // partial maxima per tensor
+static_assert(kAmaxBlocks * sizeof(float) <= COMERA_FP8_QUANTIZE_WS_BYTES, "scratch of comera_fp8_quantize");
+
+__device__ __forceinline__ float load_act(const void *x, int dtype, int64_t i) {
+    if (dtype == COMERA_BF16) return __uint_as_float(uint32_t(reinterpret_cast<const uint16_t *>(x)[i]) << 16);
+    return reinterpret_cast<const float *>(x)[i];
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+__global__ __launch_bounds__(256) void amax_partial_kernel(const void *__restrict__ x, int dtype, int64_t n,
+                                                           float *__restrict__ pmax) {
+    __shared__ float red[4];
+    float m = 0.f;
+    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256)
+        m = fmaxf(m, fabsf(load_act(x, dtype, i)));
+    m = wave_max(m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) pmax[blockIdx.x] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+// largest power of two s with amax * s <= 448 (448 = 0.875 * 2^9), the
+// exponent clamped to [-60, 60]; 1 for amax == 0
+__device__ __forceinline__ float pow2_scale(float amax) {
+    if (!(amax > 0.f) || !isfinite(amax)) return 1.f;
+    int k;
+    const float f = frexpf(amax, &k);
+    int e = f <= 0.875f ? 9 - k : 8 - k;
+    e = max(-60, min(e, 60));
+    return ldexpf(1.f, e);
+}
+
+// E4M3 code of v (|v| <= 448 expected; larger magnitudes saturate)
+__device__ __forceinline__ uint8_t e4m3_rne(float v) {
+    const uint32_t u = __float_as_uint(v);
+    const uint32_t sign = (u >> 24) & 0x80u;
+    const float a = fabsf(v);
+    uint32_t code;
+    if (!(a >= 0.015625f)) {                       // below 2^-6: subnormal steps of 2^-9 (exact scaling)
+        code = uint32_t(rintf(a * 512.f));          // 0 .. 8 (8 is the smallest normal, code 0x08)
+    } else {
+        const uint32_t ua = __float_as_uint(a);
+        int E = int((ua >> 23) & 0xFFu) - 127;
+        const uint32_t frac = ua & 0x7FFFFFu;
+        uint32_t m = frac >> 20;
+        const uint32_t rem = frac & 0xFFFFFu;
+        if (rem > 0x80000u || (rem == 0x80000u && (m & 1u))) ++m;
+        if (m == 8u) {
+            m = 0u;
+            ++E;
+        }
+        const int eb = E + 7;
+        code = (eb > 15 || (eb == 15 && m == 7u)) ? 0x7Eu : (uint32_t(eb) << 3) | m;
+    }
+    return uint8_t(code | sign);
+}
+
+// Tiles of 64 rows x 64 columns over x [R][C]: q[r][c] for c < ldq (if q;
+// zero codes for c >= C) and qt[c][r] for r < ldt (if qt; zero codes for
+// r >= R).  The grid covers ceil(R' / 64) x ceil(C' / 64) tiles with
+// R' = max(R, ldt if qt), C' = max(C, ldq if q).
+__global__ __launch_bounds__(256) void quant_kernel(const void *__restrict__ x, int dtype, int64_t R, int64_t C,
+                                                    const float *__restrict__ pmax, int nb, uint8_t *__restrict__ q,
+                                                    int64_t ldq, uint8_t *__restrict__ qt, int64_t ldt,
+                                                    float *__restrict__ s_out, const float *pa, float *oa,
+                                                    const float *pb, float *ob) {
+    __shared__ float red[4];
+    __shared__ uint8_t tile[64][65];
+    const int tid = threadIdx.x;
+    float m = 0.f;
+    for (int i = tid; i < nb; i += 256) m = fmaxf(m, pmax[i]);
+    m = wave_max(m);
+    if ((tid & 63) == 0) red[tid >> 6] = m;
+    __syncthreads();
+    const float s = pow2_scale(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])));
+    if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) {
+        if (s_out) s_out[0] = s;
+        if (pa && oa) *oa = 1.f / (s * *pa);
+        if (pb && ob) *ob = 1.f / (s * *pb);
+    }
+    const int64_t r0 = int64_t(blockIdx.x) * 64, c0 = int64_t(blockIdx.y) * 64;
+    // thread t: column t % 64 of rows t / 64 + 4 i
+    const int cc = tid & 63, rr0 = tid >> 6;
+#pragma unroll 4
+    for (int i = 0; i < 16; ++i) {
+        const int rr = rr0 + 4 * i;
+        const int64_t r = r0 + rr, c = c0 + cc;
+        const bool ok = r < R && c < C;
+        const float v = load_act(x, dtype, ok ? r * C + c : 0);
+        const uint8_t code = ok ? e4m3_rne(v * s) : uint8_t(0);
+        tile[rr][cc] = code;
+        if (q && r < R && c < ldq) q[r * ldq + c] = code;
+    }
+    if (!qt) return;
+    __syncthreads();
+    // transposed: row c of qt holds the codes of rows r0 .. r0 + 63
+#pragma unroll 4
+    for (int i = 0; i < 16; ++i) {
+        const int ccl = rr0 + 4 * i;        // column within the tile = row of qt
+        const int rrl = cc;                 // row within the tile = column of qt
+        const int64_t c = c0 + ccl, r = r0 + rrl;
+        if (c < C && r < ldt) qt[c * ldt + r] = tile[rrl][ccl];
+    }
+}
+
+}  // namespace
+
+int fp8_amax_blocks() { return kAmaxBlocks; }
+
+int launch_fp8_quant(const void *x, int dtype, int64_t R, int64_t C, float *pmax, uint8_t *q, int64_t ldq,
+                     uint8_t *qt, int64_t ldt, float *s_out, const float *pa, float *oa, const float *pb, float *ob,
+                     void *stream) {
+    if (R <= 0 || C <= 0) return 0;
+    if ((q && ldq < C) || (qt && ldt < R)) return int(hipErrorInvalidValue);
+    const int64_t n = R * C;
+    const int nb = int(std::min<int64_t>(kAmaxBlocks, (n + 255) / 256));
+    hipLaunchKernelGGL(amax_partial_kernel, dim3(nb), dim3(256), 0, hipStream_t(stream), x, dtype, n, pmax);
+    if (int e = int(hipGetLastError())) return e;
+    const int64_t rows = qt ? std::max<int64_t>(R, ldt) : R;
+    const int64_t cols = q ? std::max<int64_t>(C, ldq) : C;
+    const int64_t gx = (rows + 63) / 64, gy = (cols + 63) / 64;
+    if (gx > 2147483647 || gy > 65535) return int(hipErrorInvalidValue);
+    hipLaunchKernelGGL(quant_kernel, dim3(unsigned(gx), unsigned(gy)), dim3(256), 0, hipStream_t(stream), x, dtype, R,
+                       C, pmax, nb, q, ldq, qt, ldt, s_out, pa, oa, pb, ob);
+    return int(hipGetLastError());
+}
+
+}  // namespace comera
+
+extern "C" {
+
+comera_status comera_fp8_quantize(const void *x, int32_t dtype, int64_t rows, int64_t cols, uint8_t *q, int64_t ldq,
+                                  uint8_t *qt, int64_t ldt, float *scale, void *ws, size_t ws_bytes, void *stream) {
+    if (rows < 0 || cols < 0 || (dtype != COMERA_F32 && dtype != COMERA_BF16)) return COMERA_ERR_INVALID_ARG;
+    if (rows == 0 || cols == 0) return COMERA_OK;
+    if (!x || !scale || (!q && !qt)) return COMERA_ERR_INVALID_ARG;
+    if ((q && ldq < cols) || (qt && ldt < rows)) return COMERA_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < size_t(COMERA_FP8_QUANTIZE_WS_BYTES)) return COMERA_ERR_WORKSPACE;
+    const int64_t tr = qt ? std::max(rows, ldt) : rows, tc = q ? std::max(cols, ldq) : cols;
+    if ((tr + 63) / 64 > 2147483647 || (tc + 63) / 64 > 65535) return COMERA_ERR_UNSUPPORTED;
+    const int e = comera::launch_fp8_quant(x, dtype, rows, cols, reinterpret_cast<float *>(ws), q, ldq, qt, ldt, scale,
+                                           nullptr, nullptr, nullptr, nullptr, stream);
+    return comera::note_hip(e, "FP8 quantisation") ? COMERA_ERR_HIP : COMERA_OK;
+}
+
+}  // extern "C"

@@ -54,6 +54,12 @@ struct GemmCfg<float> {
     static constexpr int KT = 16;
     static constexpr int E = 4;
 };
+// FP8 (OCP E4M3) operands: fast kernel only
+template <>
+struct GemmCfg<uint8_t> {
+    static constexpr int KT = 64;
+    static constexpr int E = 16;
+};
 
 template <typename T>
 __device__ __forceinline__ uint4 pack_elems(const T (&v)[GemmCfg<T>::E]) {
@@ -174,6 +180,7 @@ struct GemmParams {
     int vec_a, vec_b;
     int gw;   // tile-order group width in column tiles (see tile_of)
     uint32_t tx, ty;   // column tiles, row tiles (the grid is one-dimensional)
+    const float *oscale;   // device scalar multiplying every result, or null
 };
 
 // Workgroup -> (split, row tile, column tile).  The dispatcher deals
@@ -341,6 +348,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
 // LDS bank conflicts on gfx950, 64-byte rows are kept for the operands
 // transposed on the way in, where they load faster.
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 // KTB = bytes of K per LDS row (64 or 128), FP = KTB + 16 = LDS row pitch;
@@ -482,7 +490,35 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
         }
         const char *a_s = (cur ? sA1 : sA0) + aoff;
         const char *b_s = (cur ? sB1 : sB0) + boff;
-        if constexpr (sizeof(T) == 2) {
+        if constexpr (sizeof(T) == 1) {
+            // FP8 E4M3 x E4M3 (v_mfma_scale_f32_32x32x64_f8f6f4, unit block
+            // scales 127 = 2^0): of each 64-byte k step, lane (lr, lh) supplies
+            // bytes 16 lh .. 16 lh + 15 and 32 + 16 lh .. 32 + 16 lh + 15 of its
+            // row (a_s, b_s already point 16 lh bytes in), the same k slots for
+            // A and B
+#pragma unroll
+            for (int ks = 0; ks < KT / 64; ++ks) {
+                i32x8 av[TM], bv[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    const u32x4 lo = *reinterpret_cast<const u32x4 *>(a_s + i * 32 * FP + ks * 64);
+                    const u32x4 hi = *reinterpret_cast<const u32x4 *>(a_s + i * 32 * FP + ks * 64 + 32);
+                    av[i] = i32x8{int(lo.x), int(lo.y), int(lo.z), int(lo.w), int(hi.x), int(hi.y), int(hi.z), int(hi.w)};
+                }
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    const u32x4 lo = *reinterpret_cast<const u32x4 *>(b_s + j * 32 * FP + ks * 64);
+                    const u32x4 hi = *reinterpret_cast<const u32x4 *>(b_s + j * 32 * FP + ks * 64 + 32);
+                    bv[j] = i32x8{int(lo.x), int(lo.y), int(lo.z), int(lo.w), int(hi.x), int(hi.y), int(hi.z), int(hi.w)};
+                }
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[i], bv[j], acc[i][j], 0, 0, 0,
+                                                                                    127, 0, 127);
+            }
+        } else if constexpr (sizeof(T) == 2) {
 #pragma unroll
             for (int ks = 0; ks < KT / 16; ++ks) {
                 bf16x8 av[TM], bv[TN];
@@ -518,6 +554,15 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
             lb.store(cur ? sB0 : sB1, tid);
         }
         __syncthreads();
+    }
+    if (p.oscale) {
+        const float sc = *p.oscale;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[i][j][v] *= sc;
     }
     epilogue<OUT_BF16, TM, TN, WM, WN>(p, acc, roff, coff, wm, wn, lr, lh);
 }
@@ -626,7 +671,7 @@ int launch_fast(const GemmArgs &g, const GemmParams &p, int id, void *stream) {
         case F128x128_64: return go_fast<T, AK, BK, OB, 128, 128, 64, 64, 64>(g, p, stream);
         case F256x128_64: return go_fast<T, AK, BK, OB, 256, 128, 128, 64, 64>(g, p, stream);
     }
-    if constexpr (sizeof(T) == 2) {
+    if constexpr (sizeof(T) <= 2) {
         switch (id) {
             case F256x256_128w8: return go_fast<T, AK, BK, OB, 256, 256, 128, 64, 128, 512>(g, p, stream);
             case F256x128_128w8: return go_fast<T, AK, BK, OB, 256, 128, 64, 64, 128, 512>(g, p, stream);
@@ -645,7 +690,8 @@ int pick_fast(const GemmArgs &g, int splits) {
     // bf16: 256 x 256 tiles of eight waves once they give two or more
     // workgroups per CU (transposed operands, split over K: half a wave of
     // workgroups is enough)
-    if (g.dtype == COMERA_BF16 && g.a_kc == g.b_kc && t256 >= (g.a_kc ? 512 : 128)) return F256x256_128w8;
+    if ((g.dtype == COMERA_BF16 || g.dtype == kDtypeFp8) && g.a_kc == g.b_kc && t256 >= (g.a_kc ? 512 : 128))
+        return F256x256_128w8;
     if (g.a_kc && g.b_kc) {
         // fp32 tiles of 128 x 128 fit three workgroups per CU with 64-byte rows
         if (g.dtype == COMERA_F32 && t128 >= 240) return F128x128_64;
@@ -665,7 +711,7 @@ int pick_fast(const GemmArgs &g, int splits) {
 // 16-byte aligned rows, whole K tiles in every split, row groups that divide
 // the row count of transposed operands, and byte offsets within 32 bits.
 bool fast_ok(const GemmArgs &g, int64_t kchunk, int ktb) {
-    const int64_t sz = g.dtype == COMERA_BF16 ? 2 : 4;
+    const int64_t sz = g.dtype == COMERA_BF16 ? 2 : (g.dtype == kDtypeFp8 ? 1 : 4);
     const int64_t kt = ktb / sz;
     if (g.K % kt || kchunk % kt) return false;
     auto op_ok = [&](const void *ptr, int64_t ld, bool kc, int64_t R) {
@@ -695,7 +741,7 @@ Remap remap_linear(int64_t stride) {
 
 int launch_gemm(const GemmArgs &g, void *stream) {
     if (g.M <= 0 || g.N <= 0) return 0;
-    if (g.splits <= 1 && g.scratch && g.out_elems > 0) {
+    if (g.splits <= 1 && g.scratch && g.out_elems > 0 && g.dtype != kDtypeFp8) {
         int s = gemm_auto_splits(g.M, g.N, g.K);
         while (s > 1 && int64_t(s) * g.out_elems > g.scratch_elems) --s;
         if (s > 1) {
@@ -725,13 +771,15 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     p.split_stride = g.split_stride;
     p.rmap = g.rmap;
     p.cmap = g.cmap;
-    const int E = g.dtype == COMERA_BF16 ? 8 : 4;
+    const int esz = g.dtype == COMERA_BF16 ? 2 : (g.dtype == kDtypeFp8 ? 1 : 4);
+    const int E = 16 / esz;
     auto aligned = [&](const void *ptr, int64_t ld) {
         return (reinterpret_cast<uintptr_t>(ptr) % 16 == 0) && (ld % E == 0);
     };
     p.vec_a = aligned(g.A, g.lda);
     p.vec_b = aligned(g.B, g.ldb);
     p.gw = 0;
+    p.oscale = g.oscale;
     GemmArgs gg = g;
     if (gg.splits < 1) gg.splits = 1;
     // fast path: K chunk rounded up to whole K tiles (later splits may get
@@ -740,8 +788,8 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     GemmParams pf = p;
     if (fast >= 0) {
         const int ktb = (fast == F128x128_64 || fast == F256x128_64) ? 64 : 128;
-        if (fast >= F256x256_128w8 && g.dtype != COMERA_BF16) fast = -1;
-        const int64_t kt = ktb / (g.dtype == COMERA_BF16 ? 2 : 4);
+        if (fast >= F256x256_128w8 && g.dtype == COMERA_F32) fast = -1;
+        const int64_t kt = ktb / esz;
         pf.kchunk = ceil_div(p.kchunk, kt) * kt;
         if (!fast_ok(gg, pf.kchunk, ktb)) fast = -1;
     }
@@ -750,6 +798,19 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     if (g.a_kc == AK && g.b_kc == BK && g.out_bf16 == OB) {                                \
         if (fast >= 0) return launch_fast<T, AK, BK, OB>(gg, pf, fast, stream);           \
         return launch_t<T, AK, BK, OB>(gg, p, tile, stream);                               \
+    }
+    if (g.dtype == kDtypeFp8) {
+        // FP8 operands: K-contiguous fast tiles only (the caller pads K);
+        // products too small for the measured choice take the smallest tile
+        if (!g.a_kc || !g.b_kc) return int(hipErrorInvalidValue);
+        if (fast < 0 && g.fast == -1) {
+            fast = g.M <= 64 ? F64x128_128 : (g.N <= 64 ? F128x64_128 : F128x128_128);
+            pf.kchunk = ceil_div(p.kchunk, 128) * 128;
+            if (!fast_ok(gg, pf.kchunk, 128)) fast = -1;
+        }
+        if (fast < 0) return int(hipErrorInvalidValue);
+        if (g.out_bf16) return launch_fast<uint8_t, true, true, true>(gg, pf, fast, stream);
+        return launch_fast<uint8_t, true, true, false>(gg, pf, fast, stream);
     }
     if (g.dtype == COMERA_BF16) {
         COMERA_GEMM_CASE(uint16_t, true, false, true)

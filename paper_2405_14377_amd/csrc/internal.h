@@ -68,6 +68,23 @@ struct DenseLayout {
     int e_slices[kMaxCores + 1];
 };
 
+// FP8 mixed precision of the dense order: W is built in fp32 (region
+// DenseLayout::w) and the three batch products read E4M3 codes.  K of every
+// product is padded with zero codes to a multiple of 128 (N_in_p, N_out_p,
+// b_p for the planned batch).
+struct Fp8Layout {
+    int64_t nin_p, nout_p, b_p;
+    size_t w8;      // W codes [N_in][N_out_p]      (B of dX = dY W^T)
+    size_t w8t;     // W^T codes [N_out][N_in_p]    (B of Y = X W)
+    size_t x8;      // X codes [b][N_in_p]          (A of Y)
+    size_t x8t;     // X^T codes [N_in][b_p]        (A of dW = X^T dY)
+    size_t dy8;     // dY codes [b][N_out_p]        (A of dX)
+    size_t dy8t;    // dY^T codes [N_out][b_p]      (B of dW)
+    size_t pmax;    // partial maxima of the tensor being quantised
+    size_t sc;      // scales: kScW, kScX, kScDY, then the GEMM output factors kScFwd, kScDX, kScDW
+};
+constexpr int kScW = 0, kScX = 1, kScDY = 2, kScFwd = 3, kScDX = 4, kScDW = 5;
+
 // Sweep orders (groups of consecutive cores, activations swept through the
 // groups in sequence).  Each group g (cores s[g] .. e[g]) is treated as a
 // layer of its own whose outer bonds are folded into its outer factors:
@@ -125,6 +142,8 @@ struct comera_ttm_plan_s {
     std::unique_ptr<comera_ttm_plan_s> sub[comera::kMaxCores];   // one layer per sweep group
     size_t ws_bytes = 0;
     bool reuse = false;                           // backward reuses the forward's build
+    bool fp8 = false;                             // batch products on E4M3 codes (dense order)
+    comera::Fp8Layout f8{};
     comera::KernelTiming timing;
 };
 
@@ -198,6 +217,17 @@ struct MaskGradArgs {
 };
 int launch_mask_grad(const MaskGradArgs &a, void *stream);
 
+// FP8 operands (fp8.hip): x [R][C] (fp32 or bf16 by dtype) -> per-tensor
+// power-of-two scale s (written to s_out[0]), E4M3 codes q [R][ldq] (columns
+// C .. ldq-1 zero) and / or qt [C][ldt] (x^T, columns R .. ldt-1 zero), and
+// 1 / (s * *pa) -> *oa, 1 / (s * *pb) -> *ob for the GEMMs that consume the
+// codes (any of q, qt, pa / oa, pb / ob may be null).  pmax:
+// fp8_amax_blocks() floats of scratch.
+int fp8_amax_blocks();
+int launch_fp8_quant(const void *x, int dtype, int64_t R, int64_t C, float *pmax, uint8_t *q, int64_t ldq,
+                     uint8_t *qt, int64_t ldt, float *s_out, const float *pa, float *oa, const float *pb, float *ob,
+                     void *stream);
+
 // Output index remap of a GEMM: write idx in mixed radix (digit 0 most
 // significant and unbounded, digit t < nd has radix radix[t] for t >= 1) and
 // return sum_t digit_t * stride[t].
@@ -252,8 +282,11 @@ bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, int &QI, int &Q
 int launch_wbuild(const WBuildArgs &a, void *stream);
 
 
+// operand type code of FP8 (OCP E4M3) GEMM operands, beside COMERA_F32 / COMERA_BF16
+constexpr int kDtypeFp8 = 2;
+
 struct GemmArgs {
-    int dtype = COMERA_F32;          // operand type
+    int dtype = COMERA_F32;          // operand type (COMERA_F32, COMERA_BF16 or kDtypeFp8)
     bool a_kc = true, b_kc = true;   // k contiguous in memory for A / B
     bool out_bf16 = false;
     const void *A = nullptr, *B = nullptr;
@@ -272,6 +305,7 @@ struct GemmArgs {
     float *scratch = nullptr;
     int64_t scratch_elems = 0;
     int64_t out_elems = 0;
+    const float *oscale = nullptr;   // device scalar multiplying every result (fast path), or null
 };
 // C[rmap(m) + cmap(n)] = sum_k Aop(m, k) Bop(k, n); see gemm.hip.
 int launch_gemm(const GemmArgs &g, void *stream);
@@ -373,9 +407,11 @@ int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, int want,
 void built_dense(const comera_ttm_plan_s *p, void *ws, DenseBuild &bd, int want);
 // dW = A^T B (A [K][N_in] with leading dimension lda, B [K][N_out] with ldb),
 // split over K, written blocked for the projections; *dwp, *splits describe
-// the split partials
+// the split partials.  With oscale (FP8 codes): A [N_in][lda] and B
+// [N_out][ldb] hold the transposed operands, K a multiple of 128, and every
+// result is multiplied by *oscale.
 int dw_gemm(const comera_ttm_plan_s *sp, const void *A, int64_t lda, const void *B, int64_t ldb, int64_t K,
-            void *ws, float **dwp, int *splits, void *stream);
+            void *ws, float **dwp, int *splits, void *stream, const float *oscale = nullptr);
 // core gradients (compacted, as split partials part[k] x nsplit[k]) from the
 // partials of dW; want[k] false skips core k
 int project_cores(const comera_ttm_plan_s *sp, const DenseBuild &bd, const float *dwp, int splits,

@@ -181,11 +181,40 @@ bool validate(const comera_ttm_shape *s, int64_t batch) {
 
 }  // namespace
 
+namespace {
+
+// regions of the FP8 codes, scales and partial maxima from offset off
+size_t layout_fp8(comera_ttm_plan_s *p, size_t off) {
+    Fp8Layout &F = p->f8;
+    auto r128 = [](int64_t v) { return (std::max<int64_t>(v, 1) + 127) / 128 * 128; };
+    F.nin_p = r128(p->N_in);
+    F.nout_p = r128(p->N_out);
+    F.b_p = r128(p->batch);
+    const int64_t b = std::max<int64_t>(p->batch, 1);
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = align_up(off + bytes);
+        return at;
+    };
+    F.w8 = take(size_t(p->N_in * F.nout_p));
+    F.w8t = take(size_t(p->N_out * F.nin_p));
+    F.x8 = take(size_t(b * F.nin_p));
+    F.x8t = take(size_t(p->N_in * F.b_p));
+    F.dy8 = take(size_t(b * F.nout_p));
+    F.dy8t = take(size_t(p->N_out * F.b_p));
+    F.pmax = take(sizeof(float) * size_t(fp8_amax_blocks()));
+    F.sc = take(sizeof(float) * 8);
+    return off;
+}
+
+}  // namespace
+
 void layout_dense(comera_ttm_plan_s *p, bool with_dx) {
     DenseLayout &L = p->dense;
     std::memset(&L, 0, sizeof(L));
     const int d = p->d;
-    const size_t esz = p->s.act == COMERA_BF16 ? 2 : 4;
+    // FP8: W is built in fp32 and W^T is never formed in the activation dtype
+    const size_t esz = (p->s.act == COMERA_BF16 && !p->fp8) ? 2 : 4;
     size_t off = 0;
     for (int k = 0; k < d; ++k) {
         L.gc[k] = off;
@@ -201,7 +230,7 @@ void layout_dense(comera_ttm_plan_s *p, bool with_dx) {
     L.w = off;
     off = align_up(off + esz * size_t(p->N_in * p->N_out));
     L.wt = off;
-    off = align_up(off + esz * size_t(p->N_in * p->N_out));
+    if (!p->fp8) off = align_up(off + esz * size_t(p->N_in * p->N_out));
     L.ones = off;
     off = align_up(off + sizeof(float));
     // dW = X^T dY split over tokens so that the grid holds >= ~512 workgroups
@@ -213,7 +242,7 @@ void layout_dense(comera_ttm_plan_s *p, bool with_dx) {
     // bf16 (256 x 256 tiles): the split count minimising a measured model,
     // waves of tiles x tokens per split x 40 ns plus writing and reading
     // back the split partials at 4 TB/s
-    if (p->s.act == COMERA_BF16 && p->N_in >= 256 && p->N_out >= 256) {
+    if ((p->s.act == COMERA_BF16 || p->fp8) && p->N_in >= 256 && p->N_out >= 256) {
         const int64_t t256 = ((p->N_in + 255) / 256) * ((p->N_out + 255) / 256);
         double best = -1.0;
         for (int64_t s = 1; s <= 64; ++s) {
@@ -232,6 +261,7 @@ void layout_dense(comera_ttm_plan_s *p, bool with_dx) {
     splits = std::min<int64_t>(splits, 64);
     int64_t kchunk = (b + splits - 1) / splits;
     kchunk = (kchunk + 31) / 32 * 32;
+    if (p->fp8) kchunk = (kchunk + 127) / 128 * 128;   // whole 128-token K tiles of codes
     splits = (b + kchunk - 1) / kchunk;
     L.dw_splits = int(splits);
     L.dw_kchunk = kchunk;
@@ -239,7 +269,7 @@ void layout_dense(comera_ttm_plan_s *p, bool with_dx) {
     // 128 x 128 tiles (the partials are summed in a fixed order)
     L.dx_splits = 1;
     L.dx_kchunk = p->N_out;
-    if (with_dx && p->s.act == COMERA_F32) {
+    if (with_dx && p->s.act == COMERA_F32 && !p->fp8) {
         const int64_t xt = ((b + 127) / 128) * ((p->N_in + 127) / 128);
         int64_t sx = std::max<int64_t>(1, (768 + xt / 2) / xt);
         sx = std::min<int64_t>(std::min<int64_t>(sx, 8), std::max<int64_t>(1, p->N_out / 512));
@@ -252,8 +282,9 @@ void layout_dense(comera_ttm_plan_s *p, bool with_dx) {
             off = align_up(off + sizeof(float) * size_t(L.dx_splits) * size_t(b) * size_t(p->N_in));
         }
     }
+    if (p->fp8) off = layout_fp8(p, off);
     // forward and dX products with too few output tiles are split over K
-    if (with_dx) {
+    if (with_dx && !p->fp8) {
         const int sf = gemm_auto_splits(b, p->N_out, p->N_in);
         const int sx = L.dx_splits > 1 ? 1 : gemm_auto_splits(b, p->N_in, p->N_out);
         const int64_t pe = std::max<int64_t>(sf > 1 ? sf * b * p->N_out : 0, sx > 1 ? sx * b * p->N_in : 0);
@@ -646,6 +677,30 @@ comera_status comera_ttm_plan_order_info(comera_ttm_plan_t p, int32_t i, char *d
 }
 
 size_t comera_ttm_workspace_bytes(comera_ttm_plan_t p) { return p ? p->ws_bytes : 0; }
+
+comera_status comera_ttm_plan_set_fp8(comera_ttm_plan_t p, int32_t enable) {
+    if (!p) return COMERA_ERR_INVALID_ARG;
+    const bool on = enable != 0;
+    if (on == p->fp8) return COMERA_OK;
+    if (p->zero) {
+        // W == 0: nothing is multiplied, the workspace stays empty
+        p->fp8 = on;
+        return COMERA_OK;
+    }
+    if (p->orders[p->chosen].kind != COMERA_ORDER_DENSE) return COMERA_ERR_UNSUPPORTED;
+    // every code buffer is addressed with 32-bit offsets by the GEMM
+    const int64_t b = std::max<int64_t>(p->batch, 1);
+    const int64_t nin_p = (p->N_in + 127) / 128 * 128, nout_p = (p->N_out + 127) / 128 * 128;
+    const int64_t b_p = (b + 127) / 128 * 128;
+    const int64_t lim = int64_t(1) << 32;
+    if (b * nin_p >= lim || b * nout_p >= lim || p->N_in * b_p >= lim || p->N_out * b_p >= lim ||
+        p->N_in * nout_p >= lim || p->N_out * nin_p >= lim)
+        return COMERA_ERR_UNSUPPORTED;
+    p->fp8 = on;
+    layout_dense(p);
+    p->ws_bytes = p->dense.total;
+    return COMERA_OK;
+}
 
 void comera_ttm_plan_destroy(comera_ttm_plan_t p) {
     if (!p) return;

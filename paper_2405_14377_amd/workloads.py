@@ -200,3 +200,19 @@ def random_ttm_shape(rng: np.random.Generator, d: int, max_factor: int = 4, max_
 
 def random_cores(rng: np.random.Generator, shape: TTMLayerShape, scale: float = 1.0) -> List[np.ndarray]:
     return [(rng.standard_normal(cs) * scale).astype(np.float32) for cs in shape.core_shapes()]
+
+
+def integer_bond_diagonal_cores(rng: np.random.Generator, n, m, r) -> List[np.ndarray]:
+    """Cores with entries in {-1, 0, 1}, the inner ones diagonal in their bond
+    (G[a, :, :, c] = 0 for a != c).  Every entry of the dense weight is then a
+    sum of at most r_1 products of +-1: an integer of magnitude <= r_1, exact
+    in fp32 whatever the contraction order, and exactly representable in FP8
+    E4M3 after a power-of-two scaling while r_1 <= 16."""
+    d = len(n)
+    cores = []
+    for k in range(d):
+        G = rng.integers(-1, 2, (r[k], m[k], n[k], r[k + 1])).astype(np.float32)
+        if 0 < k < d - 1:
+            G *= np.eye(r[k], dtype=np.float32)[:, None, None, :]
+        cores.append(G)
+    return cores

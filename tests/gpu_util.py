@@ -40,7 +40,8 @@ def to_np(t) -> np.ndarray:
 class TTMRun:
     """Plan + device buffers for one TTM layer."""
 
-    def __init__(self, n, m, r, cores, masks, b, act="f32", mask_active=None, force_order=-1, reuse=False):
+    def __init__(self, n, m, r, cores, masks, b, act="f32", mask_active=None, force_order=-1, reuse=False,
+                 fp8=False):
         torch, dev = torch_dev()
         self.act = act
         self.b = b
@@ -48,6 +49,8 @@ class TTMRun:
                               force_order=force_order)
         if reuse:
             self.plan.set_reuse_forward(True)
+        if fp8:
+            self.plan.set_fp8(True)
         self.G = [to_dev(c) for c in cores]
         self.D = None if masks is None else [to_dev(mk) for mk in masks]
         self.ws = torch.empty(max(self.plan.workspace_bytes, 1), dtype=torch.uint8, device=dev)

@@ -194,3 +194,32 @@ def test_embed_workspace_and_errors():
     big = C.tt_embed_shape((4, 4), (4096, 64), (1, 64, 1))
     assert lib.comera_tt_embed_forward(big, fake, 4, C._ptr_array([fake, fake]), None, fake, fake, 1 << 40, None,
                                        None) == C.ERR_UNSUPPORTED
+
+
+def test_fp8_setting_and_quantize_errors():
+    lib = C.load()
+    assert lib.comera_ttm_plan_set_fp8(None, 1) == C.ERR_INVALID_ARG
+    # dense order: the workspace grows by the code buffers (K padded to 128)
+    p = C.TTMPlan((8, 8, 12), (16, 16, 12), (1, 30, 30, 1), act=C.BF16, batch=4096, force_order=0)
+    base = p.workspace_bytes
+    p.set_fp8(True)
+    codes = 768 * 3072 * 2 + 4096 * (768 + 3072) * 2
+    assert p.workspace_bytes >= base - 768 * 3072 * 2 * 2 + codes
+    p.set_fp8(False)
+    assert p.workspace_bytes == base
+    # a sweep order has no FP8 products
+    sw = C.TTMPlan((4, 6, 5), (3, 7, 4), (1, 6, 5, 1), batch=64, force_order=1)
+    assert lib.comera_ttm_plan_set_fp8(sw.handle, 1) == C.ERR_UNSUPPORTED
+    assert lib.comera_ttm_plan_set_fp8(sw.handle, 0) == C.OK
+    fake = 1 << 40
+    W = C.FP8_QUANTIZE_WS_BYTES
+    q = lib.comera_fp8_quantize
+    assert q(fake, 2, 4, 4, fake, 4, None, 0, fake, fake, W, None) == C.ERR_INVALID_ARG     # dtype
+    assert q(fake, 0, -1, 4, fake, 4, None, 0, fake, fake, W, None) == C.ERR_INVALID_ARG    # rows
+    assert q(fake, 0, 4, 4, None, 0, None, 0, fake, fake, W, None) == C.ERR_INVALID_ARG     # no output
+    assert q(fake, 0, 4, 4, fake, 3, None, 0, fake, fake, W, None) == C.ERR_INVALID_ARG     # ldq < cols
+    assert q(fake, 0, 4, 4, None, 0, fake, 2, fake, fake, W, None) == C.ERR_INVALID_ARG     # ldt < rows
+    assert q(fake, 0, 4, 4, fake, 4, None, 0, None, fake, W, None) == C.ERR_INVALID_ARG     # no scale
+    assert q(fake, 0, 4, 4, fake, 4, None, 0, fake, fake, W - 1, None) == C.ERR_WORKSPACE
+    assert q(None, 0, 0, 4, None, 0, None, 0, None, None, 0, None) == C.OK                  # empty
+    assert q(fake, 0, 4, 1 << 23, fake, 1 << 23, None, 0, fake, fake, W, None) == C.ERR_UNSUPPORTED

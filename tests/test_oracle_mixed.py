@@ -7,21 +7,14 @@ import pytest
 
 from oracle import fp8, mixed
 from oracle import ttm as OT
+from paper_2405_14377_amd import workloads as wl
 
 
 def _exact_layer(rng, n, m, r, masks_p=None):
-    """Cores with entries in {-1, 0, 1} whose inner cores are diagonal in
-    their bond (G[a, :, :, c] = 0 for a != c): every W entry is a sum of at
-    most r products of +-1, an integer of magnitude <= r, exactly
-    representable in E4M3 after any power-of-two scaling that keeps it <= 448
-    (integers up to 16 have at most four significant bits)."""
+    """Integer cores whose dense weight is exact and FP8-representable (see
+    workloads.integer_bond_diagonal_cores), optional 0/1 masks."""
     d = len(n)
-    cores = []
-    for k in range(d):
-        G = rng.integers(-1, 2, (r[k], m[k], n[k], r[k + 1])).astype(np.float64)
-        if 0 < k < d - 1:
-            G *= np.eye(r[k])[:, None, None, :]
-        cores.append(G)
+    cores = [G.astype(np.float64) for G in wl.integer_bond_diagonal_cores(rng, n, m, r)]
     masks = None
     if masks_p is not None:
         masks = [(rng.random(r[k + 1]) < masks_p).astype(np.float64) for k in range(d - 1)]
