@@ -59,16 +59,18 @@ def layer_inputs(wid, li, act, gen_seed):
 
 
 class Layer:
-    def __init__(self, sh, X, dY, G, D, mask_active, b, act, force_order=-1):
+    def __init__(self, sh, X, dY, G, D, mask_active, b, act, force_order=-1, fp8=False):
         import torch
         from paper_2405_14377_amd import comera as C
         self.C = C
         self.sh, self.X, self.dY, self.G, self.D, self.b, self.act = sh, X, dY, G, D, b, act
         self.plan = C.TTMPlan(sh.n, sh.m, sh.r, C.BF16 if act == "bf16" else C.F32, batch=b,
-                              mask_active=mask_active, force_order=force_order)
+                              mask_active=mask_active, force_order=0 if fp8 else force_order)
         # a training step: the backward follows the forward on the same
         # workspace and cores, so it takes the forward's W and core copies
         self.plan.set_reuse_forward(True)
+        if fp8:
+            self.plan.set_fp8(True)
         dev = X.device
         self.ws = torch.empty(self.plan.workspace_bytes, dtype=torch.uint8, device=dev)
         self.Y = torch.empty((b, sh.n_out), dtype=X.dtype, device=dev)
@@ -386,6 +388,92 @@ def other_workloads(steps, warmup):
     return res
 
 
+def dense_fp8_step_fn(sh, X, dY):
+    """The three dense products on FP8 E4M3 operands with per-tensor scales
+    (torch._scaled_mm, bf16 out), operands quantised inside the step as the
+    mixed-precision layer does; None with the reason if torch cannot run it."""
+    import torch
+    dev = X.device
+    f8 = torch.float8_e4m3fn
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    W = torch.randn((sh.n_in, sh.n_out), generator=g, device=dev) / sh.n_in ** 0.5
+
+    def q(t):
+        s = 448.0 / t.abs().amax().float().clamp(min=1e-30)
+        return (t.float() * s).to(f8), (1.0 / s).reshape(())
+
+    def fn():
+        x8, sx = q(X)
+        w8t, sw = q(W.t())               # [N_out, N_in]: column-major B below
+        d8, sd = q(dY)
+        torch._scaled_mm(x8, w8t.t(), scale_a=sx, scale_b=sw, out_dtype=torch.bfloat16)
+        w8, _ = q(W)
+        torch._scaled_mm(d8, w8.t(), scale_a=sd, scale_b=sw, out_dtype=torch.bfloat16)
+        xt8, _ = q(X.t().contiguous())
+        dt8, _ = q(dY.t().contiguous())
+        torch._scaled_mm(xt8, dt8.t(), scale_a=sx, scale_b=sd, out_dtype=torch.float32)
+    try:
+        fn()
+        torch.cuda.synchronize()
+    except Exception as e:
+        return None, f"{type(e).__name__}: {e}"[:160]
+    return fn, None
+
+
+def fp8_workloads(steps, warmup):
+    """Mixed-precision layers (batch products on FP8 codes) beside the same
+    layers in bf16 (the planner's order) and the dense products in bf16 and
+    FP8, for the layer shapes of the large-batch workloads."""
+    import torch
+    from paper_2405_14377_amd import workloads as wl
+    res = {}
+    for wid in (1, 4, 6):
+        w = wl.WORKLOADS[wid]
+        for li in range(len(w.layers)):
+            sh, inp, X, dY, G, D, ma, b = layer_inputs(wid, li, "bf16", 1000 * wid + li)
+            k = steps if wid == 1 else max(3, steps // 4)
+            lay = Layer(sh, X, dY, G, D, ma, b, "bf16", fp8=True)
+            log(f"[fp8] {w.name} {sh.name}: {k} steps")
+            ms, _ = time_loop(lay.step, k, warmup)
+            C = lay.C
+            C.comera_ttm_plan_set_timing(lay.plan.handle, True)
+            for _ in range(max(2, k // 2)):
+                lay.step()
+            torch.cuda.synchronize()
+            flops = 2.0 * b * sh.n_in * sh.n_out
+            kern = {}
+            for tag, kid in (("fwd", C.KERNEL_FWD), ("dx", C.KERNEL_DX), ("dw", C.KERNEL_DW)):
+                kms, _ = C.comera_ttm_plan_kernel_time(lay.plan.handle, kid)
+                kern[tag] = {"ms": round(kms, 5), "tflops": round(flops / (kms * 1e-3) / 1e12, 1),
+                             "frac_fp8_peak": round(flops / (kms * 1e-3) / 5.0e15, 4)}
+            C.comera_ttm_plan_set_timing(lay.plan.handle, False)
+            del lay
+            torch.cuda.empty_cache()
+            ref = Layer(sh, X, dY, G, D, ma, b, "bf16")
+            bms, _ = time_loop(ref.step, k, warmup)
+            order = ref.plan.order_info(ref.plan.chosen)["desc"]
+            del ref
+            torch.cuda.empty_cache()
+            dms, _ = time_loop(dense_step_fn(sh, X, dY), k, warmup)
+            f8fn, f8err = dense_fp8_step_fn(sh, X, dY)
+            d8ms = time_loop(f8fn, k, warmup)[0] if f8fn else None
+            res[f"w{wid}_{sh.name}"] = {
+                "workload": w.name, "layer": sh.name, "tokens": b, "activations": "bf16",
+                "fp8_ms_per_step": round(ms, 4), "fp8_tokens_per_s": round(b / (ms * 1e-3), 1),
+                "fp8_gemm_kernels": kern,
+                "bf16_ms_per_step": round(bms, 4), "bf16_order": order,
+                "dense_bf16_ms_per_step": round(dms, 4),
+                "dense_fp8_ms_per_step": None if d8ms is None else round(d8ms, 4),
+                "dense_fp8_error": f8err,
+                "fp8_speedup_vs_dense_bf16": round(dms / ms, 3),
+                "fp8_speedup_vs_dense_fp8": None if d8ms is None else round(d8ms / ms, 3),
+                "fp8_speedup_vs_bf16_layer": round(bms / ms, 3)}
+            del X, dY, G, D
+            torch.cuda.empty_cache()
+    return res
+
+
 def order_timings(wids, steps, warmup):
     """Every executable contraction order of each layer of the given
     workloads, timed forward and backward separately, beside the dense
@@ -443,6 +531,7 @@ def main():
     ap.add_argument("--traffic-summary", nargs=5, metavar=("FETCH_DIR", "WRITE_DIR", "KERNEL", "GRID", "TAG"),
                     help="write profiles/traffic_<TAG>_<dtype>.md from two counter runs (no GPU); GRID 0 = any")
     ap.add_argument("--commands", nargs="*", default=[], help="commands recorded in a summary")
+    ap.add_argument("--fp8-only", action="store_true", help="only the mixed-precision (FP8) figures")
     ap.add_argument("--orders", type=int, nargs="*", default=None, metavar="WORKLOAD",
                     help="time every contraction order of these workloads (default 0 1 5) and exit")
     args = ap.parse_args()
@@ -480,6 +569,9 @@ def run_gpu(args):
         wids = args.orders or [0, 1, 5]
         for rec in order_timings(wids, args.steps, args.warmup):
             print(json.dumps(rec), flush=True)
+        return
+    if args.fp8_only:
+        print(json.dumps(fp8_workloads(args.steps, args.warmup)), flush=True)
         return
     runs = {}
     for act in ("f32", "bf16"):
@@ -537,6 +629,8 @@ def run_gpu(args):
     if not args.no_extra:
         log("[bench] other workloads")
         out["other_workloads"] = other_workloads(max(5, args.steps // 2), 3)
+        log("[bench] mixed-precision (FP8) layers")
+        out["fp8_layers"] = fp8_workloads(max(5, args.steps // 2), 3)
     if not args.no_cpu:
         log("[bench] CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline()

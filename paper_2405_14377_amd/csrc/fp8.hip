@@ -48,6 +48,53 @@ __global__ __launch_bounds__(256) void amax_partial_kernel(const void *__restric
     if (threadIdx.x == 0) pmax[blockIdx.x] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
 }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// |x| of the V elements in a 16-byte chunk (V = 4 fp32 or 8 bf16)
+template <int V>
+__device__ __forceinline__ float chunk_absmax(const u32x4 v) {
+    float m = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        if constexpr (V == 4) {
+            m = fmaxf(m, fabsf(__uint_as_float(v[w])));
+        } else {
+            m = fmaxf(m, fabsf(__uint_as_float(v[w] << 16)));
+            m = fmaxf(m, fabsf(__uint_as_float(v[w] & 0xFFFF0000u)));
+        }
+    }
+    return m;
+}
+
+// The same maxima with 16-byte loads, four in flight per thread; x 16-byte
+// aligned.  Elements past the last whole chunk are taken by workgroup 0.
+template <int V>
+__global__ __launch_bounds__(512) void amax_vec_kernel(const void *__restrict__ x, int dtype, int64_t n,
+                                                       float *__restrict__ pmax) {
+    __shared__ float red[8];
+    const u32x4 *xv = reinterpret_cast<const u32x4 *>(x);
+    const int64_t nv = n / V;
+    const int64_t stride = int64_t(gridDim.x) * 512;
+    int64_t i = int64_t(blockIdx.x) * 512 + threadIdx.x;
+    float m = 0.f;
+    for (; i + 3 * stride < nv; i += 4 * stride) {
+        const u32x4 a = xv[i], b = xv[i + stride], c = xv[i + 2 * stride], d = xv[i + 3 * stride];
+        m = fmaxf(fmaxf(m, fmaxf(chunk_absmax<V>(a), chunk_absmax<V>(b))),
+                  fmaxf(chunk_absmax<V>(c), chunk_absmax<V>(d)));
+    }
+    for (; i < nv; i += stride) m = fmaxf(m, chunk_absmax<V>(xv[i]));
+    if (blockIdx.x == 0)
+        for (int64_t j = nv * V + threadIdx.x; j < n; j += 512) m = fmaxf(m, fabsf(load_act(x, dtype, j)));
+    m = wave_max(m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float r = red[0];
+        for (int w = 1; w < 8; ++w) r = fmaxf(r, red[w]);
+        pmax[blockIdx.x] = r;
+    }
+}
+
 // largest power of two s with amax * s <= 448 (448 = 0.875 * 2^9), the
 // exponent clamped to [-60, 60]; 1 for amax == 0
 __device__ __forceinline__ float pow2_scale(float amax) {
@@ -132,6 +179,74 @@ __global__ __launch_bounds__(256) void quant_kernel(const void *__restrict__ x, 
     }
 }
 
+// quant_kernel with 16-byte loads (V elements per chunk), V-byte stores of
+// q and 16-byte stores of qt through a transposed LDS tile.  Requires x
+// 16-byte aligned, C % V == 0, q (if any) V-byte aligned with ldq % V == 0,
+// qt (if any) 16-byte aligned with ldt % 16 == 0: every chunk then lies
+// wholly inside or wholly outside each bound.
+template <int V>
+__global__ __launch_bounds__(256) void quant_vec_kernel(const void *__restrict__ x, int64_t R, int64_t C,
+                                                        const float *__restrict__ pmax, int nb, uint8_t *__restrict__ q,
+                                                        int64_t ldq, uint8_t *__restrict__ qt, int64_t ldt,
+                                                        float *__restrict__ s_out, const float *pa, float *oa,
+                                                        const float *pb, float *ob) {
+    constexpr int CPR = 64 / V;              // chunks per tile row
+    constexpr int NCH = 64 * CPR / 256;      // chunks per thread
+    constexpr int ESZ = 16 / V;              // bytes per element
+    __shared__ float red[4];
+    __shared__ __attribute__((aligned(16))) uint8_t tt[64][80];   // tt[c][r], 80-byte pitch
+    const int tid = threadIdx.x;
+    float m = 0.f;
+    for (int i = tid; i < nb; i += 256) m = fmaxf(m, pmax[i]);
+    m = wave_max(m);
+    if ((tid & 63) == 0) red[tid >> 6] = m;
+    __syncthreads();
+    const float s = pow2_scale(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])));
+    if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) {
+        if (s_out) s_out[0] = s;
+        if (pa && oa) *oa = 1.f / (s * *pa);
+        if (pb && ob) *ob = 1.f / (s * *pb);
+    }
+    const int64_t r0 = int64_t(blockIdx.x) * 64, c0 = int64_t(blockIdx.y) * 64;
+    const char *xb = reinterpret_cast<const char *>(x);
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+        const int id = tid + 256 * i;
+        const int rr = id / CPR, ch = id % CPR;
+        const int64_t r = r0 + rr, c = c0 + int64_t(ch) * V;
+        uint32_t w[V / 4];
+#pragma unroll
+        for (int k = 0; k < V / 4; ++k) w[k] = 0u;
+        if (r < R && c < C) {
+            const u32x4 v = *reinterpret_cast<const u32x4 *>(xb + (r * C + c) * ESZ);
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                float f;
+                if constexpr (V == 4) f = __uint_as_float(v[e]);
+                else f = __uint_as_float((e & 1) ? (v[e >> 1] & 0xFFFF0000u) : (v[e >> 1] << 16));
+                w[e >> 2] |= uint32_t(e4m3_rne(f * s)) << (8 * (e & 3));
+            }
+        }
+        if (q && r < R && c < ldq) {
+            if constexpr (V == 4) {
+                *reinterpret_cast<uint32_t *>(q + r * ldq + c) = w[0];
+            } else {
+                *reinterpret_cast<uint2 *>(q + r * ldq + c) = make_uint2(w[0], w[1]);
+            }
+        }
+        if (qt) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) tt[ch * V + e][rr] = uint8_t(w[e >> 2] >> (8 * (e & 3)));
+        }
+    }
+    if (!qt) return;
+    __syncthreads();
+    // qt rows c0 .. c0 + 63, bytes r0 .. r0 + 63: one 16-byte piece per thread
+    const int cc = tid >> 2, part = tid & 3;
+    const int64_t c = c0 + cc, r = r0 + part * 16;
+    if (c < C && r < ldt) *reinterpret_cast<u32x4 *>(qt + c * ldt + r) = *reinterpret_cast<const u32x4 *>(&tt[cc][part * 16]);
+}
+
 }  // namespace
 
 int fp8_amax_blocks() { return kAmaxBlocks; }
@@ -142,15 +257,36 @@ int launch_fp8_quant(const void *x, int dtype, int64_t R, int64_t C, float *pmax
     if (R <= 0 || C <= 0) return 0;
     if ((q && ldq < C) || (qt && ldt < R)) return int(hipErrorInvalidValue);
     const int64_t n = R * C;
-    const int nb = int(std::min<int64_t>(kAmaxBlocks, (n + 255) / 256));
-    hipLaunchKernelGGL(amax_partial_kernel, dim3(nb), dim3(256), 0, hipStream_t(stream), x, dtype, n, pmax);
+    const int V = dtype == COMERA_BF16 ? 8 : 4;
+    auto al = [](const void *ptr, int a) { return reinterpret_cast<uintptr_t>(ptr) % uintptr_t(a) == 0; };
+    const bool xa = al(x, 16);
+    int nb;
+    if (xa) {
+        nb = int(std::min<int64_t>(kAmaxBlocks, std::max<int64_t>(1, (n / V + 2047) / 2048)));
+        if (V == 8)
+            hipLaunchKernelGGL(amax_vec_kernel<8>, dim3(nb), dim3(512), 0, hipStream_t(stream), x, dtype, n, pmax);
+        else
+            hipLaunchKernelGGL(amax_vec_kernel<4>, dim3(nb), dim3(512), 0, hipStream_t(stream), x, dtype, n, pmax);
+    } else {
+        nb = int(std::min<int64_t>(kAmaxBlocks, (n + 255) / 256));
+        hipLaunchKernelGGL(amax_partial_kernel, dim3(nb), dim3(256), 0, hipStream_t(stream), x, dtype, n, pmax);
+    }
     if (int e = int(hipGetLastError())) return e;
     const int64_t rows = qt ? std::max<int64_t>(R, ldt) : R;
     const int64_t cols = q ? std::max<int64_t>(C, ldq) : C;
     const int64_t gx = (rows + 63) / 64, gy = (cols + 63) / 64;
     if (gx > 2147483647 || gy > 65535) return int(hipErrorInvalidValue);
-    hipLaunchKernelGGL(quant_kernel, dim3(unsigned(gx), unsigned(gy)), dim3(256), 0, hipStream_t(stream), x, dtype, R,
-                       C, pmax, nb, q, ldq, qt, ldt, s_out, pa, oa, pb, ob);
+    const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(gy), 1);
+    const bool vec = xa && C % V == 0 && (!q || (al(q, V) && ldq % V == 0)) && (!qt || (al(qt, 16) && ldt % 16 == 0));
+    if (vec && V == 8)
+        hipLaunchKernelGGL(quant_vec_kernel<8>, grid, dim3(256), 0, hipStream_t(stream), x, R, C, pmax, nb, q, ldq,
+                           qt, ldt, s_out, pa, oa, pb, ob);
+    else if (vec)
+        hipLaunchKernelGGL(quant_vec_kernel<4>, grid, dim3(256), 0, hipStream_t(stream), x, R, C, pmax, nb, q, ldq,
+                           qt, ldt, s_out, pa, oa, pb, ob);
+    else
+        hipLaunchKernelGGL(quant_kernel, grid, dim3(256), 0, hipStream_t(stream), x, dtype, R, C, pmax, nb, q, ldq,
+                           qt, ldt, s_out, pa, oa, pb, ob);
     return int(hipGetLastError());
 }
 

@@ -495,28 +495,26 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
             // scales 127 = 2^0): of each 64-byte k step, lane (lr, lh) supplies
             // bytes 16 lh .. 16 lh + 15 and 32 + 16 lh .. 32 + 16 lh + 15 of its
             // row (a_s, b_s already point 16 lh bytes in), the same k slots for
-            // A and B
+            // A and B.
 #pragma unroll
             for (int ks = 0; ks < KT / 64; ++ks) {
-                i32x8 av[TM], bv[TN];
-#pragma unroll
-                for (int i = 0; i < TM; ++i) {
-                    const u32x4 lo = *reinterpret_cast<const u32x4 *>(a_s + i * 32 * FP + ks * 64);
-                    const u32x4 hi = *reinterpret_cast<const u32x4 *>(a_s + i * 32 * FP + ks * 64 + 32);
-                    av[i] = i32x8{int(lo.x), int(lo.y), int(lo.z), int(lo.w), int(hi.x), int(hi.y), int(hi.z), int(hi.w)};
-                }
+                i32x8 bv[TN];
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
                     const u32x4 lo = *reinterpret_cast<const u32x4 *>(b_s + j * 32 * FP + ks * 64);
                     const u32x4 hi = *reinterpret_cast<const u32x4 *>(b_s + j * 32 * FP + ks * 64 + 32);
-                    bv[j] = i32x8{int(lo.x), int(lo.y), int(lo.z), int(lo.w), int(hi.x), int(hi.y), int(hi.z), int(hi.w)};
+                    bv[j] = __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
                 }
 #pragma unroll
-                for (int i = 0; i < TM; ++i)
+                for (int i = 0; i < TM; ++i) {
+                    const u32x4 lo = *reinterpret_cast<const u32x4 *>(a_s + i * 32 * FP + ks * 64);
+                    const u32x4 hi = *reinterpret_cast<const u32x4 *>(a_s + i * 32 * FP + ks * 64 + 32);
+                    const i32x8 av = __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[i], bv[j], acc[i][j], 0, 0, 0,
+                        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv[j], acc[i][j], 0, 0, 0,
                                                                                     127, 0, 127);
+                }
             }
         } else if constexpr (sizeof(T) == 2) {
 #pragma unroll
@@ -643,7 +641,11 @@ int pick_tile(int64_t M, int64_t N, int splits) {
 enum FastId {
     F128x128_128 = 0, F128x64_128, F64x128_128, F128x128_64, F256x128_64,
     // bf16 only, eight waves: 256 x 256 (waves of 128 x 64), 256 x 128 (64 x 64)
-    F256x256_128w8, F256x128_128w8
+    F256x256_128w8, F256x128_128w8,
+    // FP8 only, eight waves of 128 x 64 on 64-byte K rows (the operands of
+    // two 64-byte steps do not fit the registers of a wave beside its
+    // accumulators)
+    F256x256_64w8
 };
 
 template <typename T, bool AK, bool BK, bool OB, int BM, int BN, int WM, int WN, int KTB, int NT = 256>
@@ -671,11 +673,14 @@ int launch_fast(const GemmArgs &g, const GemmParams &p, int id, void *stream) {
         case F128x128_64: return go_fast<T, AK, BK, OB, 128, 128, 64, 64, 64>(g, p, stream);
         case F256x128_64: return go_fast<T, AK, BK, OB, 256, 128, 128, 64, 64>(g, p, stream);
     }
-    if constexpr (sizeof(T) <= 2) {
+    if constexpr (sizeof(T) == 2) {
         switch (id) {
             case F256x256_128w8: return go_fast<T, AK, BK, OB, 256, 256, 128, 64, 128, 512>(g, p, stream);
             case F256x128_128w8: return go_fast<T, AK, BK, OB, 256, 128, 64, 64, 128, 512>(g, p, stream);
         }
+    }
+    if constexpr (sizeof(T) == 1) {
+        if (id == F256x256_64w8) return go_fast<T, AK, BK, OB, 256, 256, 128, 64, 64, 512>(g, p, stream);
     }
     return int(hipErrorInvalidValue);
 }
@@ -690,6 +695,7 @@ int pick_fast(const GemmArgs &g, int splits) {
     // bf16: 256 x 256 tiles of eight waves once they give two or more
     // workgroups per CU (transposed operands, split over K: half a wave of
     // workgroups is enough)
+    if (g.dtype == kDtypeFp8 && t256 >= 512) return F256x256_64w8;
     if ((g.dtype == COMERA_BF16 || g.dtype == kDtypeFp8) && g.a_kc == g.b_kc && t256 >= (g.a_kc ? 512 : 128))
         return F256x256_128w8;
     if (g.a_kc && g.b_kc) {
@@ -787,8 +793,9 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     int fast = g.fast >= 0 ? g.fast : (g.fast == -1 && g.tile < 0 ? pick_fast(gg, gg.splits) : -1);
     GemmParams pf = p;
     if (fast >= 0) {
-        const int ktb = (fast == F128x128_64 || fast == F256x128_64) ? 64 : 128;
+        const int ktb = (fast == F128x128_64 || fast == F256x128_64 || fast == F256x256_64w8) ? 64 : 128;
         if (fast >= F256x256_128w8 && g.dtype == COMERA_F32) fast = -1;
+        if (fast == F256x256_64w8 && g.dtype != kDtypeFp8) fast = -1;
         const int64_t kt = ktb / esz;
         pf.kchunk = ceil_div(p.kchunk, kt) * kt;
         if (!fast_ok(gg, pf.kchunk, ktb)) fast = -1;

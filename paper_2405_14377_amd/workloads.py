@@ -96,6 +96,13 @@ WORKLOADS = {
                    (TTMLayerShape("tt_ffn_up", (8, 8, 12, 1, 1, 1), (1, 1, 1, 16, 16, 12), (1,) + (30,) * 5 + (1,)),
                     TTMLayerShape("tt_qkvo", (8, 8, 12, 1, 1, 1), (1, 1, 1, 12, 8, 8), (1,) + (30,) * 5 + (1,))),
                    4096, ("f32", "bf16"), ("bernoulli", 0.8)),
+    # the TT shapes of the paper's mixed-precision runtime table (appendix,
+    # Tab. LP-time): 1024 -> 4096 as (16, 8, 8 | 16, 16, 16) and 1024 -> 1024
+    # as (16, 8, 8 | 8, 8, 16), ranks 32, 40000 tokens
+    6: TTMWorkload(6, "tt_layout_1024x4096_1024x1024_r32_b40000",
+                   (TTMLayerShape("tt_1024x4096", (16, 8, 8, 1, 1, 1), (1, 1, 1, 16, 16, 16), (1,) + (32,) * 5 + (1,)),
+                    TTMLayerShape("tt_1024x1024", (16, 8, 8, 1, 1, 1), (1, 1, 1, 8, 8, 16), (1,) + (32,) * 5 + (1,))),
+                   40000, ("bf16",), ("ones",)),
 }
 
 

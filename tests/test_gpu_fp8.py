@@ -220,3 +220,25 @@ def test_fp8_smaller_batch_and_empty():
         for a, c in zip(dG, dGo):
             assert rel_err(to_np(a), c) <= 1e-4
     assert run.forward(to_dev(np.zeros((1, 768))), 0).shape[0] == 0
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_integer_layer_large_tiles(act):
+    """8192 tokens through 1024 -> 4096: the forward and dX products are large
+    enough for the eight-wave 256 x 256 FP8 tiles; still bit-exact."""
+    n, m, r, b = (4, 8, 4, 8), (8, 8, 8, 8), (1, 16, 16, 16, 1), 8192
+    rng = np.random.default_rng(15)
+    cores = wl.integer_bond_diagonal_cores(rng, n, m, r)
+    run = TTMRun(n, m, r, cores, None, b, act, force_order=0, reuse=True, fp8=True)
+    X = rng.integers(-8, 9, (b, run.n_in)).astype(np.float32)
+    dY = rng.integers(-8, 9, (b, run.n_out)).astype(np.float32)
+    Xt, dYt = to_dev(X, act), to_dev(dY, act)
+    Y = to_np(run.forward(Xt))
+    dX, dG = run.backward(Xt, dYt)
+    W = OT.dense_weight(cores)
+    rnd = (lambda a: wl.to_bf16_values(a.astype(np.float32))) if act == "bf16" else (lambda a: a)
+    assert np.array_equal(Y, rnd(X.astype(np.float64) @ W))
+    assert np.array_equal(to_np(dX), rnd(dY.astype(np.float64) @ W.T))
+    dGo = OT.project_dW(X.T.astype(np.float64) @ dY, cores)
+    for a, c in zip(dG, dGo):
+        assert rel_err(to_np(a), c) <= 1e-4
