@@ -178,6 +178,7 @@ struct GemmParams {
     int64_t M, N, K, lda, ldb, kchunk, split_stride;
     Remap rmap, cmap;
     int vec_a, vec_b;
+    int vec_c;   // fast-kernel output: four consecutive columns form one aligned vector (see epilogue_t)
     int gw;   // tile-order group width in column tiles (see tile_of)
     uint32_t tx, ty;   // column tiles, row tiles (the grid is one-dimensional)
     const float *oscale;   // device scalar multiplying every result, or null
@@ -234,6 +235,54 @@ __device__ __forceinline__ void epilogue(const GemmParams &p, const f32x16 (&acc
                     reinterpret_cast<uint16_t *>(p.C)[zoff + ro + co] = f32_to_bf16_rne(acc[i][j][v]);
                 else
                     reinterpret_cast<float *>(p.C)[zoff + ro + co] = acc[i][j][v];
+            }
+    }
+}
+
+// Write the accumulators of the swapped product: element v of lane l is
+// row l%32 of the block and column 8(v/4) + 4(l/32) + v%4, i.e. four
+// consecutive columns per group g = v/4.  With p.vec_c (columns linear with
+// stride 1, row offsets and split stride multiples of 4, C aligned) a group
+// inside the matrix is one 16-byte (fp32) or 8-byte (bf16) store; other
+// groups and layouts are written element by element through the remap
+// tables (-1 = outside).
+template <bool OUT_BF16, int TM, int TN, int WM, int WN>
+__device__ __forceinline__ void epilogue_t(const GemmParams &p, const f32x16 (&acc)[TM][TN], const int64_t *roff,
+                                           const int64_t *coff, int64_t n0, int wm, int wn, int lr, int lh) {
+    const int64_t zoff = tile_of(p).z * p.split_stride;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const int64_t ro = roff[wm * WM + i * 32 + lr];
+        if (ro < 0) continue;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int cl = wn * WN + j * 32 + 8 * g + 4 * lh;
+                const f32x16 &a = acc[i][j];
+                if (p.vec_c && n0 + cl + 3 < p.N) {
+                    const int64_t at = zoff + ro + n0 + cl;
+                    if constexpr (OUT_BF16) {
+                        const uint32_t lo = uint32_t(f32_to_bf16_rne(a[4 * g])) |
+                                            (uint32_t(f32_to_bf16_rne(a[4 * g + 1])) << 16);
+                        const uint32_t hi = uint32_t(f32_to_bf16_rne(a[4 * g + 2])) |
+                                            (uint32_t(f32_to_bf16_rne(a[4 * g + 3])) << 16);
+                        *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(p.C) + at) = make_uint2(lo, hi);
+                    } else {
+                        *reinterpret_cast<float4 *>(reinterpret_cast<float *>(p.C) + at) =
+                            make_float4(a[4 * g], a[4 * g + 1], a[4 * g + 2], a[4 * g + 3]);
+                    }
+                    continue;
+                }
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int64_t co = coff[cl + e];
+                    if (co < 0) continue;
+                    if constexpr (OUT_BF16)
+                        reinterpret_cast<uint16_t *>(p.C)[zoff + ro + co] = f32_to_bf16_rne(a[4 * g + e]);
+                    else
+                        reinterpret_cast<float *>(p.C)[zoff + ro + co] = a[4 * g + e];
+                }
             }
     }
 }
@@ -427,13 +476,19 @@ struct FastLoader {
     }
 };
 
-template <typename T, bool A_KC, bool B_KC, bool OUT_BF16, int BM, int BN, int WM, int WN, int KTB, int NT = 256>
+// PF = register stages of global prefetch: 1 keeps the next K tile in
+// registers while the current one is multiplied; 2 keeps two (the loads of
+// tile kt + 2 are issued before tile kt is multiplied), for tiles whose K
+// step is short against the load latency.
+template <typename T, bool A_KC, bool B_KC, bool OUT_BF16, int BM, int BN, int WM, int WN, int KTB, int NT = 256,
+          int PF = 1>
 __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
     constexpr int FP = KTB + 16;
     constexpr int KT = KTB / int(sizeof(T));
     constexpr int WAVES_N = BN / WN;
     constexpr int TM = WM / 32, TN = WN / 32;
     static_assert((BM / WM) * (BN / WN) * 64 == NT, "one wave per WM x WN block");
+    static_assert(PF == 1 || PF == 2, "prefetch depth");
     extern __shared__ __attribute__((aligned(16))) char smem[];
     char *sA0 = smem;
     char *sA1 = smem + BM * FP;
@@ -475,19 +530,14 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
         la.store(sA0, tid);
         lb.store(sB0, tid);
     }
-    __syncthreads();
 
     const int lr = lane & 31, lh = lane >> 5;
     const int aoff = (wm * WM + lr) * FP + lh * 16, boff = (wn * WN + lr) * FP + lh * 16;
-    for (int kt = 0; kt < ntiles; ++kt) {
-        const int cur = kt & 1;
-        const bool more = kt + 1 < ntiles;
-        if (more) {
-            abase += astep;
-            bbase += bstep;
-            la.load(abase);
-            lb.load(bbase);
-        }
+    // acc[i][j] += the product of the K tile in LDS buffer cur, with the
+    // operands swapped (B block as the MFMA's first operand): acc[i][j]
+    // holds the transposed 32 x 32 block, so each lane ends with four
+    // consecutive output columns per group (see epilogue_t)
+    auto mma = [&](int cur) {
         const char *a_s = (cur ? sA1 : sA0) + aoff;
         const char *b_s = (cur ? sB1 : sB0) + boff;
         if constexpr (sizeof(T) == 1) {
@@ -512,7 +562,7 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
                     const i32x8 av = __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv[j], acc[i][j], 0, 0, 0,
+                        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bv[j], av, acc[i][j], 0, 0, 0,
                                                                                     127, 0, 127);
                 }
             }
@@ -528,7 +578,7 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[j], av[i], acc[i][j], 0, 0, 0);
             }
         } else {
 #pragma unroll
@@ -544,14 +594,72 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
                     for (int i = 0; i < TM; ++i)
 #pragma unroll
                         for (int j = 0; j < TN; ++j)
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][e], bv[j][e], acc[i][j], 0, 0, 0);
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(bv[j][e], av[i][e], acc[i][j], 0, 0, 0);
             }
         }
-        if (more) {
-            la.store(cur ? sA0 : sA1, tid);
-            lb.store(cur ? sB0 : sB1, tid);
+    };
+
+    if constexpr (PF == 1) {
+        __syncthreads();
+        for (int kt = 0; kt < ntiles; ++kt) {
+            const int cur = kt & 1;
+            const bool more = kt + 1 < ntiles;
+            if (more) {
+                abase += astep;
+                bbase += bstep;
+                la.load(abase);
+                lb.load(bbase);
+            }
+            mma(cur);
+            if (more) {
+                la.store(cur ? sA0 : sA1, tid);
+                lb.store(cur ? sB0 : sB1, tid);
+            }
+            __syncthreads();
+        }
+    } else {
+        // tile 0 is in buffer 0; tile 1 waits in la / lb, tile t + 2 is
+        // loaded into the other register set while tile t is multiplied
+        FastLoader<T, A_KC, BM, KTB, NT> la2;
+        FastLoader<T, B_KC, BN, KTB, NT> lb2;
+        la2.setup(p.lda, m0, p.M, tid);
+        lb2.setup(p.ldb, n0, p.N, tid);
+        if (ntiles > 1) {
+            abase += astep;
+            bbase += bstep;
+            la.load(abase);
+            lb.load(bbase);
         }
         __syncthreads();
+        for (int kt = 0; kt < ntiles; kt += 2) {
+            // buffer 0 holds tile kt, la / lb hold tile kt + 1
+            if (kt + 2 < ntiles) {
+                abase += astep;
+                bbase += bstep;
+                la2.load(abase);
+                lb2.load(bbase);
+            }
+            mma(0);
+            if (kt + 1 < ntiles) {
+                la.store(sA1, tid);
+                lb.store(sB1, tid);
+            }
+            __syncthreads();
+            if (kt + 1 >= ntiles) break;
+            // buffer 1 holds tile kt + 1, la2 / lb2 hold tile kt + 2
+            if (kt + 3 < ntiles) {
+                abase += astep;
+                bbase += bstep;
+                la.load(abase);
+                lb.load(bbase);
+            }
+            mma(1);
+            if (kt + 2 < ntiles) {
+                la2.store(sA0, tid);
+                lb2.store(sB0, tid);
+            }
+            __syncthreads();
+        }
     }
     if (p.oscale) {
         const float sc = *p.oscale;
@@ -562,7 +670,7 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[i][j][v] *= sc;
     }
-    epilogue<OUT_BF16, TM, TN, WM, WN>(p, acc, roff, coff, wm, wn, lr, lh);
+    epilogue_t<OUT_BF16, TM, TN, WM, WN>(p, acc, roff, coff, n0, wm, wn, lr, lh);
 }
 
 enum TileId { T128x128 = 0, T64x64 = 1, T128x32 = 2, T32x128 = 3, T128x64 = 4, T64x128 = 5 };
@@ -642,16 +750,17 @@ enum FastId {
     F128x128_128 = 0, F128x64_128, F64x128_128, F128x128_64, F256x128_64,
     // bf16 only, eight waves: 256 x 256 (waves of 128 x 64), 256 x 128 (64 x 64)
     F256x256_128w8, F256x128_128w8,
-    // FP8 only, eight waves of 128 x 64 on 64-byte K rows (the operands of
-    // two 64-byte steps do not fit the registers of a wave beside its
+    // bf16 and FP8, eight waves of 128 x 64 on 64-byte K rows with two
+    // register stages of prefetch (FP8: the operands of two 64-byte steps
+    // per stage would not fit the registers of a wave beside its
     // accumulators)
     F256x256_64w8
 };
 
-template <typename T, bool AK, bool BK, bool OB, int BM, int BN, int WM, int WN, int KTB, int NT = 256>
+template <typename T, bool AK, bool BK, bool OB, int BM, int BN, int WM, int WN, int KTB, int NT = 256, int PF = 1>
 int go_fast(const GemmArgs &g, const GemmParams &p, void *stream) {
     constexpr size_t lds = size_t(2) * (BM + BN) * (KTB + 16) + size_t(BM + BN) * sizeof(int64_t);
-    auto kern = gemm_fast_kernel<T, AK, BK, OB, BM, BN, WM, WN, KTB, NT>;
+    auto kern = gemm_fast_kernel<T, AK, BK, OB, BM, BN, WM, WN, KTB, NT, PF>;
     // above the default 64 KB of dynamic LDS: raise the limit once per kernel
     static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                                    hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
@@ -679,8 +788,8 @@ int launch_fast(const GemmArgs &g, const GemmParams &p, int id, void *stream) {
             case F256x128_128w8: return go_fast<T, AK, BK, OB, 256, 128, 64, 64, 128, 512>(g, p, stream);
         }
     }
-    if constexpr (sizeof(T) == 1) {
-        if (id == F256x256_64w8) return go_fast<T, AK, BK, OB, 256, 256, 128, 64, 64, 512>(g, p, stream);
+    if constexpr (sizeof(T) <= 2) {
+        if (id == F256x256_64w8) return go_fast<T, AK, BK, OB, 256, 256, 128, 64, 64, 512, 2>(g, p, stream);
     }
     return int(hipErrorInvalidValue);
 }
@@ -784,6 +893,12 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     };
     p.vec_a = aligned(g.A, g.lda);
     p.vec_b = aligned(g.B, g.ldb);
+    {
+        bool v = g.cmap.nd == 1 && g.cmap.stride[0] == 1 && p.split_stride % 4 == 0 &&
+                 reinterpret_cast<uintptr_t>(g.C) % (g.out_bf16 ? 8 : 16) == 0;
+        for (int k = 0; k < g.rmap.nd; ++k) v = v && g.rmap.stride[k] % 4 == 0;
+        p.vec_c = v ? 1 : 0;
+    }
     p.gw = 0;
     p.oscale = g.oscale;
     GemmArgs gg = g;
@@ -795,7 +910,7 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     if (fast >= 0) {
         const int ktb = (fast == F128x128_64 || fast == F256x128_64 || fast == F256x256_64w8) ? 64 : 128;
         if (fast >= F256x256_128w8 && g.dtype == COMERA_F32) fast = -1;
-        if (fast == F256x256_64w8 && g.dtype != kDtypeFp8) fast = -1;
+
         const int64_t kt = ktb / esz;
         pf.kchunk = ceil_div(p.kchunk, kt) * kt;
         if (!fast_ok(gg, pf.kchunk, ktb)) fast = -1;
