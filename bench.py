@@ -405,7 +405,7 @@ def dense_fp8_step_fn(sh, X, dY):
 
     def fn():
         x8, sx = q(X)
-        w8t, sw = q(W.t())               # [N_out, N_in]: column-major B below
+        w8t, sw = q(W.t().contiguous())  # [N_out, N_in] row-major: its transpose is the column-major B
         d8, sd = q(dY)
         torch._scaled_mm(x8, w8t.t(), scale_a=sx, scale_b=sw, out_dtype=torch.bfloat16)
         w8, _ = q(W)
