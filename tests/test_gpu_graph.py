@@ -132,3 +132,49 @@ def test_embed_step_graph_replays():
                     assert torch.equal(a, c), rep
     assert int(run.err.item()) == 0
     del g
+
+
+@pytest.mark.parametrize("reuse", [False, True])
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_fp8_step_graph_replays(act, reuse):
+    """The mixed-precision layer (FP8 products): the quantisers write their
+    scales into the workspace on every call, so replays with new inputs must
+    match eager calls bit for bit."""
+    import torch
+    n, m, r, b = (8, 8, 12), (12, 8, 8), (1, 8, 8, 1), 300
+    cores, D, xs = _ttm_inputs(33, n, m, r, b, act, 3)
+    run = TTMRun(n, m, r, cores, D, b, act, force_order=0, reuse=reuse, fp8=True)
+    ref_run = TTMRun(n, m, r, cores, D, b, act, force_order=0, reuse=reuse, fp8=True)
+    Xs, dYs = to_dev(xs[0][0], act), to_dev(xs[0][1], act)
+    Ys = torch.empty((b, run.n_out), dtype=run.tdt, device="cuda")
+    dXs = torch.empty((b, run.n_in), dtype=run.tdt, device="cuda")
+    dGs = [torch.empty_like(g) for g in run.G]
+
+    def step():
+        C.comera_ttm_forward(run.plan.handle, b, Xs, run.G, run.D, Ys, run.ws)
+        C.comera_ttm_backward(run.plan.handle, b, Xs, dYs, run.G, run.D, dXs, dGs, run.ws)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            step()
+        torch.cuda.synchronize()
+        for rep in range(2):
+            for X, dY in xs:
+                Xt, dYt = to_dev(X, act), to_dev(dY, act)
+                Yr = ref_run.forward(Xt)
+                dXr, dGr = ref_run.backward(Xt, dYt)
+                torch.cuda.synchronize()
+                Xs.copy_(Xt)
+                dYs.copy_(dYt)
+                g.replay()
+                torch.cuda.synchronize()
+                assert torch.equal(Ys, Yr), rep
+                assert torch.equal(dXs, dXr), rep
+                for a, c in zip(dGs, dGr):
+                    assert torch.equal(a, c), rep
+    del g
