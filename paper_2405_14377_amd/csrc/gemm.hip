@@ -178,6 +178,7 @@ struct GemmParams {
     int64_t M, N, K, lda, ldb, kchunk, split_stride;
     Remap rmap, cmap;
     int vec_a, vec_b;
+    int stage_c;   // fast kernel: row-major output staged through LDS (see epilogue_lds)
     int gw;   // tile-order group width in column tiles (see tile_of)
     uint32_t tx, ty;   // column tiles, row tiles (the grid is one-dimensional)
     const float *oscale;   // device scalar multiplying every result, or null
@@ -427,6 +428,61 @@ struct FastLoader {
     }
 };
 
+// LDS of the fast kernel before the row / column offset tables: the two
+// operand buffers, or, for eight-wave tiles (one workgroup per CU anyway),
+// the staged output tile when that is larger and still fits the 160 KB of
+// a CU.
+constexpr size_t kLdsPerCu = 160 * 1024;
+template <int BM, int BN, int KTB, int NT, bool OB>
+constexpr size_t fast_main_lds() {
+    const size_t ops = size_t(2) * (BM + BN) * (KTB + 16);
+    const size_t stg = size_t(BM) * (BN * (OB ? 2 : 4) + 16);
+    const size_t tables = size_t(BM + BN) * sizeof(int64_t);
+    return (NT == 512 && stg > ops && stg + tables <= kLdsPerCu) ? stg : ops;
+}
+template <int BM, int BN, int KTB, int NT, bool OB>
+constexpr bool fast_stage_fits() {
+    return size_t(BM) * (BN * (OB ? 2 : 4) + 16) <= fast_main_lds<BM, BN, KTB, NT, OB>();
+}
+
+// Row-major output through LDS: the accumulators are written into a
+// BM x BN tile in LDS (16 bytes of padding per row), then every thread
+// stores 16-byte pieces of whole rows, so each output row leaves as
+// contiguous segments instead of 2- or 4-byte scattered stores.  Requires
+// (p.stage_c) linear row and column maps with unit column stride, N, the
+// row stride and the split stride multiples of the 16-byte piece, and C
+// 16-byte aligned.
+template <bool OUT_BF16, int TM, int TN, int WM, int WN, int BM, int BN, int NT>
+__device__ __forceinline__ void epilogue_lds(const GemmParams &p, const f32x16 (&acc)[TM][TN], char *stage,
+                                             int64_t m0, int64_t n0, int wm, int wn, int lr, int lh, int tid) {
+    constexpr int OESZ = OUT_BF16 ? 2 : 4;
+    constexpr int CP = BN * OESZ + 16;
+    constexpr int PIECES = BN * OESZ / 16;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int row = wm * WM + i * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+                const int col = wn * WN + j * 32 + lr;
+                if constexpr (OUT_BF16)
+                    *reinterpret_cast<uint16_t *>(stage + row * CP + col * 2) = f32_to_bf16_rne(acc[i][j][v]);
+                else
+                    *reinterpret_cast<float *>(stage + row * CP + col * 4) = acc[i][j][v];
+            }
+    __syncthreads();
+    const int64_t zoff = tile_of(p).z * p.split_stride;
+    const int64_t ld = p.rmap.stride[0];
+    for (int id = tid; id < BM * PIECES; id += NT) {
+        const int r = id / PIECES, c = id % PIECES;
+        const int64_t m = m0 + r, n = n0 + int64_t(c) * (16 / OESZ);
+        if (m < p.M && n < p.N)
+            *reinterpret_cast<u32x4 *>(reinterpret_cast<char *>(p.C) + (zoff + m * ld + n) * OESZ) =
+                *reinterpret_cast<const u32x4 *>(stage + r * CP + c * 16);
+    }
+}
+
 // PF = register stages of global prefetch: 1 keeps the next K tile in
 // registers while the current one is multiplied; 2 keeps two (the loads of
 // tile kt + 2 are issued before tile kt is multiplied), for tiles whose K
@@ -445,7 +501,7 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
     char *sA1 = smem + BM * FP;
     char *sB0 = smem + 2 * BM * FP;
     char *sB1 = sB0 + BN * FP;
-    int64_t *roff = reinterpret_cast<int64_t *>(sB1 + BN * FP);
+    int64_t *roff = reinterpret_cast<int64_t *>(smem + fast_main_lds<BM, BN, KTB, NT, OUT_BF16>());
     int64_t *coff = roff + BM;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
@@ -634,6 +690,13 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[i][j][v] *= sc;
     }
+    if constexpr (fast_stage_fits<BM, BN, KTB, NT, OUT_BF16>()) {
+        if (p.stage_c) {
+            __syncthreads();   // every wave is done with the operand buffers
+            epilogue_lds<OUT_BF16, TM, TN, WM, WN, BM, BN, NT>(p, acc, smem, m0, n0, wm, wn, lr, lh, tid);
+            return;
+        }
+    }
     epilogue<OUT_BF16, TM, TN, WM, WN>(p, acc, roff, coff, wm, wn, lr, lh);
 }
 
@@ -723,7 +786,8 @@ enum FastId {
 
 template <typename T, bool AK, bool BK, bool OB, int BM, int BN, int WM, int WN, int KTB, int NT = 256, int PF = 1>
 int go_fast(const GemmArgs &g, const GemmParams &p, void *stream) {
-    constexpr size_t lds = size_t(2) * (BM + BN) * (KTB + 16) + size_t(BM + BN) * sizeof(int64_t);
+    constexpr size_t lds = fast_main_lds<BM, BN, KTB, NT, OB>() + size_t(BM + BN) * sizeof(int64_t);
+    static_assert(lds <= kLdsPerCu, "LDS of one workgroup");
     auto kern = gemm_fast_kernel<T, AK, BK, OB, BM, BN, WM, WN, KTB, NT, PF>;
     // above the default 64 KB of dynamic LDS: raise the limit once per kernel
     static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
@@ -857,6 +921,14 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     };
     p.vec_a = aligned(g.A, g.lda);
     p.vec_b = aligned(g.B, g.ldb);
+    {
+        const int64_t V = g.out_bf16 ? 8 : 4;   // elements per 16-byte piece
+        p.stage_c = (g.rmap.nd == 1 && g.cmap.nd == 1 && g.cmap.stride[0] == 1 && g.N % V == 0 &&
+                     g.rmap.stride[0] % V == 0 && g.split_stride % V == 0 &&
+                     reinterpret_cast<uintptr_t>(g.C) % 16 == 0)
+                        ? 1
+                        : 0;
+    }
     p.gw = 0;
     p.oscale = g.oscale;
     GemmArgs gg = g;
