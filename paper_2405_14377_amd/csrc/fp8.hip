@@ -179,22 +179,25 @@ __global__ __launch_bounds__(256) void quant_kernel(const void *__restrict__ x, 
     }
 }
 
-// quant_kernel with 16-byte loads (V elements per chunk), V-byte stores of
-// q and 16-byte stores of qt through a transposed LDS tile.  Requires x
-// 16-byte aligned, C % V == 0, q (if any) V-byte aligned with ldq % V == 0,
-// qt (if any) 16-byte aligned with ldt % 16 == 0: every chunk then lies
-// wholly inside or wholly outside each bound.
+// quant_kernel with 16-byte loads (V elements per chunk) over tiles of
+// 128 rows x 128 columns: V-byte stores of q (128-byte row segments) and
+// 16-byte stores of qt through a transposed LDS tile (128-byte segments).
+// Requires x 16-byte aligned, C % V == 0, q (if any) V-byte aligned with
+// ldq % V == 0, qt (if any) 16-byte aligned with ldt % 16 == 0: every chunk
+// then lies wholly inside or wholly outside each bound.  The grid covers
+// ceil(R' / 128) x ceil(C' / 128) tiles.
+constexpr int kQT = 128;
 template <int V>
 __global__ __launch_bounds__(256) void quant_vec_kernel(const void *__restrict__ x, int64_t R, int64_t C,
                                                         const float *__restrict__ pmax, int nb, uint8_t *__restrict__ q,
                                                         int64_t ldq, uint8_t *__restrict__ qt, int64_t ldt,
                                                         float *__restrict__ s_out, const float *pa, float *oa,
                                                         const float *pb, float *ob) {
-    constexpr int CPR = 64 / V;              // chunks per tile row
-    constexpr int NCH = 64 * CPR / 256;      // chunks per thread
+    constexpr int CPR = kQT / V;             // chunks per tile row
+    constexpr int NCH = kQT * CPR / 256;     // chunks per thread
     constexpr int ESZ = 16 / V;              // bytes per element
     __shared__ float red[4];
-    __shared__ __attribute__((aligned(16))) uint8_t tt[64][80];   // tt[c][r], 80-byte pitch
+    __shared__ __attribute__((aligned(16))) uint8_t tt[kQT][kQT + 16];   // tt[c][r]
     const int tid = threadIdx.x;
     float m = 0.f;
     for (int i = tid; i < nb; i += 256) m = fmaxf(m, pmax[i]);
@@ -207,9 +210,9 @@ __global__ __launch_bounds__(256) void quant_vec_kernel(const void *__restrict__
         if (pa && oa) *oa = 1.f / (s * *pa);
         if (pb && ob) *ob = 1.f / (s * *pb);
     }
-    const int64_t r0 = int64_t(blockIdx.x) * 64, c0 = int64_t(blockIdx.y) * 64;
+    const int64_t r0 = int64_t(blockIdx.x) * kQT, c0 = int64_t(blockIdx.y) * kQT;
     const char *xb = reinterpret_cast<const char *>(x);
-#pragma unroll
+#pragma unroll 4
     for (int i = 0; i < NCH; ++i) {
         const int id = tid + 256 * i;
         const int rr = id / CPR, ch = id % CPR;
@@ -241,10 +244,15 @@ __global__ __launch_bounds__(256) void quant_vec_kernel(const void *__restrict__
     }
     if (!qt) return;
     __syncthreads();
-    // qt rows c0 .. c0 + 63, bytes r0 .. r0 + 63: one 16-byte piece per thread
-    const int cc = tid >> 2, part = tid & 3;
-    const int64_t c = c0 + cc, r = r0 + part * 16;
-    if (c < C && r < ldt) *reinterpret_cast<u32x4 *>(qt + c * ldt + r) = *reinterpret_cast<const u32x4 *>(&tt[cc][part * 16]);
+    // qt rows c0 .. c0 + 127, bytes r0 .. r0 + 127: 8 pieces of 16 bytes per row
+#pragma unroll
+    for (int i = 0; i < kQT * 8 / 256; ++i) {
+        const int id = tid + 256 * i;
+        const int cc = id >> 3, part = id & 7;
+        const int64_t c = c0 + cc, r = r0 + part * 16;
+        if (c < C && r < ldt)
+            *reinterpret_cast<u32x4 *>(qt + c * ldt + r) = *reinterpret_cast<const u32x4 *>(&tt[cc][part * 16]);
+    }
 }
 
 }  // namespace
@@ -274,10 +282,11 @@ int launch_fp8_quant(const void *x, int dtype, int64_t R, int64_t C, float *pmax
     if (int e = int(hipGetLastError())) return e;
     const int64_t rows = qt ? std::max<int64_t>(R, ldt) : R;
     const int64_t cols = q ? std::max<int64_t>(C, ldq) : C;
-    const int64_t gx = (rows + 63) / 64, gy = (cols + 63) / 64;
+    const bool vec = xa && C % V == 0 && (!q || (al(q, V) && ldq % V == 0)) && (!qt || (al(qt, 16) && ldt % 16 == 0));
+    const int tile = vec ? kQT : 64;
+    const int64_t gx = (rows + tile - 1) / tile, gy = (cols + tile - 1) / tile;
     if (gx > 2147483647 || gy > 65535) return int(hipErrorInvalidValue);
     const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(gy), 1);
-    const bool vec = xa && C % V == 0 && (!q || (al(q, V) && ldq % V == 0)) && (!qt || (al(qt, 16) && ldt % 16 == 0));
     if (vec && V == 8)
         hipLaunchKernelGGL(quant_vec_kernel<8>, grid, dim3(256), 0, hipStream_t(stream), x, R, C, pmax, nb, q, ldq,
                            qt, ldt, s_out, pa, oa, pb, ob);

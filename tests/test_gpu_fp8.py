@@ -58,6 +58,10 @@ def _midpoints():
     ("zeros", "f32", 130, 70, 128, 256),
     ("huge", "f32", 9, 200, 256, 128),
     ("signed", "bf16", 257, 129, 256, 384),
+    # 16-byte-load path (C a multiple of the chunk) with ragged tile edges
+    ("normal", "f32", 1000, 776, 896, 1024),
+    ("normal", "bf16", 333, 136, 256, 336),
+    ("signed", "bf16", 129, 264, 264, 144),
 ])
 def test_quantize_bit_exact(case):
     kind, act, rows, cols, ldq, ldt = case
