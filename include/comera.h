@@ -23,6 +23,12 @@
  *   comera_ttm_plan      chooses a contraction order from the shape, ranks and
  *                        batch among the family of Prop. 4.1 (groups of
  *                        consecutive cores, then a sequential sweep of X).
+ *   comera_ttm_backward_masks  the backward plus dD_k, the gradients of the
+ *                        rank masks (chain rule through eq. Wcompress).
+ *   comera_ttm_plan_set_fp8    the mixed-precision layer of the appendix:
+ *                        the batch products on FP8 E4M3 codes, the
+ *                        batch-free steps in fp32; comera_fp8_quantize is
+ *                        its quantiser.
  *
  * Conventions shared by every call:
  *   - X, Y, dY, dX are row-major [b, N] in the activation dtype of the plan
@@ -35,9 +41,10 @@
  *   - Host-detectable argument errors return a negative status before any
  *     launch; a failed launch returns COMERA_ERR_HIP.  No C++ exception
  *     crosses this boundary.
- *   - The plan is a host object owned by the library, immutable after
- *     creation; it may be used from several streams if each stream has its
- *     own workspace.
+ *   - The plan is a host object owned by the library.  Only the
+ *     comera_ttm_plan_set_* calls change it (host only; not concurrently
+ *     with other calls on the same plan); otherwise it may be used from
+ *     several streams if each stream has its own workspace.
  */
 #ifndef COMERA_H
 #define COMERA_H
