@@ -68,14 +68,15 @@ __device__ __forceinline__ float chunk_absmax(const u32x4 v) {
 
 // The same maxima with 16-byte loads, four in flight per thread; x 16-byte
 // aligned.  Elements past the last whole chunk are taken by workgroup 0.
+constexpr int kAmaxThreads = 1024;   // 512 workgroups of 16 waves fill every SIMD
 template <int V>
-__global__ __launch_bounds__(512) void amax_vec_kernel(const void *__restrict__ x, int dtype, int64_t n,
-                                                       float *__restrict__ pmax) {
-    __shared__ float red[8];
+__global__ __launch_bounds__(kAmaxThreads) void amax_vec_kernel(const void *__restrict__ x, int dtype, int64_t n,
+                                                                float *__restrict__ pmax) {
+    __shared__ float red[kAmaxThreads / 64];
     const u32x4 *xv = reinterpret_cast<const u32x4 *>(x);
     const int64_t nv = n / V;
-    const int64_t stride = int64_t(gridDim.x) * 512;
-    int64_t i = int64_t(blockIdx.x) * 512 + threadIdx.x;
+    const int64_t stride = int64_t(gridDim.x) * kAmaxThreads;
+    int64_t i = int64_t(blockIdx.x) * kAmaxThreads + threadIdx.x;
     float m = 0.f;
     for (; i + 3 * stride < nv; i += 4 * stride) {
         const u32x4 a = xv[i], b = xv[i + stride], c = xv[i + 2 * stride], d = xv[i + 3 * stride];
@@ -84,13 +85,13 @@ __global__ __launch_bounds__(512) void amax_vec_kernel(const void *__restrict__ 
     }
     for (; i < nv; i += stride) m = fmaxf(m, chunk_absmax<V>(xv[i]));
     if (blockIdx.x == 0)
-        for (int64_t j = nv * V + threadIdx.x; j < n; j += 512) m = fmaxf(m, fabsf(load_act(x, dtype, j)));
+        for (int64_t j = nv * V + threadIdx.x; j < n; j += kAmaxThreads) m = fmaxf(m, fabsf(load_act(x, dtype, j)));
     m = wave_max(m);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
     __syncthreads();
     if (threadIdx.x == 0) {
         float r = red[0];
-        for (int w = 1; w < 8; ++w) r = fmaxf(r, red[w]);
+        for (int w = 1; w < kAmaxThreads / 64; ++w) r = fmaxf(r, red[w]);
         pmax[blockIdx.x] = r;
     }
 }
@@ -270,11 +271,15 @@ int launch_fp8_quant(const void *x, int dtype, int64_t R, int64_t C, float *pmax
     const bool xa = al(x, 16);
     int nb;
     if (xa) {
-        nb = int(std::min<int64_t>(kAmaxBlocks, std::max<int64_t>(1, (n / V + 2047) / 2048)));
+        // at least four 16-byte loads per thread
+        const int64_t per = int64_t(kAmaxThreads) * 4;
+        nb = int(std::min<int64_t>(kAmaxBlocks, std::max<int64_t>(1, (n / V + per - 1) / per)));
         if (V == 8)
-            hipLaunchKernelGGL(amax_vec_kernel<8>, dim3(nb), dim3(512), 0, hipStream_t(stream), x, dtype, n, pmax);
+            hipLaunchKernelGGL(amax_vec_kernel<8>, dim3(nb), dim3(kAmaxThreads), 0, hipStream_t(stream), x, dtype, n,
+                               pmax);
         else
-            hipLaunchKernelGGL(amax_vec_kernel<4>, dim3(nb), dim3(512), 0, hipStream_t(stream), x, dtype, n, pmax);
+            hipLaunchKernelGGL(amax_vec_kernel<4>, dim3(nb), dim3(kAmaxThreads), 0, hipStream_t(stream), x, dtype, n,
+                               pmax);
     } else {
         nb = int(std::min<int64_t>(kAmaxBlocks, (n + 255) / 256));
         hipLaunchKernelGGL(amax_partial_kernel, dim3(nb), dim3(256), 0, hipStream_t(stream), x, dtype, n, pmax);
