@@ -445,16 +445,19 @@ constexpr bool fast_stage_fits() {
     return size_t(BM) * (BN * (OB ? 2 : 4) + 16) <= fast_main_lds<BM, BN, KTB, NT, OB>();
 }
 
-// Row-major output through LDS: the accumulators are written into a
-// BM x BN tile in LDS (16 bytes of padding per row), then every thread
-// stores 16-byte pieces of whole rows, so each output row leaves as
-// contiguous segments instead of 2- or 4-byte scattered stores.  Requires
-// (p.stage_c) linear row and column maps with unit column stride, N, the
-// row stride and the split stride multiples of the 16-byte piece, and C
-// 16-byte aligned.
+// Output through LDS: the accumulators are written into a BM x BN tile in
+// LDS (16 bytes of padding per row), then every thread stores 16-byte
+// pieces of its rows, so the output leaves as contiguous segments instead
+// of 2- or 4-byte scattered stores.  Requires (p.stage_c) that every piece
+// of 16 bytes / element size consecutive columns starting at a multiple of
+// that count is contiguous and aligned in memory: unit innermost column
+// stride, an innermost column radix that the piece divides, every other
+// stride, N and the split stride multiples of the piece, and C 16-byte
+// aligned.  Offsets come from the row and column tables (-1 = outside).
 template <bool OUT_BF16, int TM, int TN, int WM, int WN, int BM, int BN, int NT>
 __device__ __forceinline__ void epilogue_lds(const GemmParams &p, const f32x16 (&acc)[TM][TN], char *stage,
-                                             int64_t m0, int64_t n0, int wm, int wn, int lr, int lh, int tid) {
+                                             const int64_t *roff, const int64_t *coff, int wm, int wn, int lr,
+                                             int lh, int tid) {
     constexpr int OESZ = OUT_BF16 ? 2 : 4;
     constexpr int CP = BN * OESZ + 16;
     constexpr int PIECES = BN * OESZ / 16;
@@ -473,12 +476,11 @@ __device__ __forceinline__ void epilogue_lds(const GemmParams &p, const f32x16 (
             }
     __syncthreads();
     const int64_t zoff = tile_of(p).z * p.split_stride;
-    const int64_t ld = p.rmap.stride[0];
     for (int id = tid; id < BM * PIECES; id += NT) {
         const int r = id / PIECES, c = id % PIECES;
-        const int64_t m = m0 + r, n = n0 + int64_t(c) * (16 / OESZ);
-        if (m < p.M && n < p.N)
-            *reinterpret_cast<u32x4 *>(reinterpret_cast<char *>(p.C) + (zoff + m * ld + n) * OESZ) =
+        const int64_t ro = roff[r], co = coff[c * (16 / OESZ)];
+        if (ro >= 0 && co >= 0)
+            *reinterpret_cast<u32x4 *>(reinterpret_cast<char *>(p.C) + (zoff + ro + co) * OESZ) =
                 *reinterpret_cast<const u32x4 *>(stage + r * CP + c * 16);
     }
 }
@@ -693,7 +695,7 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
     if constexpr (fast_stage_fits<BM, BN, KTB, NT, OUT_BF16>()) {
         if (p.stage_c) {
             __syncthreads();   // every wave is done with the operand buffers
-            epilogue_lds<OUT_BF16, TM, TN, WM, WN, BM, BN, NT>(p, acc, smem, m0, n0, wm, wn, lr, lh, tid);
+            epilogue_lds<OUT_BF16, TM, TN, WM, WN, BM, BN, NT>(p, acc, smem, roff, coff, wm, wn, lr, lh, tid);
             return;
         }
     }
@@ -922,12 +924,15 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     p.vec_a = aligned(g.A, g.lda);
     p.vec_b = aligned(g.B, g.ldb);
     {
+        // pieces of V consecutive output columns must be contiguous and aligned
         const int64_t V = g.out_bf16 ? 8 : 4;   // elements per 16-byte piece
-        p.stage_c = (g.rmap.nd == 1 && g.cmap.nd == 1 && g.cmap.stride[0] == 1 && g.N % V == 0 &&
-                     g.rmap.stride[0] % V == 0 && g.split_stride % V == 0 &&
-                     reinterpret_cast<uintptr_t>(g.C) % 16 == 0)
-                        ? 1
-                        : 0;
+        bool ok = g.rmap.nd >= 1 && g.cmap.nd >= 1 && g.N % V == 0 && g.split_stride % V == 0 &&
+                  reinterpret_cast<uintptr_t>(g.C) % 16 == 0;
+        for (int k = 0; k < g.rmap.nd; ++k) ok = ok && g.rmap.stride[k] % V == 0;
+        const int in = g.cmap.nd - 1;
+        for (int k = 0; k < in; ++k) ok = ok && g.cmap.stride[k] % V == 0;
+        ok = ok && in >= 0 && g.cmap.stride[in] == 1 && (in == 0 || g.cmap.radix[in] % V == 0);
+        p.stage_c = ok ? 1 : 0;
     }
     p.gw = 0;
     p.oscale = g.oscale;
