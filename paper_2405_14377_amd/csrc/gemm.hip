@@ -10,15 +10,18 @@
 // straight from an interleaved core product, and the blocked intermediates of
 // the gradient projections.
 //
-// Four waves per workgroup; each wave owns a WM x WN block made of 32 x 32
-// MFMA tiles (bf16: v_mfma_f32_32x32x16_bf16, fp32: v_mfma_f32_32x32x2f32).
-// Both operand tiles are staged in LDS as rows of K (k contiguous), double
-// buffered; operands whose k is strided in memory are transposed in
-// registers on the way in.  A general kernel (64-byte K rows, bounds-checked
-// loads) handles any shape; a fast kernel takes over when all accesses are
-// in bounds by construction.  Lanes read 16-byte vectors from
-// LDS; the k slots fed to successive MFMAs are one fixed permutation of the
-// tile's k range, shared by A and B, so the sum is unchanged.
+// Four or eight waves per workgroup; each wave owns a WM x WN block made of
+// 32 x 32 MFMA tiles (bf16: v_mfma_f32_32x32x16_bf16, fp32:
+// v_mfma_f32_32x32x2f32, FP8 E4M3: v_mfma_scale_f32_32x32x64_f8f6f4 with
+// unit block scales).  Both operand tiles are staged in LDS as rows of K
+// (k contiguous), double buffered; operands whose k is strided in memory are
+// transposed in registers on the way in.  A general kernel (64-byte K rows,
+// bounds-checked loads) handles any shape; a fast kernel takes over when all
+// accesses are in bounds by construction, and writes outputs whose 16-byte
+// column pieces are contiguous through an LDS-staged tile.  Lanes read
+// 16-byte vectors from LDS; the k slots fed to successive MFMAs are one fixed
+// permutation of the tile's k range, shared by A and B, so the sum is
+// unchanged.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
