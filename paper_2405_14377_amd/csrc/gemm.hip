@@ -832,6 +832,14 @@ int launch_fast(const GemmArgs &g, const GemmParams &p, int id, void *stream) {
 // take 64-byte rows.  Returns -1 when the product is too small to fill the
 // chip with these tiles (the general kernel's smaller tiles do better).
 int pick_fast(const GemmArgs &g, int splits) {
+    // transposed operands with a side of 64 or less (the meets of the paper's
+    // TT layout) stream the token rows: these tiles would mostly compute
+    // padding, the general kernel's 32-wide skinny tiles do better
+    if (!g.a_kc && !g.b_kc && (g.M <= 64 || g.N <= 64) && g.dtype != kDtypeFp8) return -1;
+    // K-contiguous operands with a side of 64 or less: the tile whose short
+    // side is 64
+    if (g.a_kc && g.b_kc && std::min(g.M, g.N) <= 64 && g.dtype != kDtypeFp8)
+        return g.N <= 64 ? F128x64_128 : F64x128_128;
     const int64_t t128 = ceil_div(g.M, 128) * ceil_div(g.N, 128) * splits;
     const int64_t t256 = ceil_div(g.M, 256) * ceil_div(g.N, 256) * splits;
     // bf16: 256 x 256 tiles of eight waves once they give two or more
@@ -858,6 +866,12 @@ int pick_fast(const GemmArgs &g, int splits) {
 // Whether every 16-byte access of the fast kernel stays inside the operand:
 // 16-byte aligned rows, whole K tiles in every split, row groups that divide
 // the row count of transposed operands, and byte offsets within 32 bits.
+bool fast_ok_k(const GemmArgs &g, int64_t kchunk, int ktb) {
+    const int64_t sz = g.dtype == COMERA_BF16 ? 2 : (g.dtype == kDtypeFp8 ? 1 : 4);
+    const int64_t kt = ktb / sz;
+    return g.K % kt == 0 && kchunk % kt == 0;
+}
+
 bool fast_ok(const GemmArgs &g, int64_t kchunk, int ktb) {
     const int64_t sz = g.dtype == COMERA_BF16 ? 2 : (g.dtype == kDtypeFp8 ? 1 : 4);
     const int64_t kt = ktb / sz;
@@ -873,6 +887,13 @@ bool fast_ok(const GemmArgs &g, int64_t kchunk, int ktb) {
 
 int gemm_auto_splits(int64_t M, int64_t N, int64_t K) {
     const int64_t tiles = ceil_div(M, 64) * ceil_div(N, 64);
+    // a side of 64 or less with a long K streams the other operand through a
+    // few hundred 128-row tiles: split K until about 1024 workgroups load at once
+    if (std::min(M, N) <= 64 && K >= 2048) {
+        const int64_t t = ceil_div(std::max(M, N), 128);
+        if (t < 1024) return int(std::max<int64_t>(1, std::min<int64_t>(ceil_div(1024, t), std::min<int64_t>(K / 512, 8))));
+        return 1;
+    }
     if (tiles >= 256 || K < 128) return 1;
     int64_t s = ceil_div(1024, tiles);
     s = std::min<int64_t>(s, K / 64);
@@ -927,13 +948,16 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     p.vec_a = aligned(g.A, g.lda);
     p.vec_b = aligned(g.B, g.ldb);
     {
-        // pieces of V consecutive output columns must be contiguous and aligned
+        // pieces of V consecutive output columns must be contiguous and
+        // aligned; digits of radix 1 (always 0) do not matter
         const int64_t V = g.out_bf16 ? 8 : 4;   // elements per 16-byte piece
+        auto live = [](const Remap &r, int k) { return k == 0 || r.radix[k] > 1; };
         bool ok = g.rmap.nd >= 1 && g.cmap.nd >= 1 && g.N % V == 0 && g.split_stride % V == 0 &&
                   reinterpret_cast<uintptr_t>(g.C) % 16 == 0;
-        for (int k = 0; k < g.rmap.nd; ++k) ok = ok && g.rmap.stride[k] % V == 0;
-        const int in = g.cmap.nd - 1;
-        for (int k = 0; k < in; ++k) ok = ok && g.cmap.stride[k] % V == 0;
+        for (int k = 0; k < g.rmap.nd; ++k) ok = ok && (!live(g.rmap, k) || g.rmap.stride[k] % V == 0);
+        int in = g.cmap.nd - 1;                  // innermost live column digit
+        while (in > 0 && !live(g.cmap, in)) --in;
+        for (int k = 0; k < in; ++k) ok = ok && (!live(g.cmap, k) || g.cmap.stride[k] % V == 0);
         ok = ok && in >= 0 && g.cmap.stride[in] == 1 && (in == 0 || g.cmap.radix[in] % V == 0);
         p.stage_c = ok ? 1 : 0;
     }
@@ -951,7 +975,16 @@ int launch_gemm(const GemmArgs &g, void *stream) {
 
         const int64_t kt = ktb / esz;
         pf.kchunk = ceil_div(p.kchunk, kt) * kt;
-        if (!fast_ok(gg, pf.kchunk, ktb)) fast = -1;
+        if (!fast_ok(gg, pf.kchunk, ktb)) {
+            // a K that is a multiple of the 64-byte K row but not of the
+            // 128-byte one keeps a fast 128 x 128 tile on 64-byte rows
+            fast = -1;
+            if (ktb == 128 && g.dtype != COMERA_F32 && (fast_ok_k(gg, p.kchunk, 64))) {
+                fast = F128x128_64;
+                pf.kchunk = ceil_div(p.kchunk, 64 / esz) * (64 / esz);
+                if (!fast_ok(gg, pf.kchunk, 64)) fast = -1;
+            }
+        }
     }
     const int tile = g.tile >= 0 ? g.tile : pick_tile(g.M, g.N, gg.splits);
 #define COMERA_GEMM_CASE(T, AK, BK, OB)                                                    \

@@ -257,6 +257,13 @@ void layout_dense(comera_ttm_plan_s *p, bool with_dx) {
             }
         }
     }
+    // a side of 64 or less (the meets of the paper's TT layout): the product
+    // only streams the token rows, so about 1024 workgroups of the skinny
+    // 32 x 128 tiles keep enough loads in flight
+    if (std::min(p->N_in, p->N_out) <= 64 && !p->fp8) {
+        const int64_t st = ((std::min(p->N_in, p->N_out) + 31) / 32) * ((std::max(p->N_in, p->N_out) + 127) / 128);
+        splits = std::max<int64_t>(splits, (1024 + st - 1) / st);
+    }
     splits = std::min<int64_t>(splits, std::max<int64_t>(1, b / 256));
     splits = std::min<int64_t>(splits, 64);
     int64_t kchunk = (b + splits - 1) / splits;
