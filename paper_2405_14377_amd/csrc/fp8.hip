@@ -7,12 +7,16 @@
 // the fp32 values; the clamp keeps s and 1 / (s s') finite and nonzero in
 // fp32.
 //
-//   amax_partial_kernel   max |x| per workgroup (no atomics, no clearing)
-//   quant_kernel          max of the partials -> s; codes of x (row-major,
+//   amax_vec_kernel       max |x| per workgroup with 16-byte loads (no
+//                         atomics, no clearing); amax_partial_kernel for
+//                         unaligned x
+//   quant_vec_kernel      max of the partials -> s; codes of x (row-major,
 //                         rows padded with zero codes to ldq) and / or of
-//                         x^T (rows padded with zero codes to ldt); workgroup
-//                         0 also writes s and the products 1 / (s * s_partner)
-//                         that scale GEMM results
+//                         x^T (rows padded with zero codes to ldt), 128 x 128
+//                         tiles; workgroup 0 also writes s and the products
+//                         1 / (s * s_partner) that scale GEMM results;
+//                         quant_kernel does the same for shapes the 16-byte
+//                         path does not cover
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
