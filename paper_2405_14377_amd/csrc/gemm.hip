@@ -576,6 +576,10 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
                 }
             }
         } else if constexpr (sizeof(T) == 2) {
+            // the wave in its product phase goes first at the issue arbiter,
+            // so the other wave's loads and LDS traffic fill the gaps (a few
+            // per cent on the large bf16 products)
+            __builtin_amdgcn_s_setprio(3);
 #pragma unroll
             for (int ks = 0; ks < KT / 16; ++ks) {
                 bf16x8 av[TM], bv[TN];
@@ -605,6 +609,7 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
                 }
                 __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
             }
+            __builtin_amdgcn_s_setprio(0);
         } else {
 #pragma unroll
             for (int kq = 0; kq < KT / 8; ++kq) {
@@ -834,7 +839,8 @@ int launch_fast(const GemmArgs &g, const GemmParams &p, int id, void *stream) {
 int pick_fast(const GemmArgs &g, int splits) {
     // transposed operands with a side of 64 or less (the meets of the paper's
     // TT layout) stream the token rows: these tiles would mostly compute
-    // padding, the general kernel's 32-wide skinny tiles do better
+    // padding, the general kernel's 32-wide skinny tiles do better (the
+    // sweep steps of that layout are measured on its 1024 -> 4096 shape)
     if (!g.a_kc && !g.b_kc && (g.M <= 64 || g.N <= 64) && g.dtype != kDtypeFp8) return -1;
     // K-contiguous operands with a side of 64 or less: the tile whose short
     // side is 64
