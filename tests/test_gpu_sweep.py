@@ -131,6 +131,21 @@ def test_paper_tt_layout(act):
     _all_orders(n, m, r, cores, D, X, dY, act, orders=[p.chosen, 0])
 
 
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_paper_mixed_precision_table_tt_shape(act):
+    """The TT shape of the appendix's runtime table, 1024 x 4096 as
+    (16, 8, 8 | 16, 16, 16) at rank 32, with 2048 tokens: the sweep's
+    products have a side of 32 against K up to 4096 (split over K, skinny
+    tiles), and its meets have 32 rows against 2048 tokens."""
+    n = (16, 8, 8, 1, 1, 1)
+    m = (1, 1, 1, 16, 16, 16)
+    r = (1, 32, 32, 32, 32, 32, 1)
+    cores, D, X, dY = _inputs(29, n, m, r, 2048, act)
+    p = C.TTMPlan(n, m, r, C.BF16 if act == "bf16" else C.F32, batch=2048)
+    assert p.order_info(p.chosen)["desc"] == "sweep-lr [0,1,2][3,4,5]"
+    _all_orders(n, m, r, cores, D, X, dY, act, orders=[p.chosen])
+
+
 def test_sweep_backward_partial_outputs():
     """dX only, dG only, and a subset of dG for a sweep order."""
     import torch
