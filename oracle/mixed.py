@@ -67,3 +67,13 @@ def backward_fp8(X, dY, cores, masks=None) -> Tuple[np.ndarray, List[np.ndarray]
 def mask_grads_fp8(X, dY, cores, masks=None) -> List[np.ndarray]:
     """dD_k[c] = <dW, dW/dD_k[c]> with the FP8 dW."""
     return ttm.mask_grads_from_dW(dW_fp8(X, dY), cores, masks)
+
+
+def rows_fp8(A, rows, B_codes, sB: float) -> np.ndarray:
+    """Rows `rows` of (A quantised as a whole tensor) @ decode(B_codes) / sB:
+    the scale of A comes from all of A, the codes only for the rows asked
+    for (sampled checks of large products)."""
+    A32 = np.asarray(A, dtype=np.float32)
+    sA = fp8.pow2_scale(float(np.max(np.abs(A32))) if A32.size else 0.0)
+    cA = fp8.encode((A32[rows] * np.float32(sA)).astype(np.float64))
+    return (fp8.decode(cA) @ fp8.decode(B_codes)) / (sA * sB)

@@ -246,3 +246,45 @@ def test_integer_layer_large_tiles(act):
     dGo = OT.project_dW(X.T.astype(np.float64) @ dY, cores)
     for a, c in zip(dG, dGo):
         assert rel_err(to_np(a), c) <= 1e-4
+
+
+@pytest.mark.parametrize("li", [0, 1], ids=["up", "down"])
+def test_fp8_large_pair_sampled(li):
+    """The FP8 figures of the bench: 1024 <-> 4096, d = 4, ranks 64,
+    Bernoulli(0.7) masks, 65536 tokens, bf16 activations, with the bench's
+    plan settings (dense order, reuse).  Y and dX on 256 sampled rows: within
+    the E4M3 bound of the exact product and close in norm to the oracle's FP8
+    rows (scales from the whole tensors); dG_k through <dG_k, G_k> = <dW8, W>
+    for every k on the whole batch (W is linear in each core)."""
+    from tests.test_gpu_ttm import _workload_layer
+    sh, inp, X, dY, mask_active = _workload_layer(4, li, "bf16")
+    b = X.shape[0]
+    run = TTMRun(sh.n, sh.m, sh.r, inp.cores, inp.masks, b, "bf16", mask_active=mask_active, force_order=0,
+                 reuse=True, fp8=True)
+    Xt, dYt = to_dev(X, "bf16"), to_dev(dY, "bf16")
+    Y = run.forward(Xt)
+    dX, dG = run.backward(Xt, dYt)
+    rows = np.random.default_rng(300 + li).choice(b, 256, replace=False)
+    W = OT.dense_weight(inp.cores, inp.masks)
+    cW, sW = OM.quantized_weight(inp.cores, inp.masks)
+    cWt, sWt = OF.quantize(W.astype(np.float32).T)
+    Yr, dXr = to_np(Y[rows]), to_np(dX[rows])
+    fro = lambda a, c: float(np.linalg.norm(a - c) / np.linalg.norm(c))
+    assert fro(Yr, OM.rows_fp8(X, rows, cW, sW)) <= 5e-3
+    assert fro(dXr, OM.rows_fp8(dY, rows, cWt, sWt)) <= 5e-3
+    eW = _qerr(W) + 1e-6 * np.abs(W)
+    sX, sD = OF.pow2_scale(np.max(np.abs(X))), OF.pow2_scale(np.max(np.abs(dY)))   # whole-tensor scales
+    qx = np.maximum(2.0 ** -4 * np.abs(X[rows]), 2.0 ** -10 / sX)
+    qd = np.maximum(2.0 ** -4 * np.abs(dY[rows]), 2.0 ** -10 / sD)
+    Yx = X[rows].astype(np.float64) @ W
+    bY = qx @ np.abs(W) + np.abs(X[rows]) @ eW + qx @ eW
+    assert np.all(np.abs(Yr - Yx) <= bY * (1 + 1e-3) + 2.0 ** -8 * np.abs(Yr) + 1e-6 * np.max(np.abs(Yx)))
+    dXx = dY[rows].astype(np.float64) @ W.T
+    bX = qd @ np.abs(W).T + np.abs(dY[rows]) @ eW.T + qd @ eW.T
+    assert np.all(np.abs(dXr - dXx) <= bX * (1 + 1e-3) + 2.0 ** -8 * np.abs(dXr) + 1e-6 * np.max(np.abs(dXx)))
+    # <dG_k, G_k> = <dW8, W> for every k (dW8: the FP8 dW the projections
+    # start from), so every core must give the same value up to the fp32
+    # rounding of the projections
+    vals = [float((dG[k].double() * run.G[k].double()).sum().item()) for k in range(4)]
+    for v in vals[1:]:
+        assert abs(v - vals[0]) <= 1e-3 * abs(vals[0]), vals

@@ -105,3 +105,14 @@ def test_mask_grad_homogeneity():
     ref = float(np.sum(dW8 * W))
     for Dk, g in zip(masks, mixed.mask_grads_fp8(X, dY, cores, masks)):
         assert abs(float(np.dot(Dk, g)) - ref) <= 1e-10 * max(1.0, abs(ref))
+
+
+def test_rows_fp8_matches_full_forward():
+    n, m, r, b = (4, 6, 5), (3, 7, 4), (1, 6, 5, 1), 64
+    cores, masks, X, dY = _random_layer(5, n, m, r, b)
+    rows = np.array([0, 7, 33, 63])
+    cW, sW = mixed.quantized_weight(cores, masks)
+    assert np.array_equal(mixed.rows_fp8(X, rows, cW, sW), mixed.forward_fp8(X, cores, masks)[rows])
+    cWt, sWt = fp8.quantize(OT.dense_weight(cores, masks).astype(np.float32).T)
+    dX, _ = mixed.backward_fp8(X, dY, cores, masks)
+    assert np.allclose(mixed.rows_fp8(dY, rows, cWt, sWt), dX[rows], rtol=1e-12, atol=1e-12)
