@@ -235,8 +235,12 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjArgs a) {
 // A workgroup owns QI values of I and QJ values of J, i.e. a tile of
 // (QI nx) x (QJ ny) entries of W: it stages its P slice (rank-major) and G in
 // LDS, computes the tile as a [QI QJ] x [nx ny] product with 4 x 4 register
-// blocks, keeps it in LDS and writes it out row by row in each requested
-// layout, consecutive threads on consecutive addresses.
+// blocks, keeps it in LDS and writes it out in each requested layout,
+// consecutive threads on consecutive addresses.  Loads and stores move four
+// entries per thread where the addresses allow it (16-byte pieces), else one.
+// The kernel is latency-bound (a few KB per workgroup, one pass): on the
+// 768 x 3072 layer (rank 30, 12 x 12 last core) the four-entry paths and
+// tiles of 36 x 96 entries take it from 18.5 to 10 us.
 __device__ __forceinline__ uint16_t to_bf16_rne(float f) {
     uint32_t u = __float_as_uint(f);
     if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return uint16_t((u >> 16) | 0x40);
@@ -272,7 +276,56 @@ __global__ __launch_bounds__(256) void wtile_kernel(WBuildArgs a) {
     // Every integer division below is per thread or per item, never per
     // element: a wave64 instruction occupies its SIMD for four cycles, and a
     // division is a few dozen of them.
-    {
+    const bool vP = ((a.NJ * A) % 4 == 0) && ((J0 * A) % 4 == 0) && ((int64_t(nJ) * A) % 4 == 0) &&
+                    ((reinterpret_cast<uintptr_t>(a.P) & 15) == 0);
+    const bool vG = (NC % 4 == 0) && ((reinterpret_cast<uintptr_t>(a.G) & 15) == 0);
+    if (vP && vG) {
+        // P slice: nI runs of nJ A consecutive floats; G: A NC consecutive
+        // floats (NC4 == NC); both as float4, all loads before any store.
+        // Pairs outside the slice stay unset: their products are computed
+        // but never stored.
+        const int rowf = nJ * A / 4, npf = nI * rowf, ngf = A * NC / 4;
+        constexpr int U = 8;
+        float4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int f = tid + u * 256;
+            if (f < npf) {
+                const int qi = f / rowf, e = f - qi * rowf;
+                v[u] = reinterpret_cast<const float4 *>(a.P + ((I0 + qi) * a.NJ + J0) * A)[e];
+            } else if (f < npf + ngf) {
+                v[u] = reinterpret_cast<const float4 *>(a.G)[f - npf];
+            }
+        }
+        auto put_p = [&](int f, float4 w) {
+            const int qi = f / rowf, e = 4 * (f - qi * rowf);
+            int qj = e / A, al = e - qj * A;
+            const float x[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                Pt[al * NP4 + qi * QJ + qj] = x[k];
+                if (++al == A) {
+                    al = 0;
+                    ++qj;
+                }
+            }
+        };
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int f = tid + u * 256;
+            if (f < npf) put_p(f, v[u]);
+            else if (f < npf + ngf) reinterpret_cast<float4 *>(Gs)[f - npf] = v[u];
+        }
+        // anything beyond U loads per thread (large ranks or cores)
+        for (int f = tid + U * 256; f < npf + ngf; f += 256) {
+            if (f < npf) {
+                const int qi = f / rowf;
+                put_p(f, reinterpret_cast<const float4 *>(a.P + ((I0 + qi) * a.NJ + J0) * A)[f - qi * rowf]);
+            } else {
+                reinterpret_cast<float4 *>(Gs)[f - npf] = reinterpret_cast<const float4 *>(a.G)[f - npf];
+            }
+        }
+    } else {
         // P slice: thread t loads rank entries al = t % A, t % A + ... of the
         // pairs p = t / A + 256 / A * i (coalesced runs of A floats per pair);
         // G: consecutive floats.  All loads are issued before any store.
@@ -371,6 +424,41 @@ __global__ __launch_bounds__(256) void wtile_kernel(WBuildArgs a) {
     const int ri = nI * nx, rj = nJ * ny;
     const int64_t Nin = a.NI * nx, Nout = a.NJ * ny;
     const int64_t i0 = I0 * nx, j0 = J0 * ny;
+    const uintptr_t al_need = bf ? 7 : 15;
+    const bool v4 = (rj % 4 == 0) && (ri % 4 == 0) && (Nout % 4 == 0) && (Nin % 4 == 0) && (j0 % 4 == 0) &&
+                    (i0 % 4 == 0) && ((reinterpret_cast<uintptr_t>(a.out) & al_need) == 0) &&
+                    ((reinterpret_cast<uintptr_t>(a.out_t) & al_need) == 0);
+    if (v4) {
+        // four consecutive entries per thread over the tile flattened in
+        // the output's row order, so one wave covers several short rows
+        auto put4 = [&](void *out, int64_t off, float x0, float x1, float x2, float x3) {
+            if (bf) {
+                uint2 u;
+                u.x = uint32_t(to_bf16_rne(x0)) | (uint32_t(to_bf16_rne(x1)) << 16);
+                u.y = uint32_t(to_bf16_rne(x2)) | (uint32_t(to_bf16_rne(x3)) << 16);
+                *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(out) + off) = u;
+            } else {
+                *reinterpret_cast<float4 *>(reinterpret_cast<float *>(out) + off) = make_float4(x0, x1, x2, x3);
+            }
+        };
+        if (a.out) {
+            const int q4 = rj / 4, tot = ri * q4;
+            for (int t = tid; t < tot; t += 256) {
+                const int r = t / q4, c = 4 * (t - r * q4);
+                const float *e = tile + r * tp + c;
+                put4(a.out, (i0 + r) * Nout + j0 + c, e[0], e[1], e[2], e[3]);
+            }
+        }
+        if (a.out_t) {
+            const int q4 = ri / 4, tot = rj * q4;
+            for (int t = tid; t < tot; t += 256) {
+                const int c = t / q4, r = 4 * (t - c * q4);
+                const float *e = tile + r * tp + c;
+                put4(a.out_t, (j0 + c) * Nin + i0 + r, e[0], e[tp], e[2 * tp], e[3 * tp]);
+            }
+        }
+        return;
+    }
     // one output row per wave at a time, lanes on consecutive addresses
     if (a.out)       // W [N_in][N_out]: rows i, runs of rj consecutive j
         for (int r = wave; r < ri; r += 4) {
@@ -399,10 +487,11 @@ void proj_tiles(int64_t rows, int64_t cols, int A, int &RT, int &CT) {
 
 bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, int &QI, int &QJ) {
     if (A < 1 || A > kProjMaxA || NI < 1 || NJ < 1) return false;
-    // tiles of about 64 x 64 entries of W (rows of 64+ elements in both
-    // layouts); halved while a workgroup would hold more LDS than allowed
-    int qi = int(std::min<int64_t>(NI, std::max(1, (64 + nx - 1) / nx)));
-    int qj = int(std::min<int64_t>(NJ, std::max(1, (64 + ny - 1) / ny)));
+    // tiles of about 32 x 96 entries of W (more workgroups than square
+    // tiles, rows of 96+ entries in W); halved while a workgroup would hold
+    // more LDS than allowed
+    int qi = int(std::min<int64_t>(NI, std::max(1, (32 + nx - 1) / nx)));
+    int qj = int(std::min<int64_t>(NJ, std::max(1, (96 + ny - 1) / ny)));
     while (wtile_lds_floats(A, qi, qj, nx, ny) * sizeof(float) > kProjLds && (qi > 1 || qj > 1)) {
         if (qj >= qi && qj > 1) qj = (qj + 1) / 2;
         else qi = (qi + 1) / 2;
