@@ -51,8 +51,9 @@ __host__ __device__ inline size_t proj_lds_floats(int RT, int CT, int A) {
     return size_t(RT) * (CT4 + 4) + size_t(A4) * (CT4 + 4) + size_t(RT) * (A4 + 4) + size_t(round4(2 * RT));
 }
 
+// Two 1024-thread workgroups per CU: eight waves per SIMD, <= 64 registers.
 template <int kProjThreads>
-__global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjArgs a) {
+__global__ __launch_bounds__(kProjThreads, kProjThreads == 1024 ? 8 : 1) void proj_kernel(ProjArgs a) {
     extern __shared__ __attribute__((aligned(16))) float sm[];
     const int RT = a.RT, CT = a.CT, A = a.A;
     const int CT4 = round4(CT), A4 = round4(A);
@@ -68,38 +69,40 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjArgs a) {
         for (int r = tid; r < nr; r += kProjThreads) roff_s[r] = remap_off(a.rmap, r0 + r);
 
     // E_{k+1} tile, split slices summed in slice order; zero padding.  Each
-    // thread keeps 4 x 4 float4 loads (four vectors of four slices) in
-    // flight before adding them.
+    // thread keeps eight float4 loads in flight before adding them (one
+    // vector of eight slices with 1024 threads, two vectors of four with
+    // 256): 32 registers, so that two 1024-thread workgroups fit on a CU.
     const bool vec = (a.cols % 4 == 0) && (CT % 4 == 0) && (a.in_stride % 4 == 0) &&
                      (reinterpret_cast<uintptr_t>(a.En) % 16 == 0);
     if (vec) {
+        constexpr int JV = kProjThreads == 1024 ? 1 : 2, SS = kProjThreads == 1024 ? 8 : 4;
         const int q4 = CT4 / 4, n4 = RT * q4;
-        for (int jb = 0; jb * kProjThreads < n4; jb += 4) {
-            float4 v[4];
-            int ri[4], ci[4];
-            bool ok[4];
+        for (int jb = 0; jb * kProjThreads < n4; jb += JV) {
+            float4 v[JV];
+            int ri[JV], ci[JV];
+            bool ok[JV];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < JV; ++j) {
                 const int i = tid + kProjThreads * (jb + j);
                 ri[j] = i / q4;
                 ci[j] = (i - ri[j] * q4) * 4;
                 ok[j] = i < n4 && ri[j] < nr && ci[j] < nc;
                 v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
             }
-            for (int s0 = 0; s0 < a.nin; s0 += 4) {
-                float4 x[4][4];
+            for (int s0 = 0; s0 < a.nin; s0 += SS) {
+                float4 x[SS][JV];
 #pragma unroll
-                for (int ss = 0; ss < 4; ++ss)
+                for (int ss = 0; ss < SS; ++ss)
 #pragma unroll
-                    for (int j = 0; j < 4; ++j)
+                    for (int j = 0; j < JV; ++j)
                         x[ss][j] = (ok[j] && s0 + ss < a.nin)
                                        ? *reinterpret_cast<const float4 *>(a.En + (s0 + ss) * a.in_stride +
                                                                            (r0 + ri[j]) * a.cols + c0 + ci[j])
                                        : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-                for (int ss = 0; ss < 4; ++ss)
+                for (int ss = 0; ss < SS; ++ss)
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
+                    for (int j = 0; j < JV; ++j) {
                         v[j].x += x[ss][j].x;
                         v[j].y += x[ss][j].y;
                         v[j].z += x[ss][j].z;
@@ -107,7 +110,7 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjArgs a) {
                     }
             }
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < JV; ++j) {
                 const int i = tid + kProjThreads * (jb + j);
                 if (i < n4) *reinterpret_cast<float4 *>(En_s + ri[j] * pe + ci[j]) = v[j];
             }
@@ -121,8 +124,29 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjArgs a) {
             En_s[r * pe + c] = v;
         }
     }
-    // core and left-chain slices: every thread issues its loads before its stores
-    if (a.Gc)
+    // core and left-chain slices: every thread issues its loads before its
+    // stores; the core slice as float4 where the E tile is (nc is then a
+    // multiple of 4)
+    if (a.Gc && vec && (reinterpret_cast<uintptr_t>(a.Gc) % 16 == 0)) {
+        const int q4 = CT4 / 4, n = A4 * q4;
+        for (int i0 = tid; i0 < n; i0 += kProjThreads * 4) {
+            float4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * kProjThreads;
+                const int al = i / q4, c = (i - al * q4) * 4;
+                v[u] = (i < n && al < A && c < nc)
+                           ? *reinterpret_cast<const float4 *>(a.Gc + int64_t(al) * a.cols + c0 + c)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * kProjThreads;
+                const int al = i / q4, c = (i - al * q4) * 4;
+                if (i < n) *reinterpret_cast<float4 *>(Gc_s + al * pe + c) = v[u];
+            }
+        }
+    } else if (a.Gc) {
         for (int i0 = tid; i0 < A4 * CT4; i0 += kProjThreads * 4) {
             float v[4];
 #pragma unroll
@@ -138,6 +162,7 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjArgs a) {
                 if (i < A4 * CT4) Gc_s[al * pe + c] = v[u];
             }
         }
+    }
     if (a.P)
         for (int i0 = tid; i0 < RT * A4; i0 += kProjThreads * 4) {
             float v[4];
@@ -178,16 +203,41 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjArgs a) {
             const float *pa = En_s + min(ra, RT - 1) * pe + lk;
             const float *pb = Gc_s + min(gb, A4 - 1) * pe + lk;
             const bool va = ra < RT, vb = gb < A4;
-            for (int k = 0; k < CT4; k += 8) {
-                float x[4], y[4];
+            if constexpr (kProjThreads == 1024) {
+                // 64 registers: one guarded group at a time
+                for (int k = 0; k < CT4; k += 8) {
+                    float x[4], y[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    x[u] = va ? pa[k + 2 * u] : 0.f;
-                    y[u] = vb ? pb[k + 2 * u] : 0.f;
+                    for (int u = 0; u < 4; ++u) {
+                        x[u] = va ? pa[k + 2 * u] : 0.f;
+                        y[u] = vb ? pb[k + 2 * u] : 0.f;
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        if (k + 2 * u < CT4) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u], y[u], acc, 0, 0, 0);
                 }
+            } else {
+                // whole groups of four products without per-product branches
+                // (the scheduler can then hoist the next group's LDS reads),
+                // then the last two (CT4 is a multiple of 4)
+                int k = 0;
+#pragma unroll 2
+                for (; k + 8 <= CT4; k += 8) {
+                    float x[4], y[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    if (k + 2 * u < CT4) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u], y[u], acc, 0, 0, 0);
+                    for (int u = 0; u < 4; ++u) {
+                        x[u] = va ? pa[k + 2 * u] : 0.f;
+                        y[u] = vb ? pb[k + 2 * u] : 0.f;
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u], y[u], acc, 0, 0, 0);
+                }
+                if (k < CT4) {
+                    const float x0 = va ? pa[k] : 0.f, y0 = vb ? pb[k] : 0.f;
+                    const float x1 = va ? pa[k + 2] : 0.f, y1 = vb ? pb[k + 2] : 0.f;
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x0, y0, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x1, y1, acc, 0, 0, 0);
+                }
             }
             float *dst = a.Eout + int64_t(blockIdx.x) * a.out_stride;
             const int al = nt * 32 + li;
@@ -203,17 +253,38 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjArgs a) {
             const bool va = am < A4, vb = cn < CT4;
             const float *pa = P_s + lk * pp + min(am, A4 - 1);
             const float *pb = En_s + lk * pe + min(cn, CT4 - 1);
-            for (int r = 0; r < RT; r += 8) {
-                float x[4], y[4];
+            if constexpr (kProjThreads == 1024) {
+                for (int r = 0; r < RT; r += 8) {
+                    float x[4], y[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int rr = min(r + 2 * u, RT - 2);
-                    x[u] = va ? pa[rr * pp] : 0.f;
-                    y[u] = vb ? pb[rr * pe] : 0.f;
+                    for (int u = 0; u < 4; ++u) {
+                        const int rr = min(r + 2 * u, RT - 2);
+                        x[u] = va ? pa[rr * pp] : 0.f;
+                        y[u] = vb ? pb[rr * pe] : 0.f;
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        if (r + 2 * u < RT) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u], y[u], acc, 0, 0, 0);
                 }
+            } else {
+                int r = 0;
+#pragma unroll 2
+                for (; r + 8 <= RT; r += 8) {
+                    float x[4], y[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    if (r + 2 * u < RT) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u], y[u], acc, 0, 0, 0);
+                    for (int u = 0; u < 4; ++u) {
+                        x[u] = va ? pa[(r + 2 * u) * pp] : 0.f;
+                        y[u] = vb ? pb[(r + 2 * u) * pe] : 0.f;
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u], y[u], acc, 0, 0, 0);
+                }
+                if (r < RT) {   // RT is a multiple of 4
+                    const float x0 = va ? pa[r * pp] : 0.f, y0 = vb ? pb[r * pe] : 0.f;
+                    const float x1 = va ? pa[(r + 2) * pp] : 0.f, y1 = vb ? pb[(r + 2) * pe] : 0.f;
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x0, y0, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x1, y1, acc, 0, 0, 0);
+                }
             }
             float *dst = a.part + int64_t(blockIdx.y) * A * a.cols;
             const int c = nt * 32 + li;
