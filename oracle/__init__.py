@@ -17,4 +17,4 @@ differences, the rank-mask deletion invariant, inner-product identities, and
 the paper's own large-batch path (Alg. path, eq. path-T1 .. path-gGi<d) on the
 unit-mode TT layout.  No function in this package is "parity unpinned".
 """
-from . import ttm, embed, fp8, mixed  # noqa: F401
+from . import ttm, embed, fp8, mixed, regularizer  # noqa: F401
