@@ -221,6 +221,24 @@ comera_status comera_fp8_quantize(const void *x, int32_t dtype, int64_t rows, in
                                   uint8_t *q, int64_t ldq, uint8_t *qt, int64_t ldt,
                                   float *scale, void *ws, size_t ws_bytes, void *stream);
 
+/* Early-stage regulariser gradients (Sec. 3.2, eq. pretrain-rank), added in
+ * place, on `stream`, to the loss gradients a backward call returned:
+ *   dG_k += 2 beta G_k                         (beta ||G||^2, every core)
+ *   dD_k[c] += gamma sign(D_k[c]) (l_k + r_k)  (gamma S^(D), every bond)
+ * S^ is the layer size with each ||D_k||_0 relaxed to ||D_k||_1, s_j = m_j n_j;
+ * l_k = s_k for k = 0, else s_k ||D_{k-1}||_1; r_k = s_{k+1} for k + 1 = d - 1,
+ * else s_{k+1} ||D_{k+1}||_1; sign(0) = 0.  G, dG: d device pointers to fp32
+ * cores [r[k], m[k], n[k], r[k+1]] (dG null, or an entry null: that core is
+ * skipped); D, dD: d - 1 device pointers to fp32 masks of length r[k+1] (dD
+ * null or an entry null: skipped; any dD needs every D).  Caller owns all
+ * memory; nothing is allocated.  Errors: bad shape, negative or non-finite
+ * gamma / beta, a dG without its G, a dD without every D -> INVALID_ARG; a
+ * core above 2^31 entries -> UNSUPPORTED; launch failure -> HIP.
+ * Deterministic: the l1 norms are summed in a fixed order. */
+comera_status comera_ttm_regularizer_grads(const comera_ttm_shape *s, float gamma, float beta,
+                                           const float *const *G, const float *const *D, float *const *dG,
+                                           float *const *dD, void *stream);
+
 /* Diagnostics: per-kernel timing of the batch products of a plan.  While
  * enabled, forward and backward record a pair of HIP events on the call's
  * stream around each launch of the kernels below; comera_ttm_plan_kernel_time

@@ -28,6 +28,7 @@ EXPORTS = (
     "comera_tt_embed_forward", "comera_tt_embed_backward", "comera_status_string", "comera_last_hip_error",
     "comera_ttm_plan_set_timing", "comera_ttm_plan_kernel_time", "comera_ttm_plan_set_reuse_forward",
     "comera_ttm_backward_masks", "comera_tt_embed_backward_ex", "comera_ttm_plan_set_fp8", "comera_fp8_quantize",
+    "comera_ttm_regularizer_grads",
 )
 FP8_QUANTIZE_WS_BYTES = 2048
 KERNEL_FWD, KERNEL_DX, KERNEL_DW = 0, 1, 2
@@ -90,6 +91,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comera_ttm_backward.restype = i32
     lib.comera_ttm_backward_masks.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.comera_ttm_backward_masks.restype = i32
+    lib.comera_ttm_regularizer_grads.argtypes = [P(comera_ttm_shape), ctypes.c_float, ctypes.c_float, vp, vp, vp, vp,
+                                                 vp]
+    lib.comera_ttm_regularizer_grads.restype = i32
     lib.comera_ttm_plan_destroy.argtypes = [vp]
     lib.comera_ttm_plan_destroy.restype = None
     lib.comera_tt_embed_workspace_bytes.argtypes = [P(comera_tt_embed_shape), i64]
@@ -241,6 +245,16 @@ def comera_ttm_backward(plan, b: int, X, dY, G, D, dX, dG, ws, stream=None) -> i
     st = load().comera_ttm_backward(plan, int(b), _ptr(X), _ptr(dY), _ptr_array(G), _ptr_array(D), _ptr(dX),
                                     _ptr_array(dG), _ptr(ws), _nbytes(ws), _stream(stream))
     _check(st, "comera_ttm_backward")
+    return st
+
+
+def comera_ttm_regularizer_grads(shape, gamma: float, beta: float, G, D, dG, dD, stream=None) -> int:
+    """Add the early-stage regulariser gradients in place (eq. pretrain-rank):
+    dG_k += 2 beta G_k, dD_k += gamma dS^/dD_k.  `shape` is a comera_ttm_shape;
+    G, dG, D, dD are lists of device tensors (or None)."""
+    st = load().comera_ttm_regularizer_grads(ctypes.byref(shape), float(gamma), float(beta), _ptr_array(G),
+                                             _ptr_array(D), _ptr_array(dG), _ptr_array(dD), _stream(stream))
+    _check(st, "comera_ttm_regularizer_grads")
     return st
 
 
