@@ -89,8 +89,10 @@ typedef struct {
 
 typedef struct comera_ttm_plan_s *comera_ttm_plan_t;
 
-/* Plan one TTM layer (Sec. 4.2, Prop. 4.1 and the small-batch greedy search
- * of the appendix; rank masks of eq. Wcompress).  Host only: no device work.
+/* Plan one TTM layer (Sec. 4.2, Prop. 4.1: groups of consecutive cores,
+ * then a sweep of X through the groups; rank masks of eq. Wcompress).  Every
+ * order of that family is enumerated and priced by a cost model (flops at
+ * half the peak, HBM bytes, launches).  Host only: no device work.
  *   s            shape (validated: 1 <= d <= 8, factors >= 1, ranks >= 1,
  *                r[0] = r[d] = 1, act in {F32, BF16}).
  *   batch        number of token rows b (>= 0) the plan is sized for; calls
@@ -307,6 +309,23 @@ comera_status comera_tt_embed_backward_ex(const comera_tt_embed_shape *s, const 
                                           const float *const *G, const float *const *D,
                                           float *const *dG, int32_t flags, void *ws,
                                           size_t ws_bytes, int32_t *err_flag, void *stream);
+
+/* Diagnostics for host-side tests, usable without a GPU: launch check
+ * mode.  While enabled, every compute call of this library runs its whole
+ * host path (argument checks, plan and workspace arithmetic, launch sizing)
+ * but, instead of launching each kernel, checks its configuration against
+ * the gfx950 limits (grid x in [1, 2^31 - 1], grid y and z in [1, 65535],
+ * 1 to 1024 threads per workgroup, at most 160 KiB of LDS) and records it.
+ * No device memory is read or written, so outputs are left as they were; a
+ * configuration outside the limits makes the call return COMERA_ERR_HIP.
+ * The mode is process-wide: do not make real compute calls from other
+ * threads while it is on.  Each call of comera_debug_launch_check clears the
+ * record.  comera_debug_launch_info describes record i (name = the kernel
+ * expression as written in the source); any output pointer may be NULL. */
+comera_status comera_debug_launch_check(int32_t enable);
+int32_t comera_debug_launch_count(void);
+comera_status comera_debug_launch_info(int32_t i, char *name, size_t len, uint32_t *grid3, uint32_t *block3,
+                                       uint64_t *lds, int32_t *ok);
 
 /* Static English text for a status code. */
 const char *comera_status_string(comera_status s);

@@ -255,13 +255,3 @@ def mask_grad_term_scale(X, dY, cores, masks=None) -> List[np.ndarray]:
         g = np.einsum("bNajM,bNicM->ajic", H[k], F[k], optimize=True)
         out.append(np.einsum("ajic->c", np.abs(g * _f64(cores[k]))))
     return out
-
-
-# ----------------------------------------------------------------------------- helpers
-def transpose_cores(cores) -> List[np.ndarray]:
-    """Cores of W^T: swap each core's output and input mode."""
-    return [np.ascontiguousarray(np.swapaxes(_f64(G), 1, 2)) for G in cores]
-
-
-def forward_flops_dense(b: int, n_in: int, n_out: int) -> int:
-    return 2 * b * n_in * n_out

@@ -28,7 +28,8 @@ EXPORTS = (
     "comera_tt_embed_forward", "comera_tt_embed_backward", "comera_status_string", "comera_last_hip_error",
     "comera_ttm_plan_set_timing", "comera_ttm_plan_kernel_time", "comera_ttm_plan_set_reuse_forward",
     "comera_ttm_backward_masks", "comera_tt_embed_backward_ex", "comera_ttm_plan_set_fp8", "comera_fp8_quantize",
-    "comera_ttm_regularizer_grads",
+    "comera_ttm_regularizer_grads", "comera_debug_launch_check", "comera_debug_launch_count",
+    "comera_debug_launch_info",
 )
 FP8_QUANTIZE_WS_BYTES = 2048
 KERNEL_FWD, KERNEL_DX, KERNEL_DW = 0, 1, 2
@@ -119,6 +120,13 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comera_status_string.restype = ctypes.c_char_p
     lib.comera_last_hip_error.argtypes = []
     lib.comera_last_hip_error.restype = ctypes.c_char_p
+    lib.comera_debug_launch_check.argtypes = [i32]
+    lib.comera_debug_launch_check.restype = i32
+    lib.comera_debug_launch_count.argtypes = []
+    lib.comera_debug_launch_count.restype = i32
+    u32, u64 = ctypes.c_uint32, ctypes.c_uint64
+    lib.comera_debug_launch_info.argtypes = [i32, ctypes.c_char_p, sz, P(u32), P(u32), P(u64), P(i32)]
+    lib.comera_debug_launch_info.restype = i32
     _lib = lib
     return lib
 
@@ -319,6 +327,27 @@ def comera_tt_embed_backward(shape, ids, n_tokens: int, dY, G, D, dG, determinis
 
 
 EMBED_REUSE_FORWARD = 1
+
+
+def comera_debug_launch_check(enable: bool) -> None:
+    _check(load().comera_debug_launch_check(int(bool(enable))), "comera_debug_launch_check")
+
+
+def comera_debug_launch_log() -> list:
+    """Every launch recorded since launch check mode was switched on:
+    dicts with the kernel expression, grid, block, LDS bytes and whether the
+    configuration is within the limits."""
+    lib = load()
+    out = []
+    name = ctypes.create_string_buffer(256)
+    g3, b3 = (ctypes.c_uint32 * 3)(), (ctypes.c_uint32 * 3)()
+    lds, ok = ctypes.c_uint64(), ctypes.c_int32()
+    for i in range(int(lib.comera_debug_launch_count())):
+        _check(lib.comera_debug_launch_info(i, name, 256, g3, b3, ctypes.byref(lds), ctypes.byref(ok)),
+               "comera_debug_launch_info")
+        out.append({"kernel": name.value.decode(), "grid": tuple(g3), "block": tuple(b3), "lds": lds.value,
+                    "ok": bool(ok.value)})
+    return out
 
 
 def comera_tt_embed_backward_ex(shape, ids, n_tokens: int, dY, G, D, dG, flags: int, ws, err_flag=None,

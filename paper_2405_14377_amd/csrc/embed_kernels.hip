@@ -949,10 +949,10 @@ template <int RM>
 void launch_rows_nj(int nj4, dim3 grid, void *stream, const int64_t *ids, int64_t n, int64_t V, const float *Apre,
                     const float *Gs, float *Y, int Ep, int R, int Vs, int Es, int sE, int sR, int *err_flag) {
     switch (nj4) {
-        case 1: hipLaunchKernelGGL((embed_rows_kernel<RM, 1>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
-        case 2: hipLaunchKernelGGL((embed_rows_kernel<RM, 2>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
-        case 3: hipLaunchKernelGGL((embed_rows_kernel<RM, 3>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
-        default: hipLaunchKernelGGL((embed_rows_kernel<RM, 4>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
+        case 1: COMERA_LAUNCH((embed_rows_kernel<RM, 1>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
+        case 2: COMERA_LAUNCH((embed_rows_kernel<RM, 2>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
+        case 3: COMERA_LAUNCH((embed_rows_kernel<RM, 3>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
+        default: COMERA_LAUNCH((embed_rows_kernel<RM, 4>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag); break;
     }
 }
 
@@ -960,10 +960,10 @@ template <int NT>
 void launch_rows_mfma(int ns, dim3 grid, void *stream, const int64_t *ids, int64_t n, int64_t V, const float *Apre,
                       const float *Gs, float *Y, int R, int Vs, int Es, int sE, int sR, int *err_flag) {
     switch (ns) {
-        case 1: hipLaunchKernelGGL((embed_rows_mfma_kernel<NT, 1>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
-        case 2: hipLaunchKernelGGL((embed_rows_mfma_kernel<NT, 2>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
-        case 4: hipLaunchKernelGGL((embed_rows_mfma_kernel<NT, 4>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
-        default: hipLaunchKernelGGL((embed_rows_mfma_kernel<NT, 8>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+        case 1: COMERA_LAUNCH((embed_rows_mfma_kernel<NT, 1>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+        case 2: COMERA_LAUNCH((embed_rows_mfma_kernel<NT, 2>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+        case 4: COMERA_LAUNCH((embed_rows_mfma_kernel<NT, 4>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
+        default: COMERA_LAUNCH((embed_rows_mfma_kernel<NT, 8>), grid, dim3(256), 0, hipStream_t(stream), ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
     }
 }
 
@@ -987,13 +987,13 @@ int launch_embed_rows(const int64_t *ids, int64_t n, int64_t V, const float *Apr
             case 7: launch_rows_mfma<7>(ns, grid, stream, ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
             default: launch_rows_mfma<8>(ns, grid, stream, ids, n, V, Apre, Gs, Y, R, Vs, Es, sE, sR, err_flag); break;
         }
-        return int(hipGetLastError());
+        return launch_status();
     }
     if (R <= 8) launch_rows_nj<8>(nj4, grid, stream, ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag);
     else if (R <= 16) launch_rows_nj<16>(nj4, grid, stream, ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag);
     else if (R <= 32) launch_rows_nj<32>(nj4, grid, stream, ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag);
     else launch_rows_nj<64>(nj4, grid, stream, ids, n, V, Apre, Gs, Y, Ep, R, Vs, Es, sE, sR, err_flag);
-    return int(hipGetLastError());
+    return launch_status();
 }
 
 const uint32_t *embed_sorted_keys(const EmbedWs &w, int passes) { return (passes & 1) ? w.keysA : w.keysB; }
@@ -1007,33 +1007,33 @@ int launch_embed_sort(const int64_t *ids, int n, int64_t V, int passes, const Em
     for (int p = 0; p < passes; ++p) {
         // pass 0 also clears the buffers, counts out-of-range ids and sets meta[0]
         const int nclr = p == 0 ? int(std::min<int64_t>(2048, std::max<int64_t>(1, (nclear + nzero + 4095) / 4096))) : 0;
-        hipLaunchKernelGGL(radix_hist_kernel, dim3(nblk + nclr), dim3(256), 0, hipStream_t(stream), ids, kin, n, V,
+        COMERA_LAUNCH(radix_hist_kernel, dim3(nblk + nclr), dim3(256), 0, hipStream_t(stream), ids, kin, n, V,
                            8 * p, nblk, w.hist, p == 0 ? bad : nullptr, err_flag, w.headpos, p == 0 ? nclear : 0,
                            zero, p == 0 ? nzero : 0);
         // up to 64 blocks, each scatter workgroup scans the histograms itself
         const int self_scan = nblk <= 64 ? 1 : 0;
         if (!self_scan)
-            hipLaunchKernelGGL(radix_scan_kernel, dim3(1), dim3(1024), 0, hipStream_t(stream), w.hist, nblk,
+            COMERA_LAUNCH(radix_scan_kernel, dim3(1), dim3(1024), 0, hipStream_t(stream), w.hist, nblk,
                                p == 0 ? bad : nullptr, n, w.meta);
-        hipLaunchKernelGGL(radix_scatter_kernel, dim3(nblk), dim3(256), 0, hipStream_t(stream), ids, kin, vin, n, V,
+        COMERA_LAUNCH(radix_scatter_kernel, dim3(nblk), dim3(256), 0, hipStream_t(stream), ids, kin, vin, n, V,
                            8 * p, nblk, w.hist, kout, vout, self_scan, p == 0 ? bad : nullptr, w.meta);
         kin = kout;
         vin = vout;
         kout = (kout == w.keysA) ? w.keysB : w.keysA;
         vout = (vout == w.valsA) ? w.valsB : w.valsA;
     }
-    return int(hipGetLastError());
+    return launch_status();
 }
 
 int launch_embed_segsum(const float *dY, int E, int n, int passes, const EmbedWs &w, void *stream) {
     const int chunks = (n + kEmbedItem - 1) / kEmbedItem;
     const uint32_t *keys = embed_sorted_keys(w, passes), *vals = sorted_vals(w, passes);
-    hipLaunchKernelGGL(embed_segsum_kernel, dim3(chunks), dim3(256), 0, hipStream_t(stream), dY, E, w.meta, keys, vals,
+    COMERA_LAUNCH(embed_segsum_kernel, dim3(chunks), dim3(256), 0, hipStream_t(stream), dY, E, w.meta, keys, vals,
                        w.S, w.Pfirst, w.Plast, w.headpos);
-    if (int e = int(hipGetLastError())) return e;
-    hipLaunchKernelGGL(embed_segfix_kernel, dim3(chunks, unsigned((E + 63) / 64)), dim3(256), 0, hipStream_t(stream),
+    if (int e = launch_status()) return e;
+    COMERA_LAUNCH(embed_segfix_kernel, dim3(chunks, unsigned((E + 63) / 64)), dim3(256), 0, hipStream_t(stream),
                        E, w.meta, keys, w.Pfirst, w.Plast, w.S);
-    return int(hipGetLastError());
+    return launch_status();
 }
 
 int launch_embed_dapre(const EmbedWs &w, const float *Gs, int64_t Vp, int Ep, int R, int Vs, int Es, int vq, int eq,
@@ -1041,7 +1041,7 @@ int launch_embed_dapre(const EmbedWs &w, const float *Gs, int64_t Vp, int Ep, in
     if (Ep % 16 == 0 && Ep <= 64 && R <= 32 && Es <= 16 && Vs <= 1024) {
         const dim3 grid(static_cast<unsigned>(Vp), 1, 1);
 #define COMERA_DAPRE(NT, NK)                                                                                     \
-    hipLaunchKernelGGL((embed_dapre_mfma_kernel<NT, NK>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, \
+    COMERA_LAUNCH((embed_dapre_mfma_kernel<NT, NK>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, \
                        Gs, Vp, R, Vs, Es, vq, eq, w.dA)
         const int nk = (Es + 3) / 4;
         switch (Ep / 16) {
@@ -1051,19 +1051,19 @@ int launch_embed_dapre(const EmbedWs &w, const float *Gs, int64_t Vp, int Ep, in
             default: if (nk <= 2) COMERA_DAPRE(4, 2); else if (nk == 3) COMERA_DAPRE(4, 3); else COMERA_DAPRE(4, 4); break;
         }
 #undef COMERA_DAPRE
-        return int(hipGetLastError());
+        return launch_status();
     }
     const int nb = dapre_batch(Ep, R, Vs, Es);
     if (nb <= 0) return int(hipErrorInvalidValue);
     const size_t lds = dapre_lds_bytes(Ep, R, Vs, Es, nb);
     const dim3 grid(static_cast<unsigned>(Vp), 1, 1);
     switch ((Es + 3) / 4) {
-        case 1: hipLaunchKernelGGL((embed_dapre_kernel<1>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
-        case 2: hipLaunchKernelGGL((embed_dapre_kernel<2>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
-        case 3: hipLaunchKernelGGL((embed_dapre_kernel<3>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
-        default: hipLaunchKernelGGL((embed_dapre_kernel<4>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
+        case 1: COMERA_LAUNCH((embed_dapre_kernel<1>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
+        case 2: COMERA_LAUNCH((embed_dapre_kernel<2>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
+        case 3: COMERA_LAUNCH((embed_dapre_kernel<3>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
+        default: COMERA_LAUNCH((embed_dapre_kernel<4>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
     }
-    return int(hipGetLastError());
+    return launch_status();
 }
 
 int embed_dglast_chunks(int64_t Vp) { return int((Vp + kGlVp - 1) / kGlVp); }
@@ -1075,31 +1075,31 @@ int launch_embed_dglast(const EmbedWs &w, const float *Apre, bool rank_major, in
         const int nchunk = embed_dglast_chunks(Vp);
         const dim3 grid(unsigned((int64_t(Vs) * nchunk + 3) / 4));
         switch (Ep / 16) {
-            case 1: hipLaunchKernelGGL((embed_dglast_mfma_kernel<4>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
-            case 2: hipLaunchKernelGGL((embed_dglast_mfma_kernel<8>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
-            case 3: hipLaunchKernelGGL((embed_dglast_mfma_kernel<12>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
-            default: hipLaunchKernelGGL((embed_dglast_mfma_kernel<16>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
+            case 1: COMERA_LAUNCH((embed_dglast_mfma_kernel<4>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
+            case 2: COMERA_LAUNCH((embed_dglast_mfma_kernel<8>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
+            case 3: COMERA_LAUNCH((embed_dglast_mfma_kernel<12>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
+            default: COMERA_LAUNCH((embed_dglast_mfma_kernel<16>), grid, dim3(256), 0, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, R, Vs, Es, nchunk, w.dglast_part); break;
         }
-        return int(hipGetLastError());
+        return launch_status();
     }
     const int nb = dglast_batch(Ep, R, Es);
     if (nb <= 0) return int(hipErrorInvalidValue);
     const size_t lds = dglast_lds_bytes(Ep, R, Es, nb);
     const dim3 grid(unsigned(Vs), unsigned(embed_dglast_chunks(Vp)));
     switch ((Es + 3) / 4) {
-        case 1: hipLaunchKernelGGL((embed_dglast_kernel<1>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
-        case 2: hipLaunchKernelGGL((embed_dglast_kernel<2>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
-        case 3: hipLaunchKernelGGL((embed_dglast_kernel<3>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
-        default: hipLaunchKernelGGL((embed_dglast_kernel<4>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
+        case 1: COMERA_LAUNCH((embed_dglast_kernel<1>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
+        case 2: COMERA_LAUNCH((embed_dglast_kernel<2>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
+        case 3: COMERA_LAUNCH((embed_dglast_kernel<3>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
+        default: COMERA_LAUNCH((embed_dglast_kernel<4>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Apre, sE, sR, Vp, Ep, R, Vs, Es, nb, w.dglast_part); break;
     }
-    return int(hipGetLastError());
+    return launch_status();
 }
 
 int launch_embed_gather(const EmbedWs &w, int64_t V, int E, float *dG0, void *stream) {
     const int64_t total = V * E;
     const int grid = int(std::max<int64_t>(1, std::min<int64_t>((total + 255) / 256, 65536)));
-    hipLaunchKernelGGL(embed_gather_kernel, dim3(grid), dim3(256), 0, hipStream_t(stream), w.headpos, w.S, V, E, dG0);
-    return int(hipGetLastError());
+    COMERA_LAUNCH(embed_gather_kernel, dim3(grid), dim3(256), 0, hipStream_t(stream), w.headpos, w.S, V, E, dG0);
+    return launch_status();
 }
 
 }  // namespace comera

@@ -279,16 +279,16 @@ int launch_fp8_quant(const void *x, int dtype, int64_t R, int64_t C, float *pmax
         const int64_t per = int64_t(kAmaxThreads) * 4;
         nb = int(std::min<int64_t>(kAmaxBlocks, std::max<int64_t>(1, (n / V + per - 1) / per)));
         if (V == 8)
-            hipLaunchKernelGGL(amax_vec_kernel<8>, dim3(nb), dim3(kAmaxThreads), 0, hipStream_t(stream), x, dtype, n,
+            COMERA_LAUNCH(amax_vec_kernel<8>, dim3(nb), dim3(kAmaxThreads), 0, hipStream_t(stream), x, dtype, n,
                                pmax);
         else
-            hipLaunchKernelGGL(amax_vec_kernel<4>, dim3(nb), dim3(kAmaxThreads), 0, hipStream_t(stream), x, dtype, n,
+            COMERA_LAUNCH(amax_vec_kernel<4>, dim3(nb), dim3(kAmaxThreads), 0, hipStream_t(stream), x, dtype, n,
                                pmax);
     } else {
         nb = int(std::min<int64_t>(kAmaxBlocks, (n + 255) / 256));
-        hipLaunchKernelGGL(amax_partial_kernel, dim3(nb), dim3(256), 0, hipStream_t(stream), x, dtype, n, pmax);
+        COMERA_LAUNCH(amax_partial_kernel, dim3(nb), dim3(256), 0, hipStream_t(stream), x, dtype, n, pmax);
     }
-    if (int e = int(hipGetLastError())) return e;
+    if (int e = launch_status()) return e;
     const int64_t rows = qt ? std::max<int64_t>(R, ldt) : R;
     const int64_t cols = q ? std::max<int64_t>(C, ldq) : C;
     const bool vec = xa && C % V == 0 && (!q || (al(q, V) && ldq % V == 0)) && (!qt || (al(qt, 16) && ldt % 16 == 0));
@@ -297,15 +297,15 @@ int launch_fp8_quant(const void *x, int dtype, int64_t R, int64_t C, float *pmax
     if (gx > 2147483647 || gy > 65535) return int(hipErrorInvalidValue);
     const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(gy), 1);
     if (vec && V == 8)
-        hipLaunchKernelGGL(quant_vec_kernel<8>, grid, dim3(256), 0, hipStream_t(stream), x, R, C, pmax, nb, q, ldq,
+        COMERA_LAUNCH(quant_vec_kernel<8>, grid, dim3(256), 0, hipStream_t(stream), x, R, C, pmax, nb, q, ldq,
                            qt, ldt, s_out, pa, oa, pb, ob);
     else if (vec)
-        hipLaunchKernelGGL(quant_vec_kernel<4>, grid, dim3(256), 0, hipStream_t(stream), x, R, C, pmax, nb, q, ldq,
+        COMERA_LAUNCH(quant_vec_kernel<4>, grid, dim3(256), 0, hipStream_t(stream), x, R, C, pmax, nb, q, ldq,
                            qt, ldt, s_out, pa, oa, pb, ob);
     else
-        hipLaunchKernelGGL(quant_kernel, grid, dim3(256), 0, hipStream_t(stream), x, dtype, R, C, pmax, nb, q, ldq,
+        COMERA_LAUNCH(quant_kernel, grid, dim3(256), 0, hipStream_t(stream), x, dtype, R, C, pmax, nb, q, ldq,
                            qt, ldt, s_out, pa, oa, pb, ob);
-    return int(hipGetLastError());
+    return launch_status();
 }
 
 }  // namespace comera

@@ -751,8 +751,8 @@ int launch_t(const GemmArgs &g, const GemmParams &p, int tile, void *stream) {
         const dim3 grid = tile_grid(g, bm, bn, q);
         if (!grid.x) return int(hipErrorInvalidConfiguration);
         q.gw = choose_gw(g, bm, bn, g.splits);
-        hipLaunchKernelGGL(kern, grid, dim3(256), 0, hipStream_t(stream), q);
-        return int(hipGetLastError());
+        COMERA_LAUNCH_NAMED("gemm_kernel", kern, grid, dim3(256), 0, hipStream_t(stream), q);
+        return launch_status();
     };
     switch (tile) {
         case T128x128: return go(gemm_kernel<T, AK, BK, OB, 128, 128, 64, 64>, 128, 128);
@@ -800,15 +800,17 @@ int go_fast(const GemmArgs &g, const GemmParams &p, void *stream) {
     static_assert(lds <= kLdsPerCu, "LDS of one workgroup");
     auto kern = gemm_fast_kernel<T, AK, BK, OB, BM, BN, WM, WN, KTB, NT, PF>;
     // above the default 64 KB of dynamic LDS: raise the limit once per kernel
-    static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                                   hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
-    if (set) return set;
+    if (!launch_check_mode()) {
+        static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
+        if (set) return set;
+    }
     GemmParams q = p;
     const dim3 grid = tile_grid(g, BM, BN, q);
     if (!grid.x) return int(hipErrorInvalidConfiguration);
     q.gw = choose_gw(g, BM, BN, g.splits);
-    hipLaunchKernelGGL(kern, grid, dim3(NT), lds, hipStream_t(stream), q);
-    return int(hipGetLastError());
+    COMERA_LAUNCH_NAMED("gemm_fast_kernel", kern, grid, dim3(NT), lds, hipStream_t(stream), q);
+    return launch_status();
 }
 
 template <typename T, bool AK, bool BK, bool OB>

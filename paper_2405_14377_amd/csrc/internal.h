@@ -432,6 +432,23 @@ comera_status sweep_backward(const comera_ttm_plan_s *p, int64_t b, const void *
                              const float *const *G, const float *const *D, void *dX, float *const *dG,
                              float *const *dD, void *ws, void *stream);
 
+// Every kernel launch goes through COMERA_LAUNCH.  In launch check mode
+// (comera_debug_launch_check) the configuration is validated and recorded
+// instead of launched; launch_status() then returns the first failed check
+// since the last call, otherwise hipGetLastError().
+bool launch_check_mode();
+void launch_check(const char *name, dim3 grid, dim3 block, size_t lds);
+int launch_status();
+#define COMERA_LAUNCH_NAMED(name, kern, grid, block, lds, stream, ...)                        \
+    do {                                                                                      \
+        if (::comera::launch_check_mode())                                                    \
+            ::comera::launch_check(name, dim3(grid), dim3(block), size_t(lds));               \
+        else                                                                                  \
+            hipLaunchKernelGGL(kern, grid, block, lds, stream, __VA_ARGS__);                  \
+    } while (0)
+#define COMERA_LAUNCH(kern, grid, block, lds, stream, ...) \
+    COMERA_LAUNCH_NAMED(#kern, kern, grid, block, lds, stream, __VA_ARGS__)
+
 // record a failed launcher result (hipError_t value e != 0) with the step
 // name for comera_last_hip_error; returns e (api_ttm.hip)
 int note_hip(int e, const char *where);

@@ -577,13 +577,15 @@ int launch_wbuild(const WBuildArgs &a, void *stream) {
     if (a.NI <= 0 || a.NJ <= 0 || (!a.out && !a.out_t)) return 0;
     const size_t lds = wtile_lds_floats(a.A, a.QI, a.QJ, a.nx, a.ny) * sizeof(float);
     if (lds > kProjLds || a.QI < 1 || a.QJ < 1) return int(hipErrorInvalidValue);
-    static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(wtile_kernel),
-                                                   hipFuncAttributeMaxDynamicSharedMemorySize, int(kProjLds)));
-    if (set) return set;
+    if (!launch_check_mode()) {
+        static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(wtile_kernel),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(kProjLds)));
+        if (set) return set;
+    }
     const int64_t gx = (a.NJ + a.QJ - 1) / a.QJ, gy = (a.NI + a.QI - 1) / a.QI;
     if (gx >= (int64_t(1) << 31) || gy > 65535) return int(hipErrorInvalidValue);
-    hipLaunchKernelGGL(wtile_kernel, dim3(unsigned(gx), unsigned(gy)), dim3(256), lds, hipStream_t(stream), a);
-    return int(hipGetLastError());
+    COMERA_LAUNCH(wtile_kernel, dim3(unsigned(gx), unsigned(gy)), dim3(256), lds, hipStream_t(stream), a);
+    return launch_status();
 }
 
 int launch_proj(const ProjArgs &a, void *stream) {
@@ -596,10 +598,10 @@ int launch_proj(const ProjArgs &a, void *stream) {
     // else 256 (several workgroups per CU)
     const int64_t loads4 = int64_t(a.RT) * ((a.CT + 3) / 4) * std::max(1, a.nin);
     if (loads4 > 4096)
-        hipLaunchKernelGGL((proj_kernel<kProjThreadsMax>), grid, dim3(kProjThreadsMax), lds, hipStream_t(stream), a);
+        COMERA_LAUNCH((proj_kernel<kProjThreadsMax>), grid, dim3(kProjThreadsMax), lds, hipStream_t(stream), a);
     else
-        hipLaunchKernelGGL((proj_kernel<256>), grid, dim3(256), lds, hipStream_t(stream), a);
-    return int(hipGetLastError());
+        COMERA_LAUNCH((proj_kernel<256>), grid, dim3(256), lds, hipStream_t(stream), a);
+    return launch_status();
 }
 
 }  // namespace comera

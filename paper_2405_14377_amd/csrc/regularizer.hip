@@ -18,7 +18,7 @@
 #include <cmath>
 #include <cstdint>
 
-#include "comera.h"
+#include "internal.h"
 
 namespace {
 
@@ -114,12 +114,12 @@ extern "C" comera_status comera_ttm_regularizer_grads(const comera_ttm_shape *s,
     hipStream_t st = hipStream_t(stream);
     if (mx > 0) {
         const unsigned gx = unsigned(std::min<int64_t>((mx + 255) / 256, 1024));
-        hipLaunchKernelGGL(reg_core_kernel, dim3(gx, unsigned(s->d)), dim3(256), 0, st, a);
-        if (hipGetLastError() != hipSuccess) return COMERA_ERR_HIP;
+        COMERA_LAUNCH(reg_core_kernel, dim3(gx, unsigned(s->d)), dim3(256), 0, st, a);
+        if (comera::note_hip(comera::launch_status(), "regulariser: core terms")) return COMERA_ERR_HIP;
     }
     if (any_dD) {
-        hipLaunchKernelGGL(reg_mask_kernel, dim3(1), dim3(256), 0, st, a);
-        if (hipGetLastError() != hipSuccess) return COMERA_ERR_HIP;
+        COMERA_LAUNCH(reg_mask_kernel, dim3(1), dim3(256), 0, st, a);
+        if (comera::note_hip(comera::launch_status(), "regulariser: mask terms")) return COMERA_ERR_HIP;
     }
     return COMERA_OK;
 }

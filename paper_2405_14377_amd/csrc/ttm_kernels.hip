@@ -263,8 +263,8 @@ int launch_fold(const FoldArgs &a, void *stream) {
     for (int k = 0; k < a.nfold; ++k) mx = std::max<int64_t>(mx, int64_t(a.rc[k]) * a.m[k] * a.n[k] * a.rc[k + 1]);
     if (a.nfold <= 0) return 0;
     dim3 grid(grid_for(mx), a.nfold);
-    hipLaunchKernelGGL(fold_kernel, grid, dim3(256), 0, hipStream_t(stream), a);
-    return int(hipGetLastError());
+    COMERA_LAUNCH(fold_kernel, grid, dim3(256), 0, hipStream_t(stream), a);
+    return launch_status();
 }
 
 int launch_expand(const ExpandArgs &a_in, void *stream) {
@@ -280,8 +280,8 @@ int launch_expand(const ExpandArgs &a_in, void *stream) {
     }
     for (int k = a.d; k < kMaxCores; ++k) a.blk0[k] = blocks;
     if (blocks == 0) return 0;
-    hipLaunchKernelGGL(expand_kernel, dim3(unsigned(blocks)), dim3(256), 0, hipStream_t(stream), a);
-    return int(hipGetLastError());
+    COMERA_LAUNCH(expand_kernel, dim3(unsigned(blocks)), dim3(256), 0, hipStream_t(stream), a);
+    return launch_status();
 }
 
 int launch_mask_grad(const MaskGradArgs &a_in, void *stream) {
@@ -293,13 +293,13 @@ int launch_mask_grad(const MaskGradArgs &a_in, void *stream) {
     }
     for (int k = std::max(0, a.d - 1); k < kMaxCores; ++k) a.blk0[k] = blocks;
     if (blocks == 0) return 0;
-    hipLaunchKernelGGL(mask_grad_kernel, dim3(unsigned(blocks)), dim3(256), 0, hipStream_t(stream), a);
-    return int(hipGetLastError());
+    COMERA_LAUNCH(mask_grad_kernel, dim3(unsigned(blocks)), dim3(256), 0, hipStream_t(stream), a);
+    return launch_status();
 }
 
 int launch_sum_splits(const float *part, float *out, int64_t n, int splits, void *stream) {
-    hipLaunchKernelGGL(sum_splits_kernel, dim3(grid_for(n)), dim3(256), 0, hipStream_t(stream), part, out, n, splits);
-    return int(hipGetLastError());
+    COMERA_LAUNCH(sum_splits_kernel, dim3(grid_for(n)), dim3(256), 0, hipStream_t(stream), part, out, n, splits);
+    return launch_status();
 }
 
 int launch_permute_tokens(const void *in, void *out, int64_t b, int64_t M, int64_t T, int esz, void *stream) {
@@ -308,33 +308,33 @@ int launch_permute_tokens(const void *in, void *out, int64_t b, int64_t M, int64
     const int64_t total = b * tm * tt;
     const unsigned grid = unsigned(std::min<int64_t>(total, 16384));
     if (esz == 2)
-        hipLaunchKernelGGL(permute_kernel<uint16_t>, dim3(grid), dim3(256), 0, hipStream_t(stream),
+        COMERA_LAUNCH(permute_kernel<uint16_t>, dim3(grid), dim3(256), 0, hipStream_t(stream),
                            reinterpret_cast<const uint16_t *>(in), reinterpret_cast<uint16_t *>(out), b, int(M),
                            int(T), tm, tt);
     else
-        hipLaunchKernelGGL(permute_kernel<float>, dim3(grid), dim3(256), 0, hipStream_t(stream),
+        COMERA_LAUNCH(permute_kernel<float>, dim3(grid), dim3(256), 0, hipStream_t(stream),
                            reinterpret_cast<const float *>(in), reinterpret_cast<float *>(out), b, int(M), int(T),
                            tm, tt);
-    return int(hipGetLastError());
+    return launch_status();
 }
 
 int launch_sum_splits_bf16(const float *part, void *out, int64_t n, int splits, void *stream) {
-    hipLaunchKernelGGL(sum_splits_bf16_kernel, dim3(grid_for(n)), dim3(256), 0, hipStream_t(stream), part,
+    COMERA_LAUNCH(sum_splits_bf16_kernel, dim3(grid_for(n)), dim3(256), 0, hipStream_t(stream), part,
                        reinterpret_cast<uint16_t *>(out), n, splits);
-    return int(hipGetLastError());
+    return launch_status();
 }
 
 int launch_fill_one(float *ptr, void *stream) {
-    hipLaunchKernelGGL(fill_one_kernel, dim3(1), dim3(1), 0, hipStream_t(stream), ptr);
-    return int(hipGetLastError());
+    COMERA_LAUNCH(fill_one_kernel, dim3(1), dim3(1), 0, hipStream_t(stream), ptr);
+    return launch_status();
 }
 
 int launch_fill_zero(void *ptr, size_t bytes, void *stream) {
     if (bytes == 0) return 0;
     int64_t n = int64_t(bytes / 4);
-    hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for(n)), dim3(256), 0, hipStream_t(stream),
+    COMERA_LAUNCH(fill_zero_kernel, dim3(grid_for(n)), dim3(256), 0, hipStream_t(stream),
                        reinterpret_cast<uint32_t *>(ptr), n);
-    return int(hipGetLastError());
+    return launch_status();
 }
 
 }  // namespace comera

@@ -10,6 +10,7 @@ import pytest
 
 from oracle import ttm as OT
 from paper_2405_14377_amd import workloads as wl
+from tests.chunked import xt_dy_fp64
 from tests.gpu_util import TTMRun, rel_err, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
@@ -202,10 +203,12 @@ def test_encoder_layers(li):
 
 
 @pytest.mark.parametrize("li", [0, 1])
-def test_large_pair_sampled_and_invariants(li):
-    """1024 <-> 4096, d = 4, 65536 tokens, bf16: Y and dX on 512 sampled rows;
-    dG_k through <dG_k, G_k> = <Y, dY> (W is linear in each core); dG_k in
-    full on the first 4096 tokens."""
+def test_large_pair_full_size(li):
+    """1024 <-> 4096, d = 4, 65536 tokens, bf16, one plan at the full batch
+    (its token split of dW and the projections that sum the split partials):
+    every dG_k element by element against the oracle's dense-W route over
+    all 65536 tokens; Y and dX on 512 sampled rows; <dG_k, G_k> = <Y, dY> =
+    <dX, X> (W is linear in each core)."""
     import torch
     sh, inp, X, dY, mask_active = _workload_layer(4, li, "bf16")
     b = X.shape[0]
@@ -218,16 +221,15 @@ def test_large_pair_sampled_and_invariants(li):
     assert rel_err(to_np(Y[rows]), X[rows].astype(np.float64) @ W) <= TOL["bf16"]
     assert rel_err(to_np(dX[rows]), dY[rows].astype(np.float64) @ W.T) <= TOL["bf16"]
     ydy = float((Y.float() * dYt.float()).double().sum().item())
-    for k in range(4):
-        gk = float((dG[k].double() * run.G[k].double()).sum().item())
-        assert abs(gk - ydy) <= 1e-2 * abs(ydy), (k, gk, ydy)
     xdx = float((dX.float() * Xt.float()).double().sum().item())
     assert abs(xdx - ydy) <= 1e-2 * abs(ydy)
+    dGg = [to_np(g) for g in dG]
     del Y, dX, dG
     torch.cuda.empty_cache()
-    bs = 4096
-    run2 = TTMRun(sh.n, sh.m, sh.r, inp.cores, inp.masks, bs, "bf16", mask_active=mask_active)
-    _, dG2 = run2.backward(to_dev(X[:bs], "bf16"), to_dev(dY[:bs], "bf16"), want_dx=False)
-    dGr = OT.project_dW(X[:bs].astype(np.float64).T @ dY[:bs].astype(np.float64), inp.cores, inp.masks)
+    dGr = OT.project_dW(xt_dy_fp64(X, dY), inp.cores, inp.masks)
     for k in range(4):
-        assert rel_err(to_np(dG2[k]), dGr[k]) <= TOL["bf16"], k
+        err = rel_err(dGg[k], dGr[k])
+        print(f"layer {li} dG{k}: {err:.3e}")
+        assert err <= TOL["bf16"], (k, err)
+        gk = float(np.sum(dGg[k] * inp.cores[k].astype(np.float64)))
+        assert abs(gk - ydy) <= 1e-2 * abs(ydy), (k, gk, ydy)
