@@ -145,6 +145,28 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X,
                                  const float *const *G, const float *const *D, void *Y,
                                  void *ws, size_t ws_bytes, void *stream);
 
+/* comera_ttm_forward for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same Y = X W with no workspace argument.  The scratch it
+ * needs (folded cores, left chains, W^T) lives in one static device array of
+ * COMERA_TTM_NOALLOC_SCRATCH_BYTES per GPU, reserved when the library is
+ * loaded on that GPU and held until the process ends; the call allocates
+ * nothing.  It runs on the current device, which must be the device of
+ * `stream`.  Every call on a GPU shares that GPU's array, so calls that
+ * overlap on one GPU (other streams, other threads) race: serialise them.
+ * Nothing carries over between calls (every region is written before it is
+ * read).  The batch product is not split over K, so results may differ
+ * from comera_ttm_forward's in the last bits at small batches.
+ * Errors: as comera_ttm_forward; COMERA_ERR_UNSUPPORTED for a plan whose
+ * order is not the dense order (plan with force_order = 0 when the planner
+ * picks a sweep), with FP8 or reuse switched on, or whose scratch (folded
+ * cores + left chains + W + W^T in the activation dtype) exceeds
+ * COMERA_TTM_NOALLOC_SCRATCH_BYTES. */
+#define COMERA_TTM_NOALLOC_SCRATCH_BYTES (64u << 20)
+comera_status comera_ttm_forward_noalloc(comera_ttm_plan_t p, int64_t b, const void *X,
+                                         const float *const *G, const float *const *D, void *Y,
+                                         void *stream);
+
 /* dX[b, N_in] = dY W^T (eq. back X) and every dG_k (eq. back Gi), with
  * dG_k scaled by D_{k-1} on its left bond and D_k on its right bond (chain
  * rule through eq. Wcompress).  dX may be NULL (not computed); dG may be

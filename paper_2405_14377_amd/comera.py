@@ -29,7 +29,7 @@ EXPORTS = (
     "comera_ttm_plan_set_timing", "comera_ttm_plan_kernel_time", "comera_ttm_plan_set_reuse_forward",
     "comera_ttm_backward_masks", "comera_tt_embed_backward_ex", "comera_ttm_plan_set_fp8", "comera_fp8_quantize",
     "comera_ttm_regularizer_grads", "comera_debug_launch_check", "comera_debug_launch_count",
-    "comera_debug_launch_info",
+    "comera_debug_launch_info", "comera_ttm_forward_noalloc",
 )
 FP8_QUANTIZE_WS_BYTES = 2048
 KERNEL_FWD, KERNEL_DX, KERNEL_DW = 0, 1, 2
@@ -88,6 +88,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.comera_ttm_workspace_bytes.restype = sz
     lib.comera_ttm_forward.argtypes = [vp, i64, vp, vp, vp, vp, vp, sz, vp]
     lib.comera_ttm_forward.restype = i32
+    lib.comera_ttm_forward_noalloc.argtypes = [vp, i64, vp, vp, vp, vp, vp]
+    lib.comera_ttm_forward_noalloc.restype = i32
     lib.comera_ttm_backward.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.comera_ttm_backward.restype = i32
     lib.comera_ttm_backward_masks.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -246,6 +248,14 @@ def comera_ttm_forward(plan, b: int, X, G, D, Y, ws, stream=None) -> int:
     st = load().comera_ttm_forward(plan, int(b), _ptr(X), _ptr_array(G), _ptr_array(D), _ptr(Y), _ptr(ws),
                                    _nbytes(ws), _stream(stream))
     _check(st, "comera_ttm_forward")
+    return st
+
+
+def comera_ttm_forward_noalloc(plan, b: int, X, G, D, Y, stream=None, raise_on_error: bool = True) -> int:
+    st = load().comera_ttm_forward_noalloc(plan, int(b), _ptr(X), _ptr_array(G), _ptr_array(D), _ptr(Y),
+                                           _stream(stream))
+    if raise_on_error:
+        _check(st, "comera_ttm_forward_noalloc")
     return st
 
 

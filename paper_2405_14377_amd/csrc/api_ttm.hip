@@ -4,6 +4,7 @@
 
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "internal.h"
 
@@ -423,6 +424,81 @@ void timing_clear(comera_ttm_plan_s *p) {
 
 }  // namespace comera
 
+namespace {
+
+// Dense order: build W^T (and W for a backward that reuses it), then
+// Y[b, N_out] = X[b, N_in] W (eq. forward), W^T read row by row.  With
+// split_ok the product may split over K into the plan's partials region
+// (small batches); otherwise it runs unsplit.
+comera_status dense_forward(comera_ttm_plan_t p, int64_t b, const void *X, const float *const *G,
+                            const float *const *D, void *Y, void *ws, bool split_ok, void *stream) {
+    DenseBuild bd;
+    int e = build_dense(p, G, D, ws, stream, bd, kWantWT | (p->reuse ? kWantW : 0));
+    if (e) return COMERA_ERR_HIP;
+    void *ev;
+    timing_begin(p, COMERA_KERNEL_FWD, stream, &ev);
+    GemmArgs g;
+    g.dtype = p->s.act;
+    g.a_kc = true;
+    g.b_kc = true;
+    g.out_bf16 = p->s.act == COMERA_BF16;
+    g.A = X;
+    g.B = bd.wt;
+    g.C = Y;
+    g.M = b;
+    g.N = p->N_out;
+    g.K = p->N_in;
+    g.lda = p->N_in;
+    g.ldb = p->N_in;
+    g.rmap = remap_linear(p->N_out);
+    g.cmap = remap_linear(1);
+    if (split_ok && p->dense.part_elems > 0) {
+        g.scratch = reinterpret_cast<float *>(at(ws, p->dense.part));
+        g.scratch_elems = p->dense.part_elems;
+        g.out_elems = b * p->N_out;
+    }
+    e = note_hip(launch_gemm(g, stream), "forward GEMM");
+    timing_end(p, COMERA_KERNEL_FWD, stream, ev);
+    return e ? COMERA_ERR_HIP : COMERA_OK;
+}
+
+// Scratch of comera_ttm_forward_noalloc: one array per GPU, taken when the
+// library's code object is loaded on that GPU and held until the process
+// ends.  Host code must never pass the array's name to a kernel (on the host
+// it is only a stand-in for the symbol); scratch_address() returns this
+// GPU's device address of it, looked up once per device with that device
+// current.
+constexpr size_t kNoAllocScratchBytes = size_t(COMERA_TTM_NOALLOC_SCRATCH_BYTES);
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_dev[kMaxDevices] = {};
+
+int scratch_address(void **out) {
+    *out = nullptr;
+    if (launch_check_mode()) {   // host-only check: a placeholder, never dereferenced
+        *out = reinterpret_cast<void *>(uintptr_t(1) << 40);
+        return 0;
+    }
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return int(e);
+    if (dev < 0 || dev >= kMaxDevices) return int(hipErrorInvalidDevice);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return int(e);
+        if (!ptr) return int(hipErrorInvalidSymbol);
+        g_scratch_dev[dev] = ptr;
+    }
+    *out = g_scratch_dev[dev];
+    return 0;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char *comera_last_hip_error(void) { return g_last_hip_error; }
@@ -442,36 +518,33 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, 
     if (!ws || ws_bytes < p->ws_bytes) return COMERA_ERR_WORKSPACE;
     if (p->sweep.G > 0) return sweep_forward(p, b, X, G, D, Y, ws, stream);
     if (p->fp8) return fp8_forward(p, b, X, G, D, Y, ws, stream);
-    DenseBuild bd;
-    // W^T for the forward product; with reuse also W for the backward call
-    int e = build_dense(p, G, D, ws, stream, bd, kWantWT | (p->reuse ? kWantW : 0));
-    if (e) return COMERA_ERR_HIP;
-    // Y[b, N_out] = X[b, N_in] W (eq. forward), W^T read row by row
-    void *ev;
-    timing_begin(p, COMERA_KERNEL_FWD, stream, &ev);
-    GemmArgs g;
-    g.dtype = p->s.act;
-    g.a_kc = true;
-    g.b_kc = true;
-    g.out_bf16 = p->s.act == COMERA_BF16;
-    g.A = X;
-    g.B = bd.wt;
-    g.C = Y;
-    g.M = b;
-    g.N = p->N_out;
-    g.K = p->N_in;
-    g.lda = p->N_in;
-    g.ldb = p->N_in;
-    g.rmap = remap_linear(p->N_out);
-    g.cmap = remap_linear(1);
-    if (p->dense.part_elems > 0) {
-        g.scratch = reinterpret_cast<float *>(at(ws, p->dense.part));
-        g.scratch_elems = p->dense.part_elems;
-        g.out_elems = b * p->N_out;
-    }
-    e = note_hip(launch_gemm(g, stream), "forward GEMM");
-    timing_end(p, COMERA_KERNEL_FWD, stream, ev);
-    return e ? COMERA_ERR_HIP : COMERA_OK;
+    return dense_forward(p, b, X, G, D, Y, ws, true, stream);
+}
+
+comera_status comera_ttm_forward_noalloc(comera_ttm_plan_t p, int64_t b, const void *X, const float *const *G,
+                                         const float *const *D, void *Y, void *stream) {
+    if (!p || b < 0 || b > p->batch) return COMERA_ERR_INVALID_ARG;
+    if (b == 0) return COMERA_OK;
+    if (!X || !Y) return COMERA_ERR_INVALID_ARG;
+    const size_t esz = p->s.act == COMERA_BF16 ? 2 : 4;
+    if (p->zero)
+        return note_hip(launch_fill_zero(Y, size_t(b) * size_t(p->N_out) * esz, stream), "fill") ? COMERA_ERR_HIP
+                                                                                                 : COMERA_OK;
+    if (!G) return COMERA_ERR_INVALID_ARG;
+    for (int k = 0; k < p->d; ++k)
+        if (!G[k]) return COMERA_ERR_INVALID_ARG;
+    if (p->sweep.G > 0 || p->fp8 || p->reuse) return COMERA_ERR_UNSUPPORTED;
+    // the unsplit forward of the dense order touches the folded cores, the
+    // left chains, W, W^T and the 1.0 cell: every region before the dX partials
+    if (p->dense.ones + sizeof(float) > kNoAllocScratchBytes) return COMERA_ERR_UNSUPPORTED;
+    void *ws = nullptr;
+    if (note_hip(scratch_address(&ws), "scratch address")) return COMERA_ERR_HIP;
+    // no timing events: they would be allocations
+    const bool timing = p->timing.on;
+    p->timing.on = false;
+    const comera_status st = dense_forward(p, b, X, G, D, Y, ws, false, stream);
+    p->timing.on = timing;
+    return st;
 }
 
 }  // extern "C"

@@ -111,6 +111,12 @@ def run_ttm(n, m, r, batch, act, ma, out):
                     ("backward masks", lambda: lib.comera_ttm_backward_masks(h, b, X, dY, Gp, Dp, dX, dGp, dDp, ws,
                                                                               wsb, 0)),
                 ]
+                if not reuse and not fp8:
+                    st = lib.comera_ttm_forward_noalloc(h, b, X, Gp, Dp, Y, 0)
+                    out["calls"] += 1
+                    if st not in (C.OK, C.ERR_UNSUPPORTED) or (st != C.OK and order == 0 and wsb < (48 << 20)):
+                        out["bad_status"].append({"call": "forward noalloc", "order": order, "n": n, "m": m, "r": r,
+                                                  "b": b, "act": act, "st": st})
                 for name, fn in calls:
                     st = fn()
                     out["calls"] += 1
