@@ -2,13 +2,14 @@
 """Throughput of the TTM-layer hot path on one MI355X.
 
 A step is one pass of the whole path over one batch: forward Y = X W and
-backward dX = dY W^T plus every dG_k, through the C ABI, for the TTM FFN
-up-projection 768 -> 3072 (n = (8, 8, 12), m = (16, 16, 12), ranks
-(1, 30, 30, 1), Bernoulli(0.8) rank masks, 32 x 128 = 4096 tokens).  The
-plan is made once, outside the timed region.  The line reports the fp32
-run as `value`; the bf16 run (fp32 accumulation), the dense GEMM baseline,
-the roofline of the dominant kernel, the CPU oracle and the other workloads
-are reported beside it.
+backward dX = dY W^T plus every dG_k, through the C ABI, for the largest
+configuration: the TTM pair 1024 -> 4096 and 4096 -> 1024 (d = 4, factors
+(4, 8, 4, 8) / (8, 8, 8, 8), ranks (1, 64, 64, 64, 1), Bernoulli(0.7) rank
+masks, 65536 tokens, bf16 activations with fp32 accumulation), both layers
+per step.  Plans are made once, outside the timed region.  Beside it: the
+dense GEMM baseline, the roofline of the dominant kernel, the 768 -> 3072
+layer (fp32 and bf16), the other workloads, the FP8 layers and the CPU
+oracle.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -30,6 +31,7 @@ PEAK = {"f32": 157.3e12, "bf16": 2.5e15}
 HBM_PEAK = 8.0e12
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2405_14377_amd", "csrc", f) for f in ("gemm.hip", "api_ttm.hip")]
+HEADLINE_WID = 4              # the 1024 <-> 4096 d4 r64 pair, 65536 tokens, bf16
 COPY_BYTES = 1 << 28          # plain device copy used to scale the HBM byte counters
 
 
@@ -166,7 +168,7 @@ def traffic_from_profile(kernel_tag, act):
     return float(m_b.group(1))
 
 
-def kernel_roofline(layer, steps, act):
+def kernel_roofline(layer, steps, act, tag=""):
     """Mean duration of each batch-product kernel from HIP events recorded by
     the library on its launch stream, over `steps` instrumented steps."""
     import torch
@@ -178,17 +180,20 @@ def kernel_roofline(layer, steps, act):
     sh, b = layer.sh, layer.b
     flops = 2.0 * b * sh.n_in * sh.n_out        # per launch of each of the three products
     out = {}
-    for tag, kid in (("fwd", C.KERNEL_FWD), ("dx", C.KERNEL_DX), ("dw", C.KERNEL_DW)):
+    for kt, kid in (("fwd", C.KERNEL_FWD), ("dx", C.KERNEL_DX), ("dw", C.KERNEL_DW)):
         ms, cnt = C.comera_ttm_plan_kernel_time(layer.plan.handle, kid)
-        out[tag] = {"avg_ms": ms, "launches": cnt, "tflops": flops / (ms * 1e-3) / 1e12 if ms > 0 else 0.0}
+        out[kt] = {"avg_ms": ms, "launches": cnt, "tflops": flops / (ms * 1e-3) / 1e12 if ms > 0 else 0.0}
     C.comera_ttm_plan_set_timing(layer.plan.handle, False)
     dom = max(out, key=lambda t: out[t]["avg_ms"])
     ach = out[dom]["tflops"]
     peak = PEAK[act] / 1e12
-    traffic = traffic_from_profile(dom, act)
+    ttag = f"{dom}_{tag}" if tag else dom
+    traffic = traffic_from_profile(ttag, act)
     roof = {"bound": "mfma", "achieved": round(ach, 3), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(ach / peak, 4), "traffic": traffic, "kernel": f"gemm {dom} ({act})",
-            "flops_per_launch": flops, "avg_ms": round(out[dom]["avg_ms"], 5)}
+            "frac": round(ach / peak, 4), "traffic": traffic,
+            "kernel": f"gemm {dom} ({act}{', ' + tag if tag else ''})",
+            "flops_per_launch": flops, "avg_ms": round(out[dom]["avg_ms"], 5),
+            "traffic_profile": f"profiles/traffic_{ttag}_{act}.md"}
     return roof, out
 
 
@@ -263,35 +268,105 @@ def calib_copy():
 
 
 # ------------------------------------------------------------------ CPU oracle
-def cpu_baseline(min_seconds=10.0):
-    import numpy as np
-    from oracle import ttm as OT
-    from paper_2405_14377_amd import workloads as wl
-    w = wl.WORKLOADS[1]
-    sh = w.layers[0]
-    inp = wl.ttm_layer_inputs(1, 0, sh, w.mask)
-    b = w.batch
-    X = wl.activations(1, b, sh.n_in, 0, "f32")
-    dY = wl.activations(1, b, sh.n_out, 1, "f32")
-    threads = None
+def cpu_info():
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
     try:
         from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 0) for i in threadpool_info()), default=None)
+        blas = max((i.get("num_threads", 0) for i in threadpool_info()), default=None)
     except Exception:
         pass
+    return model, len(os.sched_getaffinity(0)), blas
+
+
+def _time_reps(fn, min_s):
     reps, t0 = 0, time.perf_counter()
     while True:
-        OT.forward_dense(X, inp.cores, inp.masks)
-        OT.backward_dense(X, dY, inp.cores, inp.masks)
+        fn()
         reps += 1
         el = time.perf_counter() - t0
-        if el >= min_seconds or reps >= 1000:
-            break
-    tok_s = reps * b / el
-    return {"value": round(tok_s, 1), "unit": "tokens/s", "cores": threads or len(os.sched_getaffinity(0)),
-            "kind": "oracle",
-            "sample": f"{reps} full steps (4096 tokens each) of the 768->3072 fp32 layer, fp64 dense-W route "
-                      f"(forward_dense + backward_dense), {el:.1f} s"}
+        if el >= min_s:
+            return reps, el
+
+
+def _ttm_route_rate(wid, tokens, route, min_s):
+    """tokens/s of one oracle route over every layer of a workload, on its
+    first `tokens` tokens (the same rows the GPU gets; work per token is
+    constant, so the rate is exact in work)."""
+    from oracle import ttm as OT
+    from paper_2405_14377_amd import workloads as wl
+    w = wl.WORKLOADS[wid]
+    act = w.dtypes[-1]
+    data = []
+    for li, sh in enumerate(w.layers):
+        inp = wl.ttm_layer_inputs(wid, li, sh, w.mask)
+        X = wl.activations(wid, tokens, sh.n_in, 0, act, layer=li)
+        dY = wl.activations(wid, tokens, sh.n_out, 1, act, layer=li)
+        data.append((X, dY, inp.cores, inp.masks))
+    if route == "dense":
+        fwd, bwd = OT.forward_dense, OT.backward_dense
+    else:
+        fwd, bwd = OT.forward_direct, OT.backward_direct
+
+    def step():
+        for X, dY, cores, masks in data:
+            fwd(X, cores, masks)
+            bwd(X, dY, cores, masks)
+    reps, el = _time_reps(step, min_s)
+    return {"tokens_per_s": round(reps * tokens / el, 1), "tokens": tokens, "reps": reps, "seconds": round(el, 2),
+            "layers": len(w.layers), "dtype_in": act}
+
+
+def _embed_rate(tokens, min_s):
+    import numpy as np
+    from oracle import embed as OE
+    from paper_2405_14377_amd import workloads as wl
+    w = wl.WORKLOADS[3]
+    cores = wl.embed_cores(w)
+    V, E = int(np.prod(w.v)), int(np.prod(w.e))
+    ids = wl.token_ids(w.n_tokens, V, "zipf1.1", wl.seed_of(3, 20))[:tokens]
+    dY = np.random.default_rng(wl.seed_of(3, 1)).standard_normal((tokens, E)).astype(np.float32)
+
+    def step():
+        OE.forward(ids, cores)
+        OE.backward(ids, dY, cores)
+    reps, el = _time_reps(step, min_s)
+    return {"tokens_per_s": round(reps * tokens / el, 1), "tokens": tokens, "reps": reps, "seconds": round(el, 2),
+            "ids": "zipf1.1"}
+
+
+def cpu_baseline():
+    """The fp64 oracle as it stands, on the host cores: the headline workload
+    (the 1024 <-> 4096 pair, both layers) on a 1024-token slice by the dense-W
+    route (the value) and on a 128-token slice by the direct route; the
+    768 -> 768 and 768 -> 3072 layers at full size, the six encoder layers on
+    a 1024-token slice, the embedding on a 2048-token slice."""
+    model, aff, blas = cpu_info()
+    head = _ttm_route_rate(HEADLINE_WID, 1024, "dense", 5.0)
+    direct = _ttm_route_rate(HEADLINE_WID, 128, "direct", 2.0)
+    others = {
+        "w0_768x768_full_dense_w": _ttm_route_rate(0, 32, "dense", 1.0),
+        "w0_768x768_full_direct": _ttm_route_rate(0, 32, "direct", 1.0),
+        "w1_768x3072_full_dense_w": _ttm_route_rate(1, 4096, "dense", 1.0),
+        "w1_768x3072_slice256_direct": _ttm_route_rate(1, 256, "direct", 1.0),
+        "w2_encoder6_slice1024_dense_w": _ttm_route_rate(2, 1024, "dense", 1.0),
+        "w3_embedding_slice2048": _embed_rate(2048, 1.0),
+    }
+    cores = min(aff, blas) if blas else aff
+    return {"value": head["tokens_per_s"], "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{head['reps']} steps of the 1024<->4096 d4 r64 pair (both layers) on its first 1024 tokens "
+                      f"(bf16-rounded inputs, fp64 math), dense-W route (forward_dense + backward_dense), "
+                      f"{head['seconds']} s",
+            "cpu_model": model, "affinity_cpus": aff, "blas_threads": blas,
+            "direct_route": direct, "other_configs": others}
 
 
 # ------------------------------------------------------------------ other workloads
@@ -313,7 +388,7 @@ def other_workloads(steps, warmup):
     from paper_2405_14377_amd import workloads as wl
     res = {}
     # TTM layer workloads
-    for wid, act in ((0, "f32"), (1, "bf16"), (2, "bf16"), (4, "bf16"), (5, "f32"), (5, "bf16")):
+    for wid, act in ((0, "f32"), (2, "bf16"), (5, "f32"), (5, "bf16")):
         w = wl.WORKLOADS[wid]
         layers, dense = [], []
         for li in range(len(w.layers)):
@@ -336,7 +411,7 @@ def other_workloads(steps, warmup):
                  "tflops_algorithmic": round(fl_alg / (ms * 1e-3) / 1e12, 2),
                  "dense_ms_per_step": round(dms, 4), "speedup_vs_dense": round(dms / ms, 3),
                  "graph": graph_entry(gms, gerr, dgms, dgerr)}
-        if wid in (1, 2, 4):
+        if wid == 2:
             roofs = [kernel_roofline(l, max(2, k // 2), act)[1] for l in layers]
             entry["kernels_ms"] = [{t: round(v["avg_ms"], 4) for t, v in r.items()} for r in roofs]
         entry["orders"] = [l.plan.order_info(l.plan.chosen)["desc"] for l in layers]
@@ -524,7 +599,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
-    ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"], help="dtype of the reported value")
+    ap.add_argument("--dtype", default="bf16", choices=["f32", "bf16"], help="dtype tag of a traffic summary")
+    ap.add_argument("--headline-only", action="store_true", help="only the headline workload (profiling runs)")
     ap.add_argument("--calib-copy", action="store_true", help="also run a plain device copy of known size")
     ap.add_argument("--stats-summary", nargs=3, metavar=("PROF_DIR", "OUT_MD", "COMMAND"),
                     help="write a kernel-statistics table from a rocprofv3 run (no GPU)")
@@ -563,8 +639,55 @@ def main():
         torch.cuda.synchronize()
 
 
-def run_gpu(args):
+def run_layers(wid, act, steps, warmup, seed_base, roof_tag=None):
+    """Time whole steps (every layer of workload wid, forward then backward)
+    beside the dense GEMMs of the same shapes, eager and under graph replay;
+    with roof_tag, also the per-kernel roofline of each layer."""
     import torch
+    from paper_2405_14377_amd import workloads as wl
+    w = wl.WORKLOADS[wid]
+    layers, dense = [], []
+    for li in range(len(w.layers)):
+        sh, inp, X, dY, G, D, ma, b = layer_inputs(wid, li, act, seed_base + li)
+        layers.append(Layer(sh, X, dY, G, D, ma, b, act))
+        dense.append(dense_step_fn(sh, X, dY))
+    b = w.batch
+
+    def step():
+        for lay in layers:
+            lay.step()
+
+    def dstep():
+        for f in dense:
+            f()
+    log(f"[bench] {w.name} {act}: warmup {warmup}, timing {steps} steps")
+    torch.cuda.synchronize()
+    ms, wall = time_loop(step, steps, warmup)
+    dms, _ = time_loop(dstep, steps, warmup)
+    gms, gerr = graph_loop(step, steps, warmup)
+    dgms, dgerr = graph_loop(dstep, steps, warmup)
+    res = {"workload": w.name, "dtype": act, "tokens": b, "layers": len(layers), "ms_per_step": ms, "wall_s": wall,
+           "tokens_per_s": b / (ms * 1e-3), "dense_ms": dms, "speedup_vs_dense": dms / ms,
+           "graph": graph_entry(gms, gerr, dgms, dgerr),
+           "orders": [lay.plan.order_info(lay.plan.chosen)["desc"] for lay in layers]}
+    if gms is not None:
+        res["graph"]["tokens_per_s"] = round(b / (gms * 1e-3), 1)
+    if roof_tag is not None:
+        roofs, kerns = [], {}
+        for lay in layers:
+            tag = f"{roof_tag}_{lay.sh.name}" if len(layers) > 1 else roof_tag
+            roof, kern = kernel_roofline(lay, steps, act, tag)
+            roofs.append(roof)
+            kerns[lay.sh.name] = {t: round(v["avg_ms"], 5) for t, v in kern.items()}
+        res["roofline"] = max(roofs, key=lambda r: r["avg_ms"])
+        res["kernels_ms"] = kerns
+    log(f"[bench]   {ms:.4f} ms/step, dense {dms:.4f} ms")
+    del layers, dense
+    torch.cuda.empty_cache()
+    return res
+
+
+def run_gpu(args):
     if args.orders is not None:
         wids = args.orders or [0, 1, 5]
         for rec in order_timings(wids, args.steps, args.warmup):
@@ -573,29 +696,7 @@ def run_gpu(args):
     if args.fp8_only:
         print(json.dumps(fp8_workloads(args.steps, args.warmup)), flush=True)
         return
-    runs = {}
-    for act in ("f32", "bf16"):
-        sh, inp, X, dY, G, D, ma, b = layer_inputs(1, 0, act, 1000 + (act == "bf16"))
-        layer = Layer(sh, X, dY, G, D, ma, b, act)
-        log(f"[bench] ttm 768x3072 {act}: warmup {args.warmup}, timing {args.steps} steps")
-        torch.cuda.synchronize()
-        ms, wall = time_loop(layer.step, args.steps, args.warmup)
-        dfn = dense_step_fn(sh, X, dY)
-        dms, _ = time_loop(dfn, args.steps, args.warmup)
-        gms, gerr = graph_loop(layer.step, args.steps, args.warmup)
-        dgms, dgerr = graph_loop(dfn, args.steps, args.warmup)
-        roof, kern = kernel_roofline(layer, args.steps, act)
-        runs[act] = {"ms_per_step": ms, "wall_s": wall, "tokens_per_s": b / (ms * 1e-3), "dense_ms": dms,
-                     "speedup_vs_dense": dms / ms, "roofline": roof,
-                     "kernels_ms": {t: round(v["avg_ms"], 5) for t, v in kern.items()},
-                     "graph": graph_entry(gms, gerr, dgms, dgerr)}
-        if gms is not None:
-            runs[act]["graph"]["tokens_per_s"] = round(b / (gms * 1e-3), 1)
-        log(f"[bench]   {ms:.4f} ms/step, dense {dms:.4f} ms, dominant {roof['kernel']} {roof['achieved']} TF/s")
-        del layer
-        torch.cuda.empty_cache()
-    main_run = runs[args.dtype]
-    sh = None
+    main_run = run_layers(HEADLINE_WID, "bf16", args.steps, args.warmup, 4000, roof_tag="ttm1024x4096")
     out = {
         "metric": METRIC,
         "value": round(main_run["tokens_per_s"], 1),
@@ -607,31 +708,34 @@ def run_gpu(args):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": args.dtype,
+        "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) activations, cores scaled for unit output variance)",
-        "config": {"workload": "ttm_ffn_up_768x3072_n8x8x12_m16x16x12_r30_mask0.8_b4096",
-                   "global_batch": 4096, "parallelism": "none (1 GPU)"},
+        "config": {"workload": "ttm_pair_1024x4096_4096x1024_d4_r64_mask0.7_b65536_bf16 (both layers per step)",
+                   "global_batch": 65536, "parallelism": "none (1 GPU)"},
         "roofline": main_run["roofline"],
         "speedup_vs_dense_gemm": round(main_run["speedup_vs_dense"], 3),
         "dense_gemm_ms_per_step": round(main_run["dense_ms"], 5),
         "kernels_ms": main_run["kernels_ms"],
+        "orders": main_run["orders"],
         "graph_replay": main_run["graph"],
         "stream": "one dedicated stream (default priority) for every GPU call, ours and the baseline's",
     }
-    other = "bf16" if args.dtype == "f32" else "f32"
-    r = runs[other]
-    out[f"{other}_run"] = {"value": round(r["tokens_per_s"], 1), "ms_per_step": round(r["ms_per_step"], 5),
-                           "speedup_vs_dense_gemm": round(r["speedup_vs_dense"], 3),
-                           "dense_gemm_ms_per_step": round(r["dense_ms"], 5), "roofline": r["roofline"],
-                           "kernels_ms": r["kernels_ms"], "graph_replay": r["graph"]}
+    if not args.headline_only:
+        for act in ("f32", "bf16"):
+            r = run_layers(1, act, args.steps, args.warmup, 1000 + (act == "bf16"), roof_tag="ttm768x3072")
+            out[f"ttm768x3072_{act}"] = {
+                "value": round(r["tokens_per_s"], 1), "ms_per_step": round(r["ms_per_step"], 5),
+                "speedup_vs_dense_gemm": round(r["speedup_vs_dense"], 3),
+                "dense_gemm_ms_per_step": round(r["dense_ms"], 5), "roofline": r["roofline"],
+                "kernels_ms": r["kernels_ms"], "graph_replay": r["graph"]}
     if args.calib_copy:
         calib_copy()
-    if not args.no_extra:
+    if not args.no_extra and not args.headline_only:
         log("[bench] other workloads")
         out["other_workloads"] = other_workloads(max(5, args.steps // 2), 3)
         log("[bench] mixed-precision (FP8) layers")
         out["fp8_layers"] = fp8_workloads(max(5, args.steps // 2), 3)
-    if not args.no_cpu:
+    if not args.no_cpu and not args.headline_only:
         log("[bench] CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline()
     else:
