@@ -601,6 +601,9 @@ def main():
     ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
     ap.add_argument("--dtype", default="bf16", choices=["f32", "bf16"], help="dtype tag of a traffic summary")
     ap.add_argument("--headline-only", action="store_true", help="only the headline workload (profiling runs)")
+    ap.add_argument("--workload", type=int, default=None, metavar="WID",
+                    help="only this workload's steps (3 = the embedding), eager, one JSON line (profiling runs)")
+    ap.add_argument("--act", default="bf16", choices=["f32", "bf16"], help="activation dtype for --workload")
     ap.add_argument("--calib-copy", action="store_true", help="also run a plain device copy of known size")
     ap.add_argument("--stats-summary", nargs=3, metavar=("PROF_DIR", "OUT_MD", "COMMAND"),
                     help="write a kernel-statistics table from a rocprofv3 run (no GPU)")
@@ -687,7 +690,41 @@ def run_layers(wid, act, steps, warmup, seed_base, roof_tag=None):
     return res
 
 
+def embed_steps(dist, steps, warmup):
+    """The embedding training step (forward, then backward on the forward's
+    prefix table) for one id distribution; eager."""
+    import numpy as np
+    import torch
+    from paper_2405_14377_amd import comera as C
+    from paper_2405_14377_amd import workloads as wl
+    w = wl.WORKLOADS[3]
+    dev = torch.device("cuda", 0)
+    cores = [torch.from_numpy(c).to(dev) for c in wl.embed_cores(w)]
+    shape = C.tt_embed_shape(w.v, w.e, w.r)
+    V, E, n = int(np.prod(w.v)), int(np.prod(w.e)), w.n_tokens
+    ws = torch.empty(C.comera_tt_embed_workspace_bytes(shape, n), dtype=torch.uint8, device=dev)
+    Y = torch.empty((n, E), device=dev)
+    dG = [torch.empty_like(c) for c in cores]
+    g = torch.Generator(device=dev)
+    g.manual_seed(3000)
+    dYe = torch.randn((n, E), generator=g, device=dev)
+    ids = torch.from_numpy(wl.token_ids(n, V, dist, wl.seed_of(3, 20))).to(dev)
+
+    def step():
+        C.comera_tt_embed_forward(shape, ids, n, cores, None, Y, ws, None, None)
+        C.comera_tt_embed_backward_ex(shape, ids, n, dYe, cores, None, dG, C.EMBED_REUSE_FORWARD, ws, None, None)
+    ms, _ = time_loop(step, steps, warmup)
+    return {"workload": w.name, "ids": dist, "ms_per_step": round(ms, 5), "tokens_per_s": round(n / (ms * 1e-3), 1)}
+
+
 def run_gpu(args):
+    if args.workload is not None:
+        if args.workload == 3:
+            print(json.dumps([embed_steps(dist, args.steps, args.warmup) for dist in ("zipf1.1", "uniform")]))
+        else:
+            r = run_layers(args.workload, args.act, args.steps, args.warmup, 1000 * args.workload)
+            print(json.dumps(r))
+        return
     if args.orders is not None:
         wids = args.orders or [0, 1, 5]
         for rec in order_timings(wids, args.steps, args.warmup):

@@ -74,6 +74,8 @@ typedef enum { COMERA_F32 = 0, COMERA_BF16 = 1 } comera_dtype;
 #define COMERA_ORDER_SWEEP_RL 1   /* several groups, X swept from the last group */
 #define COMERA_ORDER_SWEEP_LR 2   /* several groups, X swept from the first group */
 #define COMERA_ORDER_ZERO 3       /* some bond has no active mask entry: W == 0 */
+#define COMERA_ORDER_FUSED_RL 4   /* every core its own group, X swept from the last core by
+                                     fused kernels with the per-token states in LDS */
 
 /* Shape of one TTM linear layer (Sec. 2 eq. TTM, Sec. 4.2).
  * Core k (0-based) is G_k[r[k], m[k], n[k], r[k+1]], fp32 row-major.
@@ -110,13 +112,17 @@ typedef struct comera_ttm_plan_s *comera_ttm_plan_t;
  * Orders are numbered deterministically: index 0 is the dense order (one
  * group); then for each composition of the cores into >= 2 consecutive
  * groups, in increasing order of its cut bit mask, the right-to-left sweep
- * and then the left-to-right sweep.  d = 3 gives 7 orders, d = 4 gives 15.
- * Ties in predicted time go to the lowest index. */
+ * and then the left-to-right sweep; last, the fused single-core sweep
+ * (COMERA_ORDER_FUSED_RL: one forward kernel, one backward kernel plus the
+ * fixed-order sum of its per-workgroup core-gradient partials; executable
+ * when the per-token states fit the LDS of a CU and the compacted ranks are
+ * at most 64).  d = 3 gives 8 orders, d = 4 gives 16.  Ties in predicted
+ * time go to the lowest index. */
 comera_status comera_ttm_plan(const comera_ttm_shape *s, int64_t batch,
                               const uint8_t *mask_active, int32_t force_order,
                               comera_ttm_plan_t *out);
 
-/* Number of enumerated orders (2^d - 1), or 0 for a NULL plan. */
+/* Number of enumerated orders (2^d), or 0 for a NULL plan. */
 int32_t comera_ttm_plan_num_orders(comera_ttm_plan_t p);
 
 /* Index of the order the plan executes. */

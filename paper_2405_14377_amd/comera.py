@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libcomera.so")
 MAX_CORES = 8
 F32, BF16 = 0, 1
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_INTERNAL = 0, -1, -2, -3, -4, -5
-ORDER_DENSE, ORDER_SWEEP_RL, ORDER_SWEEP_LR, ORDER_ZERO = 0, 1, 2, 3
+ORDER_DENSE, ORDER_SWEEP_RL, ORDER_SWEEP_LR, ORDER_ZERO, ORDER_FUSED_RL = 0, 1, 2, 3, 4
 
 # every function declared in include/comera.h
 EXPORTS = (

@@ -516,6 +516,7 @@ comera_status comera_ttm_forward(comera_ttm_plan_t p, int64_t b, const void *X, 
     for (int k = 0; k < p->d; ++k)
         if (!G[k]) return COMERA_ERR_INVALID_ARG;
     if (!ws || ws_bytes < p->ws_bytes) return COMERA_ERR_WORKSPACE;
+    if (p->chain) return chain_forward(p, b, X, G, D, Y, ws, stream);
     if (p->sweep.G > 0) return sweep_forward(p, b, X, G, D, Y, ws, stream);
     if (p->fp8) return fp8_forward(p, b, X, G, D, Y, ws, stream);
     return dense_forward(p, b, X, G, D, Y, ws, true, stream);
@@ -533,7 +534,7 @@ comera_status comera_ttm_forward_noalloc(comera_ttm_plan_t p, int64_t b, const v
     if (!G) return COMERA_ERR_INVALID_ARG;
     for (int k = 0; k < p->d; ++k)
         if (!G[k]) return COMERA_ERR_INVALID_ARG;
-    if (p->sweep.G > 0 || p->fp8 || p->reuse) return COMERA_ERR_UNSUPPORTED;
+    if (p->chain || p->sweep.G > 0 || p->fp8 || p->reuse) return COMERA_ERR_UNSUPPORTED;
     // the unsplit forward of the dense order touches the folded cores, the
     // left chains, W, W^T and the 1.0 cell: every region before the dX partials
     if (p->dense.ones + sizeof(float) > kNoAllocScratchBytes) return COMERA_ERR_UNSUPPORTED;
@@ -631,6 +632,7 @@ comera_status backward_impl(comera_ttm_plan_t p, int64_t b, const void *X, const
     for (int k = 0; k < d; ++k)
         if (!G[k]) return COMERA_ERR_INVALID_ARG;
     if (!ws || ws_bytes < p->ws_bytes) return COMERA_ERR_WORKSPACE;
+    if (p->chain) return chain_backward(p, b, X, dY, G, D, dX, want_dg ? dG : nullptr, dD, ws, stream);
     if (p->sweep.G > 0) return sweep_backward(p, b, X, dY, G, D, dX, want_dg ? dG : nullptr, dD, ws, stream);
     const DenseLayout &L = p->dense;
     DenseBuild bd;

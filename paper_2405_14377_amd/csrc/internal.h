@@ -126,6 +126,46 @@ struct KernelTiming {
 };
 }  // namespace comera
 
+namespace comera {
+// Fused single-core sweep (chain.hip): the forward and the backward of a
+// whole layer, one workgroup per TB tokens at a time, states in LDS.  Ranks
+// are the compacted ones (rc), amap[k][x] is the full index of compacted
+// entry x of bond k (k = 1 .. d-1); every offset below is in floats.
+constexpr int kChainMaxRank = 64;
+struct ChainArgs {
+    const float *G[kMaxCores];
+    const float *D[kMaxCores];
+    uint8_t amap[kMaxCores + 1][kChainMaxRank];
+    int d, TB, act_bf16;
+    int r[kMaxCores + 1], rc[kMaxCores + 1], m[kMaxCores], n[kMaxCores];
+    int Nl[kMaxCores], Mg[kMaxCores];   // prod of n before core k, prod of m after core k
+    int ssz[kMaxCores + 1];             // floats of state k per token
+    int cm[kMaxCores], km[kMaxCores];   // folded cores, c-major and k-major
+    int st0, st1;                       // ping-pong state buffers
+    int sk[kMaxCores + 1];              // backward: forward states S_1 .. S_d
+    int tab;                            // backward: row tables of the meets (ints)
+    int want[kMaxCores];                // backward: core gradients asked for
+    int64_t b;
+    const void *X, *dY;
+    void *Y, *dX;
+    float *part;                        // backward: partials of the masked-core gradients, core k at
+    int64_t poff[kMaxCores];            // part + poff[k] as [grid][rc_k m_k n_k rc_{k+1}]
+    size_t lds_bytes;
+};
+}  // namespace comera
+
+namespace comera {
+// The fused single-core sweep of a plan: kernel arguments with the geometry
+// filled in (forward and backward), grids, and the workspace region of the
+// backward's core-gradient partials.
+struct ChainLayout {
+    ChainArgs fa, ba;
+    int grid_f = 0, grid_b = 0;
+    size_t part = 0;
+    size_t total = 0;
+};
+}  // namespace comera
+
 struct comera_ttm_plan_s {
     comera_ttm_shape s;
     int64_t batch = 0;
@@ -139,6 +179,8 @@ struct comera_ttm_plan_s {
     int chosen = 0;
     comera::DenseLayout dense;
     comera::SweepLayout sweep;                    // when the chosen order is a sweep
+    bool chain = false;                           // the chosen order is the fused single-core sweep
+    comera::ChainLayout ch;
     std::unique_ptr<comera_ttm_plan_s> sub[comera::kMaxCores];   // one layer per sweep group
     size_t ws_bytes = 0;
     bool reuse = false;                           // backward reuses the forward's build
@@ -424,6 +466,19 @@ int mask_grads(const comera_ttm_plan_s *p, const float *const *part, const int *
                const float *const *G, float *const *dD, void *stream);
 // out[t][j][i] = in[t][i][j] for t < b, i < M, j < T (elements of esz bytes)
 int launch_permute_tokens(const void *in, void *out, int64_t b, int64_t M, int64_t T, int esz, void *stream);
+
+// fills the size fields for TB tokens per workgroup; false when they do not
+// fit the LDS of a CU
+bool chain_fits(ChainArgs &a, int64_t b, bool backward, int TB);
+int launch_chain(const ChainArgs &a, bool backward, int grid, void *stream);
+// geometry, grids and workspace of the fused order of plan p; false when the
+// layer is outside the fused kernels' limits
+bool layout_chain(const comera_ttm_plan_s *p, ChainLayout &L);
+comera_status chain_forward(const comera_ttm_plan_s *p, int64_t b, const void *X, const float *const *G,
+                            const float *const *D, void *Y, void *ws, void *stream);
+comera_status chain_backward(const comera_ttm_plan_s *p, int64_t b, const void *X, const void *dY,
+                             const float *const *G, const float *const *D, void *dX, float *const *dG,
+                             float *const *dD, void *ws, void *stream);
 
 // sweep orders (sweep.hip)
 comera_status sweep_forward(const comera_ttm_plan_s *p, int64_t b, const void *X, const float *const *G,

@@ -52,7 +52,8 @@ void describe(Order &o, int d) {
     char buf[160];
     int pos = 0;
     const char *name = o.kind == COMERA_ORDER_DENSE ? "dense" : o.kind == COMERA_ORDER_SWEEP_RL ? "sweep-rl"
-                       : o.kind == COMERA_ORDER_SWEEP_LR ? "sweep-lr" : "zero";
+                       : o.kind == COMERA_ORDER_SWEEP_LR ? "sweep-lr" : o.kind == COMERA_ORDER_FUSED_RL ? "fused-rl"
+                       : "zero";
     pos += snprintf(buf + pos, sizeof(buf) - pos, "%s [", name);
     for (int k = 0; k < d; ++k) {
         pos += snprintf(buf + pos, sizeof(buf) - pos, "%d", k);
@@ -117,6 +118,31 @@ void cost_order(const comera_ttm_plan_s *p, Order &o) {
         const int dg = g.second - g.first + 1;
         const double steps = dg > 1 ? dg - 1 : (p->s.act == COMERA_BF16 || o.kind == COMERA_ORDER_DENSE ? 1 : 0);
         t_build += steps * kLaunch + gd.back().build_flops / (0.5 * kPeakF32);
+    }
+    if (o.kind == COMERA_ORDER_FUSED_RL) {
+        // per token, core k (0-based) is a product of (prod n before k) x
+        // (prod m after k) rows, n_k rho_{k+1} contraction and rho_k m_k
+        // columns; the backward recomputes the forward states (all but the
+        // last step), sweeps dY and takes one meet per core of the same size
+        double f_all = 0, f_first = 0;
+        for (int k = 0; k < d; ++k) {
+            double nl = 1, mg = 1;
+            for (int h = 0; h < k; ++h) nl *= double(p->s.n[h]);
+            for (int h = k + 1; h < d; ++h) mg *= double(p->s.m[h]);
+            const double f = 2.0 * nl * mg * double(p->s.n[k]) * double(p->rho[k + 1]) * double(p->rho[k]) *
+                             double(p->s.m[k]);
+            f_all += f;
+            if (k == 0) f_first = f;
+        }
+        o.flops_fwd = b * f_all;
+        o.flops_bwd = b * (f_all - f_first + 2.0 * f_all);
+        o.bytes = b * (2.0 * Nin + 2.0 * Nout) * esz;
+        // one CU per workgroup (token) on fp32 MFMA fed from LDS at a quarter
+        // of its rate; launches: forward, backward, expand of the partials
+        const double cus = std::min(b, 256.0);
+        o.t_pred = 3.0 * kLaunch + (o.flops_fwd + o.flops_bwd) / (0.25 * (kPeakF32 / 256.0) * cus) +
+                   o.bytes / kHbm;
+        return;
     }
     if (o.kind == COMERA_ORDER_DENSE) {
         const double proj = proj_flops(p, 0, d - 1, 1.0, 1.0);
@@ -604,6 +630,13 @@ comera_status comera_ttm_plan(const comera_ttm_shape *s, int64_t batch, const ui
             p->orders.push_back(o);
         }
     }
+    {
+        // every core its own group, swept right to left by the fused kernels
+        Order o;
+        o.kind = COMERA_ORDER_FUSED_RL;
+        o.cuts = (1u << (d - 1)) - 1u;
+        p->orders.push_back(o);
+    }
     for (auto &o : p->orders) {
         describe(o, d);
         if (p->zero) {
@@ -619,6 +652,9 @@ comera_status comera_ttm_plan(const comera_ttm_shape *s, int64_t batch, const ui
             cost_order(p, o);
             if (o.kind == COMERA_ORDER_DENSE) {
                 o.executable = true;
+            } else if (o.kind == COMERA_ORDER_FUSED_RL) {
+                ChainLayout cl;
+                o.executable = layout_chain(p, cl);
             } else {
                 SweepLayout sl;
                 std::unique_ptr<comera_ttm_plan_s> tmp[kMaxCores];
@@ -650,6 +686,13 @@ comera_status comera_ttm_plan(const comera_ttm_shape *s, int64_t batch, const ui
         if (o.kind == COMERA_ORDER_DENSE) {
             layout_dense(p);
             p->ws_bytes = p->dense.total;
+        } else if (o.kind == COMERA_ORDER_FUSED_RL) {
+            if (!layout_chain(p, p->ch)) {
+                delete p;
+                return COMERA_ERR_INTERNAL;
+            }
+            p->chain = true;
+            p->ws_bytes = p->ch.total;
         } else {
             if (!layout_sweep(p, o.kind, o.cuts, p->sweep, p->sub)) {
                 delete p;

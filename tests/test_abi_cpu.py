@@ -42,10 +42,10 @@ def test_status_strings():
 @pytest.mark.parametrize("d", [1, 2, 3, 4, 5])
 def test_order_count(d):
     p = C.TTMPlan([2] * d, [3] * d, [1] + [2] * (d - 1) + [1], batch=8)
-    assert p.num_orders == 2 ** d - 1
+    assert p.num_orders == 2 ** d
     assert p.order_info(0)["kind"] == C.ORDER_DENSE
     kinds = [p.order_info(i)["kind"] for i in range(1, p.num_orders)]
-    assert kinds == [C.ORDER_SWEEP_RL, C.ORDER_SWEEP_LR] * (2 ** (d - 1) - 1)
+    assert kinds == [C.ORDER_SWEEP_RL, C.ORDER_SWEEP_LR] * (2 ** (d - 1) - 1) + [C.ORDER_FUSED_RL]
     # every order of a small layer can run; the choice is one of them
     assert all(p.order_info(i)["executable"] for i in range(p.num_orders))
     assert 0 <= p.chosen < p.num_orders
@@ -53,9 +53,9 @@ def test_order_count(d):
 
 def test_order_descriptions_d3():
     p = C.TTMPlan((8, 8, 12), (12, 8, 8), (1, 8, 8, 1), batch=32)
-    descs = [p.order_info(i)["desc"] for i in range(7)]
+    descs = [p.order_info(i)["desc"] for i in range(8)]
     assert descs == ["dense [0,1,2]", "sweep-rl [0][1,2]", "sweep-lr [0][1,2]", "sweep-rl [0,1][2]",
-                     "sweep-lr [0,1][2]", "sweep-rl [0][1][2]", "sweep-lr [0][1][2]"]
+                     "sweep-lr [0,1][2]", "sweep-rl [0][1][2]", "sweep-lr [0][1][2]", "fused-rl [0][1][2]"]
 
 
 def _rank24_masks():
@@ -83,6 +83,11 @@ def test_flops_ffn_up_rank24():
     assert info["sweep-lr [0][1][2]"]["flops_fwd"] / 1e9 == pytest.approx(125.6, abs=0.1)
     assert info["sweep-rl [0][1,2]"]["flops_fwd"] / 1e9 == pytest.approx(33.84, abs=0.01)
     assert info["sweep-rl [0,1][2]"]["flops_fwd"] / 1e9 == pytest.approx(40.49, abs=0.01)
+    # the fused single-core sweep runs the same batch contractions in its
+    # forward (no batch-free build); its backward recomputes every forward
+    # step but the last, sweeps dY and meets at every core: 3 s - s0
+    assert info["fused-rl [0][1][2]"]["flops_fwd"] == pytest.approx(s2 + s1 + s0, rel=1e-12)
+    assert info["fused-rl [0][1][2]"]["flops_bwd"] == pytest.approx(3 * (s2 + s1 + s0) - s0, rel=1e-12)
     # the dense order is the cheapest forward here
     assert min(info.values(), key=lambda o: o["flops_fwd"])["desc"] == "dense [0,1,2]"
 
@@ -131,7 +136,7 @@ def test_plan_errors():
     assert st == C.ERR_INVALID_ARG
     st, _ = C.comera_ttm_plan(C.ttm_shape((2, 2), (2, 2), (1, 2, 1), act=7), 4, raise_on_error=False)
     assert st == C.ERR_INVALID_ARG
-    st, _ = C.comera_ttm_plan(C.ttm_shape((2, 2), (2, 2), (1, 2, 1)), 4, force_order=3, raise_on_error=False)
+    st, _ = C.comera_ttm_plan(C.ttm_shape((2, 2), (2, 2), (1, 2, 1)), 4, force_order=4, raise_on_error=False)
     assert st == C.ERR_INVALID_ARG
     st, _ = C.comera_ttm_plan(C.ttm_shape((2, 2), (2, 2), (1, 2, 1)), -1, raise_on_error=False)
     assert st == C.ERR_INVALID_ARG

@@ -180,3 +180,27 @@ def test_sweep_backward_bitwise_deterministic():
     assert torch.equal(dX1, dX2)
     for a, b in zip(dG1, dG2):
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+@pytest.mark.parametrize("b", [1, 513, 1537, 5000])
+def test_fused_order_token_groups(b, act):
+    """The fused single-core sweep with more tokens than workgroups (the
+    backward keeps at most 512 workgroups, each summing its token groups'
+    meets into its own partial in order; above 1024 tokens the forward takes
+    several tokens per workgroup): the oracle's Y, dX and every dG_k, and a
+    second backward bit for bit equal to the first."""
+    import torch
+    n, m, r = (3, 4, 2), (2, 5, 3), (1, 5, 4, 1)
+    cores, D, X, dY = _inputs(40 + b, n, m, r, b, act)
+    probe = C.TTMPlan(n, m, r, C.BF16 if act == "bf16" else C.F32, batch=b)
+    last = probe.num_orders - 1
+    assert probe.order_info(last)["kind"] == C.ORDER_FUSED_RL and probe.order_info(last)["executable"]
+    _all_orders(n, m, r, cores, D, X, dY, act, orders=[last])
+    run = TTMRun(n, m, r, cores, D, b, act, force_order=last)
+    Xt, dYt = to_dev(X, act), to_dev(dY, act)
+    dX1, dG1 = run.backward(Xt, dYt)
+    dX2, dG2 = run.backward(Xt, dYt)
+    assert torch.equal(dX1, dX2)
+    for g1, g2 in zip(dG1, dG2):
+        assert torch.equal(g1, g2)
