@@ -140,7 +140,12 @@ struct ChainArgs {
     int r[kMaxCores + 1], rc[kMaxCores + 1], m[kMaxCores], n[kMaxCores];
     int Nl[kMaxCores], Mg[kMaxCores];   // prod of n before core k, prod of m after core k
     int ssz[kMaxCores + 1];             // floats of state k per token
+    int cstart[kMaxCores + 1];          // first element of core k in one flat index over the cores
+    int smap;                           // LDS copy of amap (ints)
     int cm[kMaxCores], km[kMaxCores];   // folded cores, c-major and k-major
+    int cp[kMaxCores], kp[kMaxCores];   // their row pitches (floats)
+    int compacted;                      // amap is not the identity
+    int wave0[kMaxCores + 1];           // staging: first wave of core k's block
     int st0, st1;                       // ping-pong state buffers
     int sk[kMaxCores + 1];              // backward: forward states S_1 .. S_d
     int tab;                            // backward: row tables of the meets (ints)
