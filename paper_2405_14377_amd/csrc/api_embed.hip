@@ -119,6 +119,17 @@ int build_prefix(const comera_tt_embed_shape *s, const EmbedLayout &L, const flo
                  void *ws, void *stream, float **gc, float **P) {
     const int d = s->d;
     if (d == 1) return 0;
+    if (d == 3 && embed_table_supported(int(s->r[1]), int(s->e[0]))) {
+        // one kernel: the table straight from the raw cores 0 and 1, and their
+        // folded copies for the backward's projections
+        gc[0] = reinterpret_cast<float *>(at(ws, L.gc[0]));
+        gc[1] = reinterpret_cast<float *>(at(ws, L.gc[1]));
+        P[1] = gc[0];
+        P[2] = reinterpret_cast<float *>(at(ws, L.p[2]));
+        return launch_embed_table(G[0], D ? D[0] : nullptr, G[1], D ? D[1] : nullptr, P[2], gc[0], gc[1],
+                                  int(s->v[0]), int(s->v[1]), int(s->e[0]), int(s->e[1]), int(s->r[1]),
+                                  int(s->r[2]), stream);
+    }
     FoldArgs fa;
     std::memset(&fa, 0, sizeof(fa));
     fa.d = d;

@@ -60,6 +60,12 @@ int launch_embed_dapre(const EmbedWs &w, const float *Gs, int64_t Vp, int Ep, in
 int launch_embed_dglast(const EmbedWs &w, const float *Apre, bool rank_major, int64_t Vp, int Ep, int R, int Vs,
                         int Es, void *stream);
 int embed_dglast_chunks(int64_t Vp);
+// prefix table of a three-core table straight from the raw cores 0 and 1
+// (masks folded on the fly), rank-major [v0 v1][r2][e0 e1]; also writes the
+// folded cores gc0 [v0][e0][r1] and gc1 [r1][v1][e1][r2]
+bool embed_table_supported(int r1, int e0);
+int launch_embed_table(const float *G0, const float *D0, const float *G1, const float *D1, float *A, float *gc0,
+                       float *gc1, int v0, int v1, int e0, int e1, int r1, int r2, void *stream);
 // d = 1: dG_0[0, v, e, 0] = S[headpos[v]][e] (0 for absent ids)
 int launch_embed_gather(const EmbedWs &w, int64_t V, int E, float *dG0, void *stream);
 // shapes the embedding kernels handle (LDS staging limits)

@@ -207,6 +207,78 @@ __global__ __launch_bounds__(256) void embed_rows_mfma_kernel(const int64_t *__r
     }
 }
 
+// ---------------------------------------------------------------- prefix table
+// Prefix table of a three-core table (eq. emb_A1): for prefix (z0, z1),
+//   A[(z0, z1)][a2][(e0, e1)] = sum_{a1} G~0[0][z0][e0][a1] G~1[a1][z1][e1][a2]
+// with the masks folded on the fly (G~0 = G0 D0 on a1, G~1 = G1 D1 on a2),
+// stored rank-major.  Workgroup (z1, block of kTabZ values of z0): the
+// block's G~0 rows are staged in LDS; thread (a2, e1) holds the column
+// G~1[:, z1, e1, a2] in registers and forms the kTabZ x e0 entries at its
+// (a2, e1) position; the block's kTabZ tables go out through LDS as
+// contiguous rows.  The workgroups of z0 block 0 also write the folded G~1
+// slice to gc1 ([r1][v1][e1][r2]) and those of z1 = 0 the folded G~0 rows to
+// gc0 ([v0][e0][r1]): the backward's prefix-core projections read them.
+constexpr int kTabZ = 4;
+template <int R1MAX>
+__global__ __launch_bounds__(256) void embed_table_kernel(const float *__restrict__ G0, const float *__restrict__ D0,
+                                                          const float *__restrict__ G1, const float *__restrict__ D1,
+                                                          float *__restrict__ A, float *__restrict__ gc0,
+                                                          float *__restrict__ gc1, int v0, int v1, int e0, int e1,
+                                                          int r1, int r2) {
+    extern __shared__ __attribute__((aligned(16))) float tl[];
+    const int z1 = blockIdx.x, zb = blockIdx.y * kTabZ;
+    const int nz = min(kTabZ, v0 - zb);
+    const int Ep = e0 * e1;
+    constexpr int r1p = R1MAX;                         // row pitch: the products below read whole rows
+    float *g0s = tl;                                   // [kTabZ][e0][r1p], zero past r1
+    float *out = g0s + kTabZ * e0 * r1p;               // [kTabZ][r2][Ep]
+    // the block's folded G~0 rows (and their copy in gc0 from z1 = 0)
+    for (int i = threadIdx.x; i < nz * e0 * r1p; i += blockDim.x) {
+        const int zl = i / (e0 * r1p), rem = i - zl * e0 * r1p, ee = rem / r1p, a1 = rem - ee * r1p;
+        const int a1c = min(a1, r1 - 1);
+        float v = G0[(int64_t(zb + zl) * e0 + ee) * r1 + a1c] * (D0 ? D0[a1c] : 1.f);
+        v = a1 < r1 ? v : 0.f;
+        if (a1 < r1 && z1 == 0) gc0[(int64_t(zb + zl) * e0 + ee) * r1 + a1] = v;
+        g0s[i] = v;
+    }
+    __syncthreads();
+    for (int p = threadIdx.x; p < r2 * e1; p += blockDim.x) {
+        // consecutive threads take consecutive e1 (consecutive LDS words of the staged table)
+        const int a2 = p / e1, ee1 = p - a2 * e1;
+        const float dm = D1 ? D1[a2] : 1.f;
+        // unconditional loads (index clamped into the core), then a select:
+        // loads under a branch would each wait for their round trip
+        float col[R1MAX];
+#pragma unroll
+        for (int a1 = 0; a1 < R1MAX; ++a1) {
+            const float g = G1[((int64_t(min(a1, r1 - 1)) * v1 + z1) * e1 + ee1) * r2 + a2];
+            col[a1] = a1 < r1 ? g * dm : 0.f;
+        }
+        if (blockIdx.y == 0)
+#pragma unroll
+            for (int a1 = 0; a1 < R1MAX; ++a1)
+                if (a1 < r1) gc1[((int64_t(a1) * v1 + z1) * e1 + ee1) * r2 + a2] = col[a1];
+        for (int zl = 0; zl < nz; ++zl)
+            for (int ee0 = 0; ee0 < e0; ++ee0) {
+                const float4 *g4 = reinterpret_cast<const float4 *>(g0s + (zl * e0 + ee0) * r1p);
+                float acc = 0.f;
+#pragma unroll
+                for (int q = 0; q < R1MAX / 4; ++q) {
+                    const float4 g = g4[q];
+                    acc += g.x * col[4 * q] + g.y * col[4 * q + 1] + g.z * col[4 * q + 2] + g.w * col[4 * q + 3];
+                }
+                out[(zl * r2 + a2) * Ep + ee0 * e1 + ee1] = acc;
+            }
+    }
+    __syncthreads();
+    // every table row (r2 x Ep floats) of a prefix is contiguous
+    const int per = r2 * Ep;
+    for (int zl = 0; zl < nz; ++zl) {
+        float *dst = A + (int64_t(zb + zl) * v1 + z1) * per;
+        for (int i = threadIdx.x; i < per; i += blockDim.x) dst[i] = out[zl * per + i];
+    }
+}
+
 // ---------------------------------------------------------------- radix sort
 // Stable LSD radix sort of (key, token) pairs, 8-bit digits, kBlk keys per
 // workgroup.  Keys are the ids; out-of-range ids get the key V and sort last.
@@ -1063,6 +1135,27 @@ int launch_embed_dapre(const EmbedWs &w, const float *Gs, int64_t Vp, int Ep, in
         case 3: COMERA_LAUNCH((embed_dapre_kernel<3>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
         default: COMERA_LAUNCH((embed_dapre_kernel<4>), grid, dim3(256), lds, hipStream_t(stream), w.headpos, w.S, Gs, Ep, R, Vs, Es, vq, eq, nb, w.dA); break;
     }
+    return launch_status();
+}
+
+bool embed_table_supported(int r1, int e0) { return r1 >= 1 && r1 <= 64 && e0 >= 1; }
+
+int launch_embed_table(const float *G0, const float *D0, const float *G1, const float *D1, float *A, float *gc0,
+                       float *gc1, int v0, int v1, int e0, int e1, int r1, int r2, void *stream) {
+    const int r1p = r1 <= 16 ? 16 : (r1 <= 32 ? 32 : 64);   // the kernel's R1MAX
+    const size_t lds = sizeof(float) * (size_t(kTabZ) * e0 * r1p + size_t(kTabZ) * r2 * e0 * e1);
+    if (!embed_table_supported(r1, e0) || lds > 64 * 1024) return int(hipErrorInvalidValue);
+    const dim3 grid(unsigned(v1), unsigned((v0 + kTabZ - 1) / kTabZ));
+    if (grid.y > 65535) return int(hipErrorInvalidValue);
+    if (r1 <= 16)
+        COMERA_LAUNCH((embed_table_kernel<16>), grid, dim3(256), lds, hipStream_t(stream), G0, D0, G1, D1, A, gc0, gc1,
+                      v0, v1, e0, e1, r1, r2);
+    else if (r1 <= 32)
+        COMERA_LAUNCH((embed_table_kernel<32>), grid, dim3(256), lds, hipStream_t(stream), G0, D0, G1, D1, A, gc0, gc1,
+                      v0, v1, e0, e1, r1, r2);
+    else
+        COMERA_LAUNCH((embed_table_kernel<64>), grid, dim3(256), lds, hipStream_t(stream), G0, D0, G1, D1, A, gc0, gc1,
+                      v0, v1, e0, e1, r1, r2);
     return launch_status();
 }
 

@@ -358,15 +358,16 @@ __global__ __launch_bounds__(256) void wtile_kernel(WBuildArgs a) {
         const int rowf = nJ * A / 4, npf = nI * rowf, ngf = A * NC / 4;
         constexpr int U = 8;
         float4 v[U];
+        // the address is selected first and every load is issued
+        // unconditionally (in bounds: past the end it reads G's first
+        // vector), so the loads do not wait for each other under branches
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int f = tid + u * 256;
-            if (f < npf) {
-                const int qi = f / rowf, e = f - qi * rowf;
-                v[u] = reinterpret_cast<const float4 *>(a.P + ((I0 + qi) * a.NJ + J0) * A)[e];
-            } else if (f < npf + ngf) {
-                v[u] = reinterpret_cast<const float4 *>(a.G)[f - npf];
-            }
+            const int qi = f < npf ? f / rowf : 0, e = f - qi * rowf;
+            const float4 *src = f < npf ? reinterpret_cast<const float4 *>(a.P + ((I0 + qi) * a.NJ + J0) * A) + e
+                                        : reinterpret_cast<const float4 *>(a.G) + (f < npf + ngf ? f - npf : 0);
+            v[u] = *src;
         }
         auto put_p = [&](int f, float4 w) {
             const int qi = f / rowf, e = 4 * (f - qi * rowf);
@@ -407,12 +408,16 @@ __global__ __launch_bounds__(256) void wtile_kernel(WBuildArgs a) {
         const int ng_t = (A * NC4 - tid + 255) / 256;
         int qi = pp0 / QJ, qj = pp0 - (pp0 / QJ) * QJ;
         const int dqi = pstep / QJ, dqj = pstep - dqi * QJ;
+        // addresses selected first, loads unconditional (an in-bounds
+        // element when outside), zero selected afterwards
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            v[u] = 0.f;
+            const float *src = a.G;
+            bool ok = false;
             if (u < np_t) {
                 const int p = pp0 + u * pstep;
-                if (p < NP && qi < nI && qj < nJ) v[u] = a.P[((I0 + qi) * a.NJ + J0 + qj) * A + pa0];
+                ok = p < NP && qi < nI && qj < nJ;
+                if (ok) src = a.P + ((I0 + qi) * a.NJ + J0 + qj) * A + pa0;
                 qi += dqi;
                 qj += dqj;
                 if (qj >= QJ) {
@@ -422,8 +427,11 @@ __global__ __launch_bounds__(256) void wtile_kernel(WBuildArgs a) {
             } else if (u - np_t < ng_t) {
                 const int g = tid + (u - np_t) * 256;
                 const int al = g / NC4, c = g - al * NC4;
-                if (c < NC) v[u] = a.G[al * NC + c];
+                ok = c < NC;
+                if (ok) src = a.G + al * NC + c;
             }
+            const float x = *src;
+            v[u] = ok ? x : 0.f;
         }
         for (int u = 0; u < U; ++u) {
             if (u < np_t) {

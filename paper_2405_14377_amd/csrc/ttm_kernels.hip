@@ -186,21 +186,35 @@ __global__ __launch_bounds__(256) void mask_grad_kernel(MaskGradArgs a) {
     if (threadIdx.x == 0) out[c] = red[0];
 }
 
-__global__ void sum_splits_kernel(const float *__restrict__ part, float *__restrict__ out, int64_t n, int splits) {
-    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
-        float v = 0.f;
-        for (int s = 0; s < splits; ++s) v += part[s * n + i];
-        out[i] = v;
+// sum of the split partials in split order, eight loads in flight
+__device__ __forceinline__ float split_sum(const float *__restrict__ part, int64_t n, int64_t i, int splits) {
+    float v = 0.f;
+    int s = 0;
+    for (; s + 8 <= splits; s += 8) {
+        float x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = part[(s + u) * n + i];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v += x[u];
     }
+    float x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x[u] = part[int64_t(s + u < splits ? s + u : 0) * n + i];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+        if (s + u < splits) v += x[u];
+    return v;
+}
+
+__global__ void sum_splits_kernel(const float *__restrict__ part, float *__restrict__ out, int64_t n, int splits) {
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+        out[i] = split_sum(part, n, i, splits);
 }
 
 __global__ void sum_splits_bf16_kernel(const float *__restrict__ part, uint16_t *__restrict__ out, int64_t n,
                                        int splits) {
-    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
-        float v = 0.f;
-        for (int s = 0; s < splits; ++s) v += part[s * n + i];
-        out[i] = f32_to_bf16_rne(v);
-    }
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+        out[i] = f32_to_bf16_rne(split_sum(part, n, i, splits));
 }
 
 // out[t][j][i] = in[t][i][j] (i < M, j < Tn) through a 32 x 33 LDS tile; the
