@@ -218,7 +218,7 @@ __global__ __launch_bounds__(256) void embed_rows_mfma_kernel(const int64_t *__r
 // contiguous rows.  The workgroups of z0 block 0 also write the folded G~1
 // slice to gc1 ([r1][v1][e1][r2]) and those of z1 = 0 the folded G~0 rows to
 // gc0 ([v0][e0][r1]): the backward's prefix-core projections read them.
-constexpr int kTabZ = 4;
+constexpr int kTabZ = 2;
 template <int R1MAX>
 __global__ __launch_bounds__(256) void embed_table_kernel(const float *__restrict__ G0, const float *__restrict__ D0,
                                                           const float *__restrict__ G1, const float *__restrict__ D1,
@@ -258,17 +258,31 @@ __global__ __launch_bounds__(256) void embed_table_kernel(const float *__restric
 #pragma unroll
             for (int a1 = 0; a1 < R1MAX; ++a1)
                 if (a1 < r1) gc1[((int64_t(a1) * v1 + z1) * e1 + ee1) * r2 + a2] = col[a1];
-        for (int zl = 0; zl < nz; ++zl)
-            for (int ee0 = 0; ee0 < e0; ++ee0) {
-                const float4 *g4 = reinterpret_cast<const float4 *>(g0s + (zl * e0 + ee0) * r1p);
-                float acc = 0.f;
+        // four (z0, e0) entries at a time: independent accumulators, so the
+        // FMAs of one wave do not wait on each other
+        const int nrow = nz * e0;
+        for (int r0 = 0; r0 < nrow; r0 += 4) {
+            float acc[4];
 #pragma unroll
-                for (int q = 0; q < R1MAX / 4; ++q) {
-                    const float4 g = g4[q];
-                    acc += g.x * col[4 * q] + g.y * col[4 * q + 1] + g.z * col[4 * q + 2] + g.w * col[4 * q + 3];
+            for (int h = 0; h < 4; ++h) acc[h] = 0.f;
+#pragma unroll
+            for (int q = 0; q < R1MAX / 4; ++q) {
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    const int row = min(r0 + h, nrow - 1);
+                    const float4 g = reinterpret_cast<const float4 *>(g0s + row * r1p)[q];
+                    acc[h] += g.x * col[4 * q] + g.y * col[4 * q + 1] + g.z * col[4 * q + 2] + g.w * col[4 * q + 3];
                 }
-                out[(zl * r2 + a2) * Ep + ee0 * e1 + ee1] = acc;
             }
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+                const int row = r0 + h;
+                if (row < nrow) {
+                    const int zl = row / e0, ee0 = row - zl * e0;
+                    out[(zl * r2 + a2) * Ep + ee0 * e1 + ee1] = acc[h];
+                }
+            }
+        }
     }
     __syncthreads();
     // every table row (r2 x Ep floats) of a prefix is contiguous
