@@ -18,7 +18,10 @@
 // transposed in registers on the way in.  A general kernel (64-byte K rows,
 // bounds-checked loads) handles any shape; a fast kernel takes over when all
 // accesses are in bounds by construction, and writes outputs whose 16-byte
-// column pieces are contiguous through an LDS-staged tile.  Lanes read
+// column pieces are contiguous through an LDS-staged tile (the fast kernel's
+// bf16 products take the operands in the order B, A so that each lane ends
+// with four consecutive columns of one row, converted to bf16 two at a time
+// by the hardware's packed round-to-nearest-even).  Lanes read
 // 16-byte vectors from LDS; the k slots fed to successive MFMAs are one fixed
 // permutation of the tile's k range, shared by A and B, so the sum is
 // unchanged.
@@ -43,6 +46,15 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return uint16_t((u >> 16) | 0x40);
     u += 0x7fffu + ((u >> 16) & 1u);
     return uint16_t(u >> 16);
+}
+
+// two floats -> two bf16 (round to nearest even) in one dword, a low; one
+// v_cvt_pk_bf16_f32 on gfx950
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack2_bf16(float a, float b) {
+    const f32x2_t v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
 template <typename T>
@@ -217,29 +229,28 @@ __device__ __forceinline__ TileIdx tile_of(const GemmParams &p) {
 }
 
 // Write the accumulators: 32x32 layout, element v of lane l is row
-// (v/4)*8 + (l/32)*4 + v%4 and column l%32.
-template <bool OUT_BF16, int TM, int TN, int WM, int WN>
+// (v/4)*8 + (l/32)*4 + v%4 and column l%32; with SWAP (operands given to the
+// MFMA in the order B, A) the transpose: row l%32, column (v/4)*8 + (l/32)*4 + v%4.
+template <bool OUT_BF16, int TM, int TN, int WM, int WN, bool SWAP = false>
 __device__ __forceinline__ void epilogue(const GemmParams &p, const f32x16 (&acc)[TM][TN], const int64_t *roff,
                                          const int64_t *coff, int wm, int wn, int lr, int lh) {
     const int64_t zoff = tile_of(p).z * p.split_stride;
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int cl = wn * WN + j * 32 + lr;
-        const int64_t co = coff[cl];
-        if (co < 0) continue;
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int rl = wm * WM + i * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
-                const int64_t ro = roff[rl];
-                if (ro < 0) continue;
+                const int ra = (v >> 2) * 8 + lh * 4 + (v & 3);
+                const int rl = wm * WM + i * 32 + (SWAP ? lr : ra);
+                const int cl = wn * WN + j * 32 + (SWAP ? ra : lr);
+                const int64_t ro = roff[rl], co = coff[cl];
+                if (ro < 0 || co < 0) continue;
                 if constexpr (OUT_BF16)
                     reinterpret_cast<uint16_t *>(p.C)[zoff + ro + co] = f32_to_bf16_rne(acc[i][j][v]);
                 else
                     reinterpret_cast<float *>(p.C)[zoff + ro + co] = acc[i][j][v];
             }
-    }
 }
 
 template <typename T, bool A_KC, bool B_KC, bool OUT_BF16, int BM, int BN, int WM, int WN>
@@ -457,26 +468,52 @@ constexpr bool fast_stage_fits() {
 // stride, an innermost column radix that the piece divides, every other
 // stride, N and the split stride multiples of the piece, and C 16-byte
 // aligned.  Offsets come from the row and column tables (-1 = outside).
-template <bool OUT_BF16, int TM, int TN, int WM, int WN, int BM, int BN, int NT>
+template <bool OUT_BF16, int TM, int TN, int WM, int WN, int BM, int BN, int NT, bool SWAP = false>
 __device__ __forceinline__ void epilogue_lds(const GemmParams &p, const f32x16 (&acc)[TM][TN], char *stage,
                                              const int64_t *roff, const int64_t *coff, int wm, int wn, int lr,
                                              int lh, int tid) {
     constexpr int OESZ = OUT_BF16 ? 2 : 4;
     constexpr int CP = BN * OESZ + 16;
     constexpr int PIECES = BN * OESZ / 16;
+    if constexpr (SWAP) {
+        // four consecutive columns per lane and group g: one 8- or 16-byte write
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+            for (int j = 0; j < TN; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int row = wm * WM + i * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
-                const int col = wn * WN + j * 32 + lr;
-                if constexpr (OUT_BF16)
-                    *reinterpret_cast<uint16_t *>(stage + row * CP + col * 2) = f32_to_bf16_rne(acc[i][j][v]);
-                else
-                    *reinterpret_cast<float *>(stage + row * CP + col * 4) = acc[i][j][v];
-            }
+                for (int g = 0; g < 4; ++g) {
+                    const int row = wm * WM + i * 32 + lr;
+                    const int col = wn * WN + j * 32 + g * 8 + lh * 4;
+                    if constexpr (OUT_BF16) {
+                        u32x2 w;
+                        w[0] = pack2_bf16(acc[i][j][4 * g], acc[i][j][4 * g + 1]);
+                        w[1] = pack2_bf16(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+                        *reinterpret_cast<u32x2 *>(stage + row * CP + col * 2) = w;
+                    } else {
+                        f32x4 w;
+                        w[0] = acc[i][j][4 * g];
+                        w[1] = acc[i][j][4 * g + 1];
+                        w[2] = acc[i][j][4 * g + 2];
+                        w[3] = acc[i][j][4 * g + 3];
+                        *reinterpret_cast<f32x4 *>(stage + row * CP + col * 4) = w;
+                    }
+                }
+    } else {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = wm * WM + i * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+                    const int col = wn * WN + j * 32 + lr;
+                    if constexpr (OUT_BF16)
+                        *reinterpret_cast<uint16_t *>(stage + row * CP + col * 2) = f32_to_bf16_rne(acc[i][j][v]);
+                    else
+                        *reinterpret_cast<float *>(stage + row * CP + col * 4) = acc[i][j][v];
+                }
+    }
     __syncthreads();
     const int64_t zoff = tile_of(p).z * p.split_stride;
     for (int id = tid; id < BM * PIECES; id += NT) {
@@ -591,7 +628,7 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[j], av[i], acc[i][j], 0, 0, 0);
             }
             if constexpr (TM == 4 && TN == 2 && KT == 64) {
                 // eight-wave tiles: the operands of step ks + 1 are read
@@ -700,14 +737,17 @@ __global__ __launch_bounds__(NT) void gemm_fast_kernel(GemmParams p) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[i][j][v] *= sc;
     }
+    // bf16 products take the operands swapped (B, A): each lane holds four
+    // consecutive columns of one row
+    constexpr bool SWAP = sizeof(T) == 2;
     if constexpr (fast_stage_fits<BM, BN, KTB, NT, OUT_BF16>()) {
         if (p.stage_c) {
             __syncthreads();   // every wave is done with the operand buffers
-            epilogue_lds<OUT_BF16, TM, TN, WM, WN, BM, BN, NT>(p, acc, smem, roff, coff, wm, wn, lr, lh, tid);
+            epilogue_lds<OUT_BF16, TM, TN, WM, WN, BM, BN, NT, SWAP>(p, acc, smem, roff, coff, wm, wn, lr, lh, tid);
             return;
         }
     }
-    epilogue<OUT_BF16, TM, TN, WM, WN>(p, acc, roff, coff, wm, wn, lr, lh);
+    epilogue<OUT_BF16, TM, TN, WM, WN, SWAP>(p, acc, roff, coff, wm, wn, lr, lh);
 }
 
 enum TileId { T128x128 = 0, T64x64 = 1, T128x32 = 2, T32x128 = 3, T128x64 = 4, T64x128 = 5 };
