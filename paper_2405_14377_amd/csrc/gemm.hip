@@ -784,6 +784,174 @@ dim3 tile_grid(const GemmArgs &g, int bm, int bn, GemmParams &q) {
     return dim3(static_cast<unsigned>(total), 1, 1);
 }
 
+// ---------------------------------------------------------------- DMA path
+// bf16 products of two K-contiguous operands, 256 x 256 tiles of eight waves
+// (128 x 64 each), K stages of 64 in two LDS slots.  The operand tiles go
+// from global memory straight into LDS (global_load_lds_dwordx4: lane l of a
+// wave writes 16 bytes at the instruction's LDS base + 16 l), so they take no
+// registers and no LDS store instructions, and the loads of stage kt + 1 fly
+// while stage kt is multiplied.  LDS rows are 128 bytes without padding;
+// 16-byte chunk c of row r sits at position c ^ ((r / 2) & 7): gfx950's LDS
+// serves a 16-byte read of 16 lanes at a time from 64 four-byte banks, and
+// the sixteen rows that sixteen consecutive lanes read then fall in sixteen
+// different groups of four banks (two rows of 128 bytes per bank line, the
+// eight even and the eight odd rows each on all eight positions).
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+constexpr int kDmaKT = 64;                      // k per stage
+constexpr int kDmaRowB = 2 * kDmaKT;            // bytes of K per LDS row
+constexpr int kDmaOpB = 256 * kDmaRowB;         // one operand tile
+constexpr int kDmaStageB = 2 * kDmaOpB;         // A and B of one stage
+
+template <bool OUT_BF16>
+constexpr size_t dma_main_lds() {
+    const size_t ops = size_t(2) * kDmaStageB;
+    const size_t stg = size_t(256) * (256 * (OUT_BF16 ? 2 : 4) + 16);
+    return (stg > ops && stg + 512 * sizeof(int64_t) <= kLdsPerCu) ? stg : ops;
+}
+
+template <bool OUT_BF16>
+__global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
+    constexpr int BM = 256, BN = 256, WM = 128, WN = 64, NT = 512, KT = kDmaKT;
+    constexpr int TM = WM / 32, TN = WN / 32, WAVES_N = BN / WN;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    int64_t *roff = reinterpret_cast<int64_t *>(smem + dma_main_lds<OUT_BF16>());
+    int64_t *coff = roff + BM;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const TileIdx ti = tile_of(p);
+    const int64_t m0 = ti.row * BM, n0 = ti.col * BN;
+    const int ntiles = int(p.K / KT);
+    const char *abase = reinterpret_cast<const char *>(p.A);
+    const char *bbase = reinterpret_cast<const char *>(p.B);
+    constexpr int64_t kstep = KT * int64_t(sizeof(uint16_t));
+
+    // loads: instruction j of wave w fills LDS rows 8 (4 w + j) .. + 7 of an
+    // operand tile; lane l takes row 8 (4 w + j) + l / 8 and position l % 8,
+    // i.e. logical chunk (l % 8) ^ ((row / 2) & 7)
+    uint32_t aoffs[4], boffs[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int row = (wave * 4 + j) * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ ((row >> 1) & 7);
+        const int64_t ga = min(m0 + row, p.M - 1), gb = min(n0 + row, p.N - 1);
+        aoffs[j] = uint32_t((ga * p.lda + c * 8) * int64_t(sizeof(uint16_t)));
+        boffs[j] = uint32_t((gb * p.ldb + c * 8) * int64_t(sizeof(uint16_t)));
+    }
+    auto issue = [&](int slot, int kt) {
+        char *sa = smem + slot * kDmaStageB + wave * 4 * 1024;
+        char *sb = sa + kDmaOpB;
+        const int64_t koff = kt * kstep;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(abase + koff + aoffs[j]),
+                                             (lds_void_t *)(sa + j * 1024), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(bbase + koff + boffs[j]),
+                                             (lds_void_t *)(sb + j * 1024), 16, 0, 0);
+        }
+    };
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    if (ntiles > 0) issue(0, 0);
+    for (int i = tid; i < BM; i += NT) roff[i] = m0 + i < p.M ? remap(p.rmap, m0 + i) : int64_t(-1);
+    for (int i = tid; i < BN; i += NT) coff[i] = n0 + i < p.N ? remap(p.cmap, n0 + i) : int64_t(-1);
+
+    const int lr = lane & 31, lh = lane >> 5;
+    // reads: lane (lr, lh) of k step ks takes logical chunk 2 ks + lh of its
+    // row; every row it reads has the swizzle of row lr (rows start at
+    // multiples of 32)
+    uint32_t kpos[KT / 16];
+#pragma unroll
+    for (int ks = 0; ks < KT / 16; ++ks) kpos[ks] = uint32_t(((2 * ks + lh) ^ ((lr >> 1) & 7)) * 16);
+    const int arow = (wm * WM + lr) * kDmaRowB, brow = kDmaOpB + (wn * WN + lr) * kDmaRowB;
+    auto mma = [&](int slot) {
+        const char *st = smem + slot * kDmaStageB;
+        __builtin_amdgcn_s_setprio(3);
+#pragma unroll
+        for (int ks = 0; ks < KT / 16; ++ks) {
+            bf16x8 av[TM], bv[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                av[i] = *reinterpret_cast<const bf16x8 *>(st + arow + i * 32 * kDmaRowB + kpos[ks]);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                bv[j] = *reinterpret_cast<const bf16x8 *>(st + brow + j * 32 * kDmaRowB + kpos[ks]);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[j], av[i], acc[i][j], 0, 0, 0);
+        }
+        // the operands of step ks + 1 are read between the products of step ks
+        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+#pragma unroll
+        for (int r = 0; r < KT / 16 - 1; ++r) {
+#pragma unroll
+            for (int t = 0; t < 6; ++t) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        __builtin_amdgcn_s_setprio(0);
+    };
+
+    for (int kt = 0; kt < ntiles; ++kt) {
+        // vmcnt(0): this wave's part of stage kt has landed in LDS; the
+        // barrier then covers every wave's part, and every wave is done with
+        // the slot refilled below (it held stage kt - 1).  A plain barrier:
+        // the products of the previous stage have consumed their LDS reads,
+        // and the clobber keeps the compiler from moving LDS accesses across
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        asm volatile("s_barrier" ::: "memory");
+        if (kt + 1 < ntiles) issue((kt + 1) & 1, kt + 1);
+        mma(kt & 1);
+    }
+    __syncthreads();   // every wave is done with the operand slots
+    if (p.oscale) {
+        const float sc = *p.oscale;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[i][j][v] *= sc;
+    }
+    if constexpr (dma_main_lds<OUT_BF16>() >= size_t(BM) * (BN * (OUT_BF16 ? 2 : 4) + 16)) {
+        if (p.stage_c) {
+            epilogue_lds<OUT_BF16, TM, TN, WM, WN, BM, BN, NT, true>(p, acc, smem, roff, coff, wm, wn, lr, lh, tid);
+            return;
+        }
+    }
+    epilogue<OUT_BF16, TM, TN, WM, WN, true>(p, acc, roff, coff, wm, wn, lr, lh);
+}
+
+template <bool OB>
+int launch_dma(const GemmArgs &g, const GemmParams &p, void *stream) {
+    constexpr size_t lds = dma_main_lds<OB>() + size_t(512) * sizeof(int64_t);
+    static_assert(lds <= kLdsPerCu, "LDS of one workgroup");
+    auto kern = gemm_dma_kernel<OB>;
+    if (!launch_check_mode()) {
+        static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
+        if (set) return set;
+    }
+    GemmParams q = p;
+    const dim3 grid = tile_grid(g, 256, 256, q);
+    if (!grid.x) return int(hipErrorInvalidConfiguration);
+    q.gw = choose_gw(g, 256, 256, g.splits);
+    COMERA_LAUNCH_NAMED("gemm_dma_kernel", kern, grid, dim3(512), lds, hipStream_t(stream), q);
+    return launch_status();
+}
+
 template <typename T, bool AK, bool BK, bool OB>
 int launch_t(const GemmArgs &g, const GemmParams &p, int tile, void *stream) {
     auto go = [&](auto kern, int bm, int bn) {
@@ -831,7 +999,9 @@ enum FastId {
     // register stages of prefetch (FP8: the operands of two 64-byte steps
     // per stage would not fit the registers of a wave beside its
     // accumulators)
-    F256x256_64w8
+    F256x256_64w8,
+    // bf16, K-contiguous operands, straight-to-LDS loads (gemm_dma_kernel)
+    F256x256_dma
 };
 
 template <typename T, bool AK, bool BK, bool OB, int BM, int BN, int WM, int WN, int KTB, int NT = 256, int PF = 1>
@@ -894,6 +1064,7 @@ int pick_fast(const GemmArgs &g, int splits) {
     // workgroups per CU (transposed operands, split over K: half a wave of
     // workgroups is enough)
     if (g.dtype == kDtypeFp8 && t256 >= 512) return F256x256_64w8;
+    if (g.dtype == COMERA_BF16 && g.a_kc && g.b_kc && splits == 1 && t256 >= 512) return F256x256_dma;
     if ((g.dtype == COMERA_BF16 || g.dtype == kDtypeFp8) && g.a_kc == g.b_kc && t256 >= (g.a_kc ? 512 : 128))
         return F256x256_128w8;
     if (g.a_kc && g.b_kc) {
@@ -1039,6 +1210,10 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     if (g.a_kc == AK && g.b_kc == BK && g.out_bf16 == OB) {                                \
         if (fast >= 0) return launch_fast<T, AK, BK, OB>(gg, pf, fast, stream);           \
         return launch_t<T, AK, BK, OB>(gg, p, tile, stream);                               \
+    }
+    if (fast == F256x256_dma) {
+        if (g.dtype != COMERA_BF16 || !g.a_kc || !g.b_kc || gg.splits > 1) return int(hipErrorInvalidValue);
+        return g.out_bf16 ? launch_dma<true>(gg, pf, stream) : launch_dma<false>(gg, pf, stream);
     }
     if (g.dtype == kDtypeFp8) {
         // FP8 operands: K-contiguous fast tiles only (the caller pads K);
