@@ -785,35 +785,144 @@ dim3 tile_grid(const GemmArgs &g, int bm, int bn, GemmParams &q) {
 }
 
 // ---------------------------------------------------------------- DMA path
-// bf16 products of two K-contiguous operands, 256 x 256 tiles of eight waves
+// bf16 products whose operands are both K-contiguous (KC: forward, dX) or
+// both M/N-contiguous (MN: dW = X^T dY), 256 x 256 tiles of eight waves
 // (128 x 64 each), K stages of 64 in two LDS slots.  The operand tiles go
 // from global memory straight into LDS (global_load_lds_dwordx4: lane l of a
 // wave writes 16 bytes at the instruction's LDS base + 16 l), so they take no
 // registers and no LDS store instructions, and the loads of stage kt + 1 fly
-// while stage kt is multiplied.  LDS rows are 128 bytes without padding;
-// 16-byte chunk c of row r sits at position c ^ ((r / 2) & 7): gfx950's LDS
-// serves a 16-byte read of 16 lanes at a time from 64 four-byte banks, and
-// the sixteen rows that sixteen consecutive lanes read then fall in sixteen
-// different groups of four banks (two rows of 128 bytes per bank line, the
-// eight even and the eight odd rows each on all eight positions).
+// while stage kt is multiplied.  LDS rows carry no padding; 16-byte chunks
+// are placed by an XOR swizzle instead (gfx950's LDS serves 16 or 32 lanes
+// at a time from 64 four-byte banks):
+//  - KC: rows of 128 bytes = 64 k of one m; chunk c of row r at c ^ ((r / 2)
+//    & 7), so the sixteen rows sixteen consecutive lanes read fall in sixteen
+//    different groups of four banks;
+//  - MN: rows of 512 bytes = 256 m of one k; chunk c of row k at
+//    c ^ (4 (k & 3)).  The MFMA wants eight consecutive k of one m per lane:
+//    ds_read_b64_tr_b16 hands lane i of each 16-lane group element i % 4 of
+//    the 8-byte reads of lanes i / 4 + 4 e (e = 0..3); with lane j of the
+//    group reading 4 m at row k0 + j / 4, column m0 + 4 (j % 4), lane i gets
+//    m0 + i at k0 .. k0 + 3, and a second read at k0 + 4 the rest.  The two
+//    slots are separate LDS arrays addressed by name (the K loop runs in
+//    pairs of stages), so the compiler sees that the loads in flight into one
+//    slot do not feed the reads of the other.
 typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
 
 constexpr int kDmaKT = 64;                      // k per stage
-constexpr int kDmaRowB = 2 * kDmaKT;            // bytes of K per LDS row
-constexpr int kDmaOpB = 256 * kDmaRowB;         // one operand tile
+constexpr int kDmaOpB = 256 * kDmaKT * 2;       // one operand tile (32 KB)
 constexpr int kDmaStageB = 2 * kDmaOpB;         // A and B of one stage
 
 template <bool OUT_BF16>
 constexpr size_t dma_main_lds() {
+    // operand slots, or (when larger and within the CU) the staged bf16 tile
     const size_t ops = size_t(2) * kDmaStageB;
-    const size_t stg = size_t(256) * (256 * (OUT_BF16 ? 2 : 4) + 16);
-    return (stg > ops && stg + 512 * sizeof(int64_t) <= kLdsPerCu) ? stg : ops;
+    const size_t stg = OUT_BF16 ? size_t(256) * (256 * 2 + 16) : 0;
+    return stg > ops ? stg : ops;
+}
+
+// Loads of one stage (KC or MN) into the LDS slot sa (A) / sa + kDmaOpB (B):
+// instruction j of wave w fills bytes 1024 (4 w + j) .. + 1023 of an operand
+// tile.  KC: row 8 (4 w + j) + l / 8, position l % 8.  MN: k row
+// 2 (4 w + j) + l / 32, position l % 32.  Rows / columns past the operand
+// are clamped (their results are never stored).
+template <bool MN>
+__device__ __forceinline__ void dma_offsets(const GemmParams &p, int64_t m0, int64_t n0, int wave, int lane,
+                                            uint32_t (&aoffs)[4], uint32_t (&boffs)[4]) {
+    constexpr int ESZ = int(sizeof(uint16_t));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if constexpr (!MN) {
+            const int row = (wave * 4 + j) * 8 + (lane >> 3);
+            const int c = (lane & 7) ^ ((row >> 1) & 7);
+            const int64_t ga = min(m0 + row, p.M - 1), gb = min(n0 + row, p.N - 1);
+            aoffs[j] = uint32_t((ga * p.lda + c * 8) * ESZ);
+            boffs[j] = uint32_t((gb * p.ldb + c * 8) * ESZ);
+        } else {
+            const int kr = (wave * 4 + j) * 2 + (lane >> 5);
+            const int c = (lane & 31) ^ (4 * (kr & 3));
+            const int64_t ga = min(m0 + 8 * c, p.M - 8), gb = min(n0 + 8 * c, p.N - 8);
+            aoffs[j] = uint32_t((kr * p.lda + ga) * ESZ);
+            boffs[j] = uint32_t((kr * p.ldb + gb) * ESZ);
+        }
+    }
+}
+
+__device__ __forceinline__ void dma_issue(char *sa, const char *ga, const char *gb, const uint32_t (&aoffs)[4],
+                                          const uint32_t (&boffs)[4], int wave) {
+    sa += wave * 4 * 1024;
+    char *sb = sa + kDmaOpB;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(ga + aoffs[j]), (lds_void_t *)(sa + j * 1024),
+                                         16, 0, 0);
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(gb + boffs[j]), (lds_void_t *)(sb + j * 1024),
+                                         16, 0, 0);
+    }
+}
+
+// acc += the products of one stage in LDS slot st.  KC: lane (lr, lh) of k
+// step ks takes logical chunk 2 ks + lh of its row (kpos).  MN: per 32-row
+// block, two transposed 8-byte reads (k rows 16 ks + 8 lh + j / 4 and + 4).
+template <bool MN, int TM, int TN>
+__device__ __forceinline__ void dma_mma(f32x16 (&acc)[TM][TN], const char *st, const uint32_t (&aaddr)[TM],
+                                        const uint32_t (&baddr)[TN], const uint32_t (&kpos)[4]) {
+    constexpr int RPS = MN ? 2 : 1;   // LDS reads per operand block and k step
+    auto read_op = [&](uint32_t addr, int ks) -> bf16x8 {
+        if constexpr (!MN) {
+            return *reinterpret_cast<const bf16x8 *>(st + addr + kpos[ks]);
+        } else {
+            const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)(st + addr + ks * 16 * 512));
+            const s16x4 hi =
+                __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)(st + addr + ks * 16 * 512 + 4 * 512));
+            return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+    };
+    __builtin_amdgcn_s_setprio(3);
+#pragma unroll
+    for (int ks = 0; ks < kDmaKT / 16; ++ks) {
+        bf16x8 av[TM], bv[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) av[i] = read_op(aaddr[i], ks);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) bv[j] = read_op(baddr[j], ks);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[j], av[i], acc[i][j], 0, 0, 0);
+    }
+    // the operands of step ks + 1 are read between the products of step ks
+    __builtin_amdgcn_sched_group_barrier(0x100, 6 * RPS, 0);
+#pragma unroll
+    for (int r = 0; r < kDmaKT / 16 - 1; ++r) {
+#pragma unroll
+        for (int t = 0; t < 6; ++t) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, RPS, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_s_setprio(0);
+}
+
+// vmcnt(0): this wave's part of the stage about to be read has landed in
+// LDS; the barrier then covers every wave's part, and every wave is done
+// with the slot refilled next (it held the previous stage).  A plain
+// barrier: a workgroup fence would also wait for nothing more here, and the
+// clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void dma_stage_barrier() {
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    asm volatile("s_barrier" ::: "memory");
 }
 
 template <bool OUT_BF16>
 __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     constexpr int BM = 256, BN = 256, WM = 128, WN = 64, NT = 512, KT = kDmaKT;
     constexpr int TM = WM / 32, TN = WN / 32, WAVES_N = BN / WN;
+    constexpr int ESZ = int(sizeof(uint16_t));
     extern __shared__ __attribute__((aligned(16))) char smem[];
     int64_t *roff = reinterpret_cast<int64_t *>(smem + dma_main_lds<OUT_BF16>());
     int64_t *coff = roff + BM;
@@ -824,32 +933,9 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     const int ntiles = int(p.K / KT);
     const char *abase = reinterpret_cast<const char *>(p.A);
     const char *bbase = reinterpret_cast<const char *>(p.B);
-    constexpr int64_t kstep = KT * int64_t(sizeof(uint16_t));
-
-    // loads: instruction j of wave w fills LDS rows 8 (4 w + j) .. + 7 of an
-    // operand tile; lane l takes row 8 (4 w + j) + l / 8 and position l % 8,
-    // i.e. logical chunk (l % 8) ^ ((row / 2) & 7)
+    constexpr int64_t kstep = KT * ESZ;
     uint32_t aoffs[4], boffs[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int row = (wave * 4 + j) * 8 + (lane >> 3);
-        const int c = (lane & 7) ^ ((row >> 1) & 7);
-        const int64_t ga = min(m0 + row, p.M - 1), gb = min(n0 + row, p.N - 1);
-        aoffs[j] = uint32_t((ga * p.lda + c * 8) * int64_t(sizeof(uint16_t)));
-        boffs[j] = uint32_t((gb * p.ldb + c * 8) * int64_t(sizeof(uint16_t)));
-    }
-    auto issue = [&](int slot, int kt) {
-        char *sa = smem + slot * kDmaStageB + wave * 4 * 1024;
-        char *sb = sa + kDmaOpB;
-        const int64_t koff = kt * kstep;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(abase + koff + aoffs[j]),
-                                             (lds_void_t *)(sa + j * 1024), 16, 0, 0);
-            __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(bbase + koff + boffs[j]),
-                                             (lds_void_t *)(sb + j * 1024), 16, 0, 0);
-        }
-    };
+    dma_offsets<false>(p, m0, n0, wave, lane, aoffs, boffs);
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -859,61 +945,27 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    if (ntiles > 0) issue(0, 0);
+    if (ntiles > 0) dma_issue(smem, abase, bbase, aoffs, boffs, wave);
     for (int i = tid; i < BM; i += NT) roff[i] = m0 + i < p.M ? remap(p.rmap, m0 + i) : int64_t(-1);
     for (int i = tid; i < BN; i += NT) coff[i] = n0 + i < p.N ? remap(p.cmap, n0 + i) : int64_t(-1);
 
     const int lr = lane & 31, lh = lane >> 5;
-    // reads: lane (lr, lh) of k step ks takes logical chunk 2 ks + lh of its
-    // row; every row it reads has the swizzle of row lr (rows start at
+    // every row a lane reads has the swizzle of row lr (rows start at
     // multiples of 32)
-    uint32_t kpos[KT / 16];
+    uint32_t kpos[4], aaddr[TM], baddr[TN];
 #pragma unroll
-    for (int ks = 0; ks < KT / 16; ++ks) kpos[ks] = uint32_t(((2 * ks + lh) ^ ((lr >> 1) & 7)) * 16);
-    const int arow = (wm * WM + lr) * kDmaRowB, brow = kDmaOpB + (wn * WN + lr) * kDmaRowB;
-    auto mma = [&](int slot) {
-        const char *st = smem + slot * kDmaStageB;
-        __builtin_amdgcn_s_setprio(3);
+    for (int ks = 0; ks < 4; ++ks) kpos[ks] = uint32_t(((2 * ks + lh) ^ ((lr >> 1) & 7)) * 16);
 #pragma unroll
-        for (int ks = 0; ks < KT / 16; ++ks) {
-            bf16x8 av[TM], bv[TN];
+    for (int i = 0; i < TM; ++i) aaddr[i] = uint32_t((wm * WM + i * 32 + lr) * 128);
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-                av[i] = *reinterpret_cast<const bf16x8 *>(st + arow + i * 32 * kDmaRowB + kpos[ks]);
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-                bv[j] = *reinterpret_cast<const bf16x8 *>(st + brow + j * 32 * kDmaRowB + kpos[ks]);
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[j], av[i], acc[i][j], 0, 0, 0);
-        }
-        // the operands of step ks + 1 are read between the products of step ks
-        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
-#pragma unroll
-        for (int r = 0; r < KT / 16 - 1; ++r) {
-#pragma unroll
-            for (int t = 0; t < 6; ++t) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            }
-            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-        __builtin_amdgcn_s_setprio(0);
-    };
+    for (int j = 0; j < TN; ++j) baddr[j] = uint32_t(kDmaOpB + (wn * WN + j * 32 + lr) * 128);
 
     for (int kt = 0; kt < ntiles; ++kt) {
-        // vmcnt(0): this wave's part of stage kt has landed in LDS; the
-        // barrier then covers every wave's part, and every wave is done with
-        // the slot refilled below (it held stage kt - 1).  A plain barrier:
-        // the products of the previous stage have consumed their LDS reads,
-        // and the clobber keeps the compiler from moving LDS accesses across
-        __builtin_amdgcn_s_waitcnt(0x0F70);
-        asm volatile("s_barrier" ::: "memory");
-        if (kt + 1 < ntiles) issue((kt + 1) & 1, kt + 1);
-        mma(kt & 1);
+        dma_stage_barrier();
+        if (kt + 1 < ntiles)
+            dma_issue(smem + ((kt + 1) & 1) * kDmaStageB, abase + (kt + 1) * kstep, bbase + (kt + 1) * kstep, aoffs,
+                      boffs, wave);
+        dma_mma<false, TM, TN>(acc, smem + (kt & 1) * kDmaStageB, aaddr, baddr, kpos);
     }
     __syncthreads();   // every wave is done with the operand slots
     if (p.oscale) {
@@ -925,7 +977,7 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[i][j][v] *= sc;
     }
-    if constexpr (dma_main_lds<OUT_BF16>() >= size_t(BM) * (BN * (OUT_BF16 ? 2 : 4) + 16)) {
+    if constexpr (OUT_BF16) {
         if (p.stage_c) {
             epilogue_lds<OUT_BF16, TM, TN, WM, WN, BM, BN, NT, true>(p, acc, smem, roff, coff, wm, wn, lr, lh, tid);
             return;
@@ -934,12 +986,129 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     epilogue<OUT_BF16, TM, TN, WM, WN, true>(p, acc, roff, coff, wm, wn, lr, lh);
 }
 
-template <bool OB>
+// MN operands (dW): two named LDS slots, each also holding a quarter of the
+// output tile (64 rows) on its way out
+constexpr int kDmaMnSlotB = 64 * (256 * 4 + 16);   // >= kDmaStageB, one fp32 quarter tile
+
+template <bool OUT_BF16>
+__global__ __launch_bounds__(512) void gemm_dma_mn_kernel(GemmParams p) {
+    static_assert(kDmaMnSlotB >= kDmaStageB, "slot size");
+    constexpr int BM = 256, BN = 256, WM = 128, WN = 64, NT = 512, KT = kDmaKT;
+    constexpr int TM = WM / 32, TN = WN / 32, WAVES_N = BN / WN;
+    constexpr int ESZ = int(sizeof(uint16_t));
+    __shared__ __attribute__((aligned(16))) char slot0[kDmaMnSlotB];
+    __shared__ __attribute__((aligned(16))) char slot1[kDmaMnSlotB];
+    __shared__ int64_t roff[BM], coff[BN];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const TileIdx ti = tile_of(p);
+    const int64_t m0 = ti.row * BM, n0 = ti.col * BN;
+    const int64_t kbeg = ti.z * p.kchunk;
+    const int64_t kend = min(p.K, kbeg + p.kchunk);
+    const int ntiles = kend > kbeg ? int((kend - kbeg) / KT) : 0;
+    const char *abase = reinterpret_cast<const char *>(p.A) + kbeg * p.lda * ESZ;
+    const char *bbase = reinterpret_cast<const char *>(p.B) + kbeg * p.ldb * ESZ;
+    const int64_t astep = KT * p.lda * ESZ, bstep = KT * p.ldb * ESZ;
+    uint32_t aoffs[4], boffs[4];
+    dma_offsets<true>(p, m0, n0, wave, lane, aoffs, boffs);
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    if (ntiles > 0) dma_issue(slot0, abase, bbase, aoffs, boffs, wave);
+    for (int i = tid; i < BM; i += NT) roff[i] = m0 + i < p.M ? remap(p.rmap, m0 + i) : int64_t(-1);
+    for (int i = tid; i < BN; i += NT) coff[i] = n0 + i < p.N ? remap(p.cmap, n0 + i) : int64_t(-1);
+
+    const int lr = lane & 31, lh = lane >> 5;
+    const int g1 = (lane >> 4) & 1, jj = lane & 15, q = jj >> 2;
+    const int krow = 8 * lh + q;   // (krow & 3) == q for every k step and half
+    uint32_t kpos[4] = {0, 0, 0, 0}, aaddr[TM], baddr[TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const int m = wm * WM + i * 32 + 16 * g1 + 4 * (jj & 3);
+        aaddr[i] = uint32_t(krow * 512 + (((m >> 3) ^ (4 * q)) * 16) + (m & 7) * 2);
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int n = wn * WN + j * 32 + 16 * g1 + 4 * (jj & 3);
+        baddr[j] = uint32_t(kDmaOpB + krow * 512 + (((n >> 3) ^ (4 * q)) * 16) + (n & 7) * 2);
+    }
+
+    for (int kt = 0; kt < ntiles; kt += 2) {
+        dma_stage_barrier();
+        if (kt + 1 < ntiles) dma_issue(slot1, abase + (kt + 1) * astep, bbase + (kt + 1) * bstep, aoffs, boffs, wave);
+        dma_mma<true, TM, TN>(acc, slot0, aaddr, baddr, kpos);
+        if (kt + 1 >= ntiles) break;
+        dma_stage_barrier();
+        if (kt + 2 < ntiles) dma_issue(slot0, abase + (kt + 2) * astep, bbase + (kt + 2) * bstep, aoffs, boffs, wave);
+        dma_mma<true, TM, TN>(acc, slot1, aaddr, baddr, kpos);
+    }
+    __syncthreads();   // every wave is done with the operand slots
+    if (p.oscale) {
+        const float sc = *p.oscale;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[i][j][v] *= sc;
+    }
+    if (!p.stage_c) {
+        epilogue<OUT_BF16, TM, TN, WM, WN, true>(p, acc, roff, coff, wm, wn, lr, lh);
+        return;
+    }
+    // a quarter of the rows (two 32-row blocks of one wm) at a time through slot0
+    constexpr int OESZ = OUT_BF16 ? 2 : 4;
+    constexpr int CP = BN * OESZ + 16, PIECES = BN * OESZ / 16;
+    const int64_t zoff = ti.z * p.split_stride;
+#pragma unroll
+    for (int qr = 0; qr < 4; ++qr) {
+        if (wm == qr / 2) {
+#pragma unroll
+            for (int i = 2 * (qr % 2); i < 2 * (qr % 2) + 2; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        char *dst = slot0 + ((i % 2) * 32 + lr) * CP + (wn * WN + j * 32 + g * 8 + lh * 4) * OESZ;
+                        if constexpr (OUT_BF16) {
+                            u32x2 w;
+                            w[0] = pack2_bf16(acc[i][j][4 * g], acc[i][j][4 * g + 1]);
+                            w[1] = pack2_bf16(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+                            *reinterpret_cast<u32x2 *>(dst) = w;
+                        } else {
+                            f32x4 w;
+                            w[0] = acc[i][j][4 * g];
+                            w[1] = acc[i][j][4 * g + 1];
+                            w[2] = acc[i][j][4 * g + 2];
+                            w[3] = acc[i][j][4 * g + 3];
+                            *reinterpret_cast<f32x4 *>(dst) = w;
+                        }
+                    }
+        }
+        __syncthreads();
+        for (int id = tid; id < 64 * PIECES; id += NT) {
+            const int r = id / PIECES, c = id % PIECES;
+            const int64_t ro = roff[qr * 64 + r], co = coff[c * (16 / OESZ)];
+            if (ro >= 0 && co >= 0)
+                *reinterpret_cast<u32x4 *>(reinterpret_cast<char *>(p.C) + (zoff + ro + co) * OESZ) =
+                    *reinterpret_cast<const u32x4 *>(slot0 + r * CP + c * 16);
+        }
+        __syncthreads();
+    }
+}
+
+template <bool OB, bool MN>
 int launch_dma(const GemmArgs &g, const GemmParams &p, void *stream) {
-    constexpr size_t lds = dma_main_lds<OB>() + size_t(512) * sizeof(int64_t);
+    constexpr size_t lds = MN ? 0 : dma_main_lds<OB>() + size_t(512) * sizeof(int64_t);
     static_assert(lds <= kLdsPerCu, "LDS of one workgroup");
-    auto kern = gemm_dma_kernel<OB>;
-    if (!launch_check_mode()) {
+    auto kern = MN ? gemm_dma_mn_kernel<OB> : gemm_dma_kernel<OB>;
+    if (!MN && !launch_check_mode()) {
         static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
         if (set) return set;
@@ -1064,7 +1233,11 @@ int pick_fast(const GemmArgs &g, int splits) {
     // workgroups per CU (transposed operands, split over K: half a wave of
     // workgroups is enough)
     if (g.dtype == kDtypeFp8 && t256 >= 512) return F256x256_64w8;
+    // bf16 256 x 256 tiles with straight-to-LDS operand loads: K-contiguous
+    // unsplit products of two or more waves of tiles, M/N-contiguous ones
+    // (dW) from half a wave
     if (g.dtype == COMERA_BF16 && g.a_kc && g.b_kc && splits == 1 && t256 >= 512) return F256x256_dma;
+    if (g.dtype == COMERA_BF16 && !g.a_kc && !g.b_kc && t256 >= 128) return F256x256_dma;
     if ((g.dtype == COMERA_BF16 || g.dtype == kDtypeFp8) && g.a_kc == g.b_kc && t256 >= (g.a_kc ? 512 : 128))
         return F256x256_128w8;
     if (g.a_kc && g.b_kc) {
@@ -1212,8 +1385,9 @@ int launch_gemm(const GemmArgs &g, void *stream) {
         return launch_t<T, AK, BK, OB>(gg, p, tile, stream);                               \
     }
     if (fast == F256x256_dma) {
-        if (g.dtype != COMERA_BF16 || !g.a_kc || !g.b_kc || gg.splits > 1) return int(hipErrorInvalidValue);
-        return g.out_bf16 ? launch_dma<true>(gg, pf, stream) : launch_dma<false>(gg, pf, stream);
+        if (g.dtype != COMERA_BF16 || g.a_kc != g.b_kc) return int(hipErrorInvalidValue);
+        if (g.a_kc) return g.out_bf16 ? launch_dma<true, false>(gg, pf, stream) : launch_dma<false, false>(gg, pf, stream);
+        return g.out_bf16 ? launch_dma<true, true>(gg, pf, stream) : launch_dma<false, true>(gg, pf, stream);
     }
     if (g.dtype == kDtypeFp8) {
         // FP8 operands: K-contiguous fast tiles only (the caller pads K);
