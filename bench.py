@@ -187,11 +187,15 @@ def kernel_roofline(layer, steps, act, tag=""):
     dom = max(out, key=lambda t: out[t]["avg_ms"])
     ach = out[dom]["tflops"]
     peak = PEAK[act] / 1e12
-    ttag = f"{dom}_{tag}" if tag else dom
+    # the counter summary is keyed by the product it measured: M x N x K and
+    # whether the operands are K-contiguous (fwd, dX) or M/N-contiguous (dW)
+    shape = {"fwd": (b, sh.n_out, sh.n_in, "kc"), "dx": (b, sh.n_in, sh.n_out, "kc"),
+             "dw": (sh.n_in, sh.n_out, b, "mn")}[dom]
+    ttag = "gemm_{}x{}x{}_{}".format(*shape)
     traffic = traffic_from_profile(ttag, act)
     roof = {"bound": "mfma", "achieved": round(ach, 3), "peak": peak, "unit": "TFLOP/s",
             "frac": round(ach / peak, 4), "traffic": traffic,
-            "kernel": f"gemm {dom} ({act}{', ' + tag if tag else ''})",
+            "kernel": f"gemm {dom} ({act}{', ' + tag if tag else ''}; {shape[0]}x{shape[1]}x{shape[2]} {shape[3]})",
             "flops_per_launch": flops, "avg_ms": round(out[dom]["avg_ms"], 5),
             "traffic_profile": f"profiles/traffic_{ttag}_{act}.md"}
     return roof, out
@@ -724,6 +728,8 @@ def run_gpu(args):
         else:
             r = run_layers(args.workload, args.act, args.steps, args.warmup, 1000 * args.workload)
             print(json.dumps(r))
+        if args.calib_copy:
+            calib_copy()
         return
     if args.orders is not None:
         wids = args.orders or [0, 1, 5]
