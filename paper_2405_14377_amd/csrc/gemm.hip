@@ -1234,10 +1234,12 @@ int pick_fast(const GemmArgs &g, int splits) {
     // workgroups is enough)
     if (g.dtype == kDtypeFp8 && t256 >= 512) return F256x256_64w8;
     // bf16 256 x 256 tiles with straight-to-LDS operand loads: K-contiguous
-    // unsplit products of two or more waves of tiles, M/N-contiguous ones
-    // (dW) from half a wave
-    if (g.dtype == COMERA_BF16 && g.a_kc && g.b_kc && splits == 1 && t256 >= 512) return F256x256_dma;
-    if (g.dtype == COMERA_BF16 && !g.a_kc && !g.b_kc && t256 >= 128) return F256x256_dma;
+    // unsplit products from half a wave of tiles (below that the smaller
+    // tiles fill more CUs), M/N-contiguous ones (dW) from an eighth: their
+    // transposing loads are what the DMA form saves (measured on the layer
+    // shapes)
+    if (g.dtype == COMERA_BF16 && g.a_kc && g.b_kc && splits == 1 && t256 >= 128) return F256x256_dma;
+    if (g.dtype == COMERA_BF16 && !g.a_kc && !g.b_kc && t256 >= 32) return F256x256_dma;
     if ((g.dtype == COMERA_BF16 || g.dtype == kDtypeFp8) && g.a_kc == g.b_kc && t256 >= (g.a_kc ? 512 : 128))
         return F256x256_128w8;
     if (g.a_kc && g.b_kc) {

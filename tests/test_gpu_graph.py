@@ -178,3 +178,111 @@ def test_fp8_step_graph_replays(act, reuse):
                 for a, c in zip(dGs, dGr):
                     assert torch.equal(a, c), rep
     del g
+
+
+def test_model_step_graph_replays():
+    """One graph for a whole model-shaped step (Sec. 4.3): the 32768 x 768
+    TT embedding, then the six TTM layers of the encoder workload (q, k, v
+    read the embedded rows in bf16, o reads v, the feed-forward pair reads
+    o), their backward in reverse, the input gradients of q, k and v summed
+    into the embedding's dY, and the embedding backward.  The layers keep
+    the workload's cores and masks at 2048 tokens.  Every replay (three
+    input sets, twice each, with eager work between) must equal the same
+    sequence run eagerly on other workspaces, bit for bit; the last replay's
+    embedding gradient is also checked against the oracle."""
+    import torch
+    from oracle import embed as OE
+    b = 2048
+    enc = wl.WORKLOADS[2]
+    ew = wl.WORKLOADS[3]
+    rng = np.random.default_rng(41)
+    ecores = wl.embed_cores(ew)
+    V = int(np.prod(ew.v))
+
+    def layers():
+        out = []
+        for li, sh in enumerate(enc.layers):
+            inp = wl.ttm_layer_inputs(2, li, sh, enc.mask)
+            active = [int(x != 0) for mk in inp.masks for x in mk]
+            out.append((sh, TTMRun(sh.n, sh.m, sh.r, inp.cores, inp.masks, b, "bf16", mask_active=active,
+                                   reuse=True)))
+        return out
+
+    def model(L, emb, bufs):
+        (ids, dYq, dYk, dYd), o = bufs["in"], bufs["out"]
+        C.comera_tt_embed_forward(emb.shape, ids, b, emb.G, None, o["Ye"], emb.ws, emb.err)
+        o["X0"].copy_(o["Ye"])
+        names = [sh.name for sh, _ in L]
+        run = dict(zip(names, [r for _, r in L]))
+        fwd = [("q", "X0", "Yq"), ("k", "X0", "Yk"), ("v", "X0", "Yv"), ("o", "Yv", "Yo"),
+               ("ffn_up", "Yo", "Yu"), ("ffn_down", "Yu", "Yd")]
+        for nm, xi, yo in fwd:
+            C.comera_ttm_forward(run[nm].plan.handle, b, o[xi], run[nm].G, run[nm].D, o[yo], run[nm].ws)
+        bwd = [("ffn_down", "Yu", dYd, "dYu"), ("ffn_up", "Yo", "dYu", "dYo"), ("o", "Yv", "dYo", "dYv"),
+               ("v", "X0", "dYv", "dXv"), ("k", "X0", dYk, "dXk"), ("q", "X0", dYq, "dXq")]
+        for nm, xi, dy, dx in bwd:
+            dyt = o[dy] if isinstance(dy, str) else dy
+            C.comera_ttm_backward(run[nm].plan.handle, b, o[xi], dyt, run[nm].G, run[nm].D, o[dx],
+                                  o["dG_" + nm], run[nm].ws)
+        o["dYe"].copy_(o["dXq"])
+        o["dYe"].add_(o["dXk"])
+        o["dYe"].add_(o["dXv"])
+        C.comera_tt_embed_backward(emb.shape, ids, b, o["dYe"], emb.G, None, o["dGe"], 1, emb.ws, emb.err)
+
+    def buffers(L, emb):
+        dev, bf = "cuda", torch.bfloat16
+        o = {"Ye": torch.empty((b, emb.E), device=dev), "dYe": torch.empty((b, emb.E), device=dev),
+             "X0": torch.empty((b, emb.E), dtype=bf, device=dev),
+             "dGe": [torch.empty_like(g) for g in emb.G]}
+        for nm, width in (("Yq", 768), ("Yk", 768), ("Yv", 768), ("Yo", 768), ("Yu", 3072), ("Yd", 768),
+                          ("dYu", 3072), ("dYo", 768), ("dYv", 768), ("dXv", 768), ("dXk", 768), ("dXq", 768)):
+            o[nm] = torch.empty((b, width), dtype=bf, device=dev)
+        for sh, r in L:
+            o["dG_" + sh.name] = [torch.empty_like(g) for g in r.G]
+        return o
+
+    def draw():
+        ids = wl.token_ids(b, V, "zipf1.1", int(rng.integers(1 << 30)))
+        return (ids, wl.to_bf16_values(rng.standard_normal((b, 768)).astype(np.float32)),
+                wl.to_bf16_values(rng.standard_normal((b, 768)).astype(np.float32)),
+                wl.to_bf16_values(rng.standard_normal((b, 768)).astype(np.float32)))
+
+    def upload(emb, s):
+        ids, dq, dk, dd = s
+        return emb.ids_dev(ids), to_dev(dq, "bf16"), to_dev(dk, "bf16"), to_dev(dd, "bf16")
+
+    L, Lr = layers(), layers()
+    emb, embr = EmbedRun(ew.v, ew.e, ew.r, ecores, None, b), EmbedRun(ew.v, ew.e, ew.r, ecores, None, b)
+    sets = [draw() for _ in range(3)]
+    cap = {"in": upload(emb, sets[0]), "out": buffers(L, emb)}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        model(L, emb, cap)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            model(L, emb, cap)
+        torch.cuda.synchronize()
+        for rep in range(2):
+            for s in sets:
+                ref = {"in": upload(embr, s), "out": buffers(Lr, embr)}
+                model(Lr, embr, ref)
+                torch.cuda.synchronize()
+                for dst, src in zip(cap["in"], ref["in"]):
+                    dst.copy_(src)
+                g.replay()
+                torch.cuda.synchronize()
+                for k, v in ref["out"].items():
+                    got = cap["out"][k]
+                    if isinstance(v, list):
+                        for a, c in zip(got, v):
+                            assert torch.equal(a, c), (rep, k)
+                    else:
+                        assert torch.equal(got, v), (rep, k)
+    assert int(emb.err.item()) == 0
+    ids = sets[-1][0]
+    dGo = OE.backward(ids, to_np(cap["out"]["dYe"]).astype(np.float64), ecores)
+    for a, c in zip(cap["out"]["dGe"], dGo):
+        assert rel_err(to_np(a), c) <= 1e-4
+    del g
