@@ -33,13 +33,12 @@ void dense_ptrs(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd) {
 }
 
 int fold_cores(const comera_ttm_plan_s *p, const float *const *G, const float *const *D, float *const *dst,
-               const CoreStrides *st, void *stream, float *p2) {
+               const CoreStrides *st, void *stream) {
     const int d = p->d;
     FoldArgs fa;
     std::memset(&fa, 0, sizeof(fa));
     fa.d = d;
     fa.nfold = d;
-    fa.P2 = d >= 3 ? p2 : nullptr;
     fa.compacted = p->compacted ? 1 : 0;
     for (int k = 0; k < d; ++k) {
         fa.G[k] = G[k];
@@ -88,13 +87,6 @@ int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, int want,
     int64_t Il = sp->s.n[0], Jl = sp->s.m[0];
     for (int k = 1; k < d; ++k) {
         const bool last = k == d - 1;
-        if (k == 1 && !last && bd.p2_ready) {
-            // written by the fold launch
-            bd.P[2] = reinterpret_cast<float *>(at(ws, L.p[2]));
-            Il *= sp->s.n[1];
-            Jl *= sp->s.m[1];
-            continue;
-        }
         if (!last) {
             void *out = at(ws, L.p[k + 1]);
             int e = chain_gemm(bd.P[k], bd.gc[k], out, false, Il, Jl, int(sp->rho[k]), int(sp->s.n[k]),
@@ -346,10 +338,7 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
     dense_ptrs(p, ws, bd);
     CoreStrides st[kMaxCores];
     dense_strides(p, st);
-    // three or more cores: the fold launch also writes the first left chain
-    float *p2 = p->d >= 3 ? reinterpret_cast<float *>(at(ws, p->dense.p[2])) : nullptr;
-    if (int e = fold_cores(p, G, D, bd.gc, st, stream, p2)) return e;
-    bd.p2_ready = p2 != nullptr;
+    if (int e = fold_cores(p, G, D, bd.gc, st, stream)) return e;
     return build_chain(p, ws, bd, want, stream);
 }
 

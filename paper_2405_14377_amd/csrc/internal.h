@@ -223,10 +223,6 @@ struct FoldArgs {
     int nfold;                   // cores folded (grid.y); d for a linear layer
     int compacted;
     CoreStrides st[kMaxCores];   // placement of each copy
-    // optional (d >= 3): the first left chain
-    //   P2[(i0 i1)][(j0 j1)][c] = sum_a G~0[0][j0][i0][a] G~1[a][j1][i1][c]
-    // from the raw cores (masks folded, bonds compacted), one more grid row
-    float *P2;
 };
 int launch_fold(const FoldArgs &a, void *stream);
 
@@ -441,7 +437,6 @@ struct DenseBuild {
     float *P[kMaxCores + 1];   // left chains P_k = [I_<k][J_<k][rho_k], k = 1..d-1
     void *w;                   // W [N_in][N_out] in the activation dtype
     void *wt;                  // W^T [N_out][N_in] in the activation dtype
-    bool p2_ready = false;     // P[2] already written (by the fold launch)
 };
 // which layouts of W build_chain writes
 constexpr int kWantW = 1, kWantWT = 2;
@@ -450,7 +445,7 @@ void dense_ptrs(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd);
 // fold the masks into compacted copies of every core of layer p (eq. Wcompress):
 // core k goes to dst[k], placed by st[k]
 int fold_cores(const comera_ttm_plan_s *p, const float *const *G, const float *const *D, float *const *dst,
-               const CoreStrides *st, void *stream, float *p2 = nullptr);
+               const CoreStrides *st, void *stream);
 // left chains and W (want & kWantW) and / or W^T (want & kWantWT) of a
 // layer from its folded cores
 int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, int want, void *stream);

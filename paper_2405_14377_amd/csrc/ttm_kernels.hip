@@ -38,6 +38,10 @@ __device__ int rank_bit(const BondBits &b, int a) {
 }
 
 // ---------------------------------------------------------------- fold / expand
+// threads of a fold workgroup (a constant, not blockDim, which would be one
+// more memory round trip)
+constexpr int kFoldThreads = 256;
+
 // Map of a compacted bond's entries to full ones, built in LDS by 256
 // threads at once: thread t owns full entry t and, when it is active, writes
 // t at its rank (the set bits below it).  Compaction only happens for ranks
@@ -50,72 +54,40 @@ __device__ __forceinline__ void bond_map(const FoldArgs &a, int bond, int *map) 
         map[t] = t;
         return;
     }
-    const BondBits &b = a.act[bond];
+    // the four words by uniform (scalar) loads, then picked per lane
+    const BondBits b = a.act[bond];
     const int w = t >> 6, bit = t & 63;
-    if ((b.w[w] >> bit) & 1) {
-        int rank = __popcll(b.w[w] & ((uint64_t(1) << bit) - 1));
-        for (int u = 0; u < w; ++u) rank += __popcll(b.w[u]);
-        map[rank] = t;
-    }
+    const int c1 = __popcll(b.w[0]), c2 = c1 + __popcll(b.w[1]), c3 = c2 + __popcll(b.w[2]);
+    const uint64_t word = w == 0 ? b.w[0] : w == 1 ? b.w[1] : w == 2 ? b.w[2] : b.w[3];
+    const int below = w == 0 ? 0 : w == 1 ? c1 : w == 2 ? c2 : c3;
+    if ((word >> bit) & 1) map[below + __popcll(word & ((uint64_t(1) << bit) - 1))] = t;
 }
 
-// Rows k < nfold of the grid fold core k; row nfold (when P2 is set) writes
-// the first left chain straight from the raw cores.
-__global__ __launch_bounds__(256) void fold_kernel(FoldArgs a) {
+__global__ __launch_bounds__(kFoldThreads) void fold_kernel(FoldArgs a) {
     __shared__ int map_l[256], map_r[256];
     const int k = blockIdx.y;
-    const bool p2 = k == a.nfold;
-    if (k > a.nfold || (p2 && !a.P2)) return;
-    // bonds on either side of core k; of cores 0 and 1 for P2
-    bond_map(a, p2 ? 1 : k, map_l);
-    bond_map(a, p2 ? 2 : k + 1, map_r);
+    if (k >= a.nfold) return;
+    // bonds on either side of core k
+    bond_map(a, k, map_l);
+    bond_map(a, k + 1, map_r);
     __syncthreads();
-    if (!p2) {
-        const int rl = a.rc[k], rr = a.rc[k + 1], m = a.m[k], n = a.n[k];
-        const int total = rl * m * n * rr;     // core sizes are far below 2^31 (host checks)
-        const float *G = a.G[k];
-        const float *D = (k < a.d - 1) ? a.D[k] : nullptr;
-        const CoreStrides st = a.st[k];
-        for (int o = blockIdx.x * blockDim.x + threadIdx.x; o < total; o += gridDim.x * blockDim.x) {
-            // compacted element o = (al, jm, in, c)
-            const int c = o % rr;
-            int t = o / rr;
-            const int in = t % n;
-            t /= n;
-            const int jm = t % m;
-            const int al = t / m;
-            const int fa = a.compacted ? map_l[al] : al, fc = a.compacted ? map_r[c] : c;
-            float v = G[((fa * m + jm) * n + in) * a.r[k + 1] + fc];
-            if (D) v *= D[fc];
-            a.Gc[k][al * st.sa + jm * st.sm + in * st.sn + c * st.sc] = v;
-        }
-        return;
-    }
-    // P2[(i0 i1)][(j0 j1)][c] = sum_a G0[0][j0][i0][f(a)] D0[f(a)] G1[f(a)][j1][i1][g(c)] D1[g(c)]
-    const int n0 = a.n[0], m0 = a.m[0], n1 = a.n[1], m1 = a.m[1];
-    const int rho1 = a.rc[1], rho2 = a.rc[2], r1 = a.r[1], r2 = a.r[2];
-    const float *G0 = a.G[0], *G1 = a.G[1], *D0 = a.D[0], *D1 = a.D[1];
-    const int total = n0 * n1 * m0 * m1 * rho2;
-    for (int o = blockIdx.x * blockDim.x + threadIdx.x; o < total; o += gridDim.x * blockDim.x) {
-        const int c = o % rho2;
-        int t = o / rho2;
-        const int j1 = t % m1;
-        t /= m1;
-        const int j0 = t % m0;
-        t /= m0;
-        const int i1 = t % n1;
-        const int i0 = t / n1;
-        const int fc = a.compacted ? map_r[c] : c;
-        const float *g0 = G0 + (j0 * n0 + i0) * r1;
-        const float *g1 = G1 + (j1 * n1 + i1) * r2 + fc;
-        const int s1 = m1 * n1 * r2;   // stride of G1's left bond
-        float acc = 0.f;
-        for (int al = 0; al < rho1; ++al) {
-            const int fa = a.compacted ? map_l[al] : al;
-            const float x = g0[fa] * (D0 ? D0[fa] : 1.f);
-            acc += x * g1[int64_t(fa) * s1];
-        }
-        a.P2[o] = acc * (D1 ? D1[fc] : 1.f);
+    const int rl = a.rc[k], rr = a.rc[k + 1], m = a.m[k], n = a.n[k];
+    const int total = rl * m * n * rr;     // core sizes are far below 2^31 (host checks)
+    const float *G = a.G[k];
+    const float *D = (k < a.d - 1) ? a.D[k] : nullptr;
+    const CoreStrides st = a.st[k];
+    for (int o = blockIdx.x * kFoldThreads + threadIdx.x; o < total; o += gridDim.x * kFoldThreads) {
+        // compacted element o = (al, jm, in, c)
+        const int c = o % rr;
+        int t = o / rr;
+        const int in = t % n;
+        t /= n;
+        const int jm = t % m;
+        const int al = t / m;
+        const int fa = a.compacted ? map_l[al] : al, fc = a.compacted ? map_r[c] : c;
+        float v = G[((fa * m + jm) * n + in) * a.r[k + 1] + fc];
+        if (D) v *= D[fc];
+        a.Gc[k][al * st.sa + jm * st.sm + in * st.sn + c * st.sc] = v;
     }
 }
 
@@ -317,15 +289,12 @@ int launch_fold(const FoldArgs &a, void *stream) {
     int64_t mx = 1;
     for (int k = 0; k < a.nfold; ++k) mx = std::max<int64_t>(mx, int64_t(a.rc[k]) * a.m[k] * a.n[k] * a.rc[k + 1]);
     if (a.nfold <= 0) return 0;
-    const bool p2 = a.P2 && a.d >= 3;
-    if (a.P2 && !p2) return int(hipErrorInvalidValue);
     // compacted bonds index a 256-entry map (one entry per thread)
     if (a.compacted)
         for (int k = 0; k <= a.d; ++k)
             if (a.r[k] > 256) return int(hipErrorInvalidValue);
-    if (p2) mx = std::max<int64_t>(mx, int64_t(a.n[0]) * a.n[1] * a.m[0] * a.m[1] * a.rc[2]);
-    dim3 grid(grid_for(mx), a.nfold + (p2 ? 1 : 0));
-    COMERA_LAUNCH(fold_kernel, grid, dim3(256), 0, hipStream_t(stream), a);
+    dim3 grid(grid_for(mx), a.nfold);
+    COMERA_LAUNCH(fold_kernel, grid, dim3(kFoldThreads), 0, hipStream_t(stream), a);
     return launch_status();
 }
 
