@@ -13,8 +13,9 @@
 // and by the expand kernel (meet), so results are bitwise reproducible.
 //
 // The contractions are small (rank <= 64) and read operands that the step
-// fetched once into LDS; they run on MFMA, one 32 x 32 output tile per wave
-// at a time.
+// fetched once into LDS; they run on MFMA in 16 x 16 output tiles (a rank of
+// 45 pads to 48, not 64), one tile per wave at a time, with the operands
+// zero-padded in LDS so that no read is guarded.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -25,30 +26,96 @@
 namespace comera {
 namespace {
 
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kProjMaxA = 64;
-constexpr size_t kProjLds = 64 * 1024;
+constexpr size_t kProjLds = 80 * 1024;    // dynamic LDS of a projection workgroup
+constexpr size_t kWtileLds = 64 * 1024;   // of a W-tile workgroup
 constexpr int kProjThreadsMax = 1024;  // threads per projection workgroup (large tiles)
 
-__device__ __forceinline__ int64_t remap_off(const Remap &r, int64_t idx) {
+// Offset of flat index idx under a mixed-radix remap, with the index and the
+// radices below 2^32 (launch_proj checks): 32-bit divisions instead of the
+// emulated 64-bit ones
+__device__ __forceinline__ int64_t remap_off32(const Remap &r, uint32_t idx) {
     int64_t off = 0;
     for (int t = r.nd - 1; t >= 1; --t) {
-        const int64_t q = idx / r.radix[t];
-        off += (idx - q * r.radix[t]) * r.stride[t];
+        const uint32_t rad = uint32_t(r.radix[t]);
+        const uint32_t q = idx / rad;
+        off += int64_t(idx - q * rad) * r.stride[t];
         idx = q;
     }
-    return off + idx * r.stride[0];
+    return off + int64_t(idx) * r.stride[0];
 }
+
+// Position (r, c) of element tid + k T of a row-major index space of width
+// w, stepped by T without a division per step: (dr, dc) = (T / w, T % w).
+struct Walk {
+    int r, c;
+    __device__ __forceinline__ Walk(int tid, int w) : r(tid / w), c(tid - (tid / w) * w) {}
+    __device__ __forceinline__ void step(int w, int dr, int dc) {
+        c += dc;
+        r += dr;
+        if (c >= w) {
+            c -= w;
+            ++r;
+        }
+    }
+};
 
 __host__ __device__ inline int round4(int x) { return (x + 3) & ~3; }
 
-// LDS floats of a projection workgroup: E tile, core slice, left-chain
-// slice (row pitches padded by 4 floats) and the adjoint row-offset table
-// (RT int64, kept 16-byte aligned)
+__host__ __device__ inline int round16(int x) { return (x + 15) & ~15; }
+
+// LDS floats of a projection workgroup: the E tile [R16][C16 + 4], the core
+// slice [A16][C16 + 4], the left-chain slice transposed [A16][R16 + 4] (R16,
+// C16, A16: RT, CT, A rounded up to 16; zero past the data, so that the
+// products read whole 16-deep blocks) and the adjoint row-offset table (RT
+// int64, kept 16-byte aligned).  Row pitches of 4 mod 16 floats keep the
+// 16-byte reads of 16 consecutive rows on distinct banks.
 __host__ __device__ inline size_t proj_lds_floats(int RT, int CT, int A) {
-    const int CT4 = round4(CT), A4 = round4(A);
-    return size_t(RT) * (CT4 + 4) + size_t(A4) * (CT4 + 4) + size_t(RT) * (A4 + 4) + size_t(round4(2 * RT));
+    const int R16 = round16(RT), C16 = round16(CT), A16 = round16(A);
+    return size_t(R16) * (C16 + 4) + size_t(A16) * (C16 + 4) + size_t(A16) * (R16 + 4) + size_t(round4(2 * RT));
+}
+
+// One 16 x 16 output tile over nb 16-deep blocks of K.  A operand rows
+// start at pa (k contiguous: one 16-byte read per block); the B operand
+// starts at pb, k contiguous as well (ROWB) or k along rows of pitch pe
+// (four single reads per block).  Whole groups of NG blocks read all their
+// operands before the first of their products (the order is pinned: the
+// compiler would otherwise move each read down to its product and wait for
+// it there); the remaining blocks go one at a time.
+template <bool ROWB, int NG>
+__device__ __forceinline__ f32x4 proj_tile(const float *pa, const float *pb, int nb, int pe) {
+    constexpr int RB = ROWB ? 1 : 4;   // LDS reads of one B block
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    auto read = [&](int g, f32x4 &x, f32x4 &y) {
+        x = *reinterpret_cast<const f32x4 *>(pa + 16 * g);
+        if constexpr (ROWB) {
+            y = *reinterpret_cast<const f32x4 *>(pb + 16 * g);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) y[j] = pb[(16 * g + j) * pe];
+        }
+    };
+    int g0 = 0;
+    for (; g0 + NG <= nb; g0 += NG) {
+        f32x4 x[NG], y[NG];
+#pragma unroll
+        for (int b = 0; b < NG; ++b) read(g0 + b, x[b], y[b]);
+#pragma unroll
+        for (int b = 0; b < NG; ++b)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(x[b][j], y[b][j], acc, 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, NG * (1 + RB), 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 4 * NG, 0);
+    }
+    for (; g0 < nb; ++g0) {
+        f32x4 x, y;
+        read(g0, x, y);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(x[j], y[j], acc, 0, 0, 0);
+    }
+    return acc;
 }
 
 // Two 1024-thread workgroups per CU: eight waves per SIMD, <= 64 registers.
@@ -56,51 +123,61 @@ template <int kProjThreads>
 __global__ __launch_bounds__(kProjThreads, kProjThreads == 1024 ? 8 : 1) void proj_kernel(ProjArgs a) {
     extern __shared__ __attribute__((aligned(16))) float sm[];
     const int RT = a.RT, CT = a.CT, A = a.A;
-    const int CT4 = round4(CT), A4 = round4(A);
-    const int pe = CT4 + 4, pp = A4 + 4;
-    float *En_s = sm;                    // [RT][pe]
-    float *Gc_s = En_s + RT * pe;        // [A4][pe]
-    float *P_s = Gc_s + A4 * pe;         // [RT][pp]
-    int64_t *roff_s = reinterpret_cast<int64_t *>(P_s + RT * pp);   // [RT] remapped adjoint rows
+    const int R16 = round16(RT), C16 = round16(CT), A16 = round16(A);
+    const int pe = C16 + 4, pt = R16 + 4;
+    float *En_s = sm;                    // [R16][pe]
+    float *Gc_s = En_s + R16 * pe;       // [A16][pe]
+    float *Pt_s = Gc_s + A16 * pe;       // [A16][pt]: P_k transposed
+    int64_t *roff_s = reinterpret_cast<int64_t *>(Pt_s + A16 * pt);   // [RT] remapped adjoint rows
     const int tid = threadIdx.x;
+    constexpr int T = kProjThreads;
     const int64_t r0 = int64_t(blockIdx.y) * RT, c0 = int64_t(blockIdx.x) * CT;
     const int nr = int(min<int64_t>(RT, a.rows - r0)), nc = int(min<int64_t>(CT, a.cols - c0));
     if (a.Gc)
-        for (int r = tid; r < nr; r += kProjThreads) roff_s[r] = remap_off(a.rmap, r0 + r);
+        for (int r = tid; r < nr; r += T) roff_s[r] = remap_off32(a.rmap, uint32_t(r0 + r));
 
+    // Every load below comes from an in-bounds address (the tile corner for
+    // positions past the data) and is then replaced by 0 where it lies
+    // outside, so that the loads are issued unconditionally; positions are
+    // stepped with Walk rather than divided out per element.
+    //
     // E_{k+1} tile, split slices summed in slice order; zero padding.  Each
-    // thread keeps eight float4 loads in flight before adding them (one
-    // vector of eight slices with 1024 threads, two vectors of four with
-    // 256): 32 registers, so that two 1024-thread workgroups fit on a CU.
+    // thread keeps four float4 loads in flight before adding them (one
+    // vector of four slices with 1024 threads, two with 256), so that two
+    // 1024-thread workgroups fit on a CU.
     const bool vec = (a.cols % 4 == 0) && (CT % 4 == 0) && (a.in_stride % 4 == 0) &&
                      (reinterpret_cast<uintptr_t>(a.En) % 16 == 0);
+    const float *etile = a.En + r0 * a.cols + c0;
     if (vec) {
-        constexpr int JV = kProjThreads == 1024 ? 1 : 2, SS = kProjThreads == 1024 ? 8 : 4;
-        const int q4 = CT4 / 4, n4 = RT * q4;
-        for (int jb = 0; jb * kProjThreads < n4; jb += JV) {
+        constexpr int JV = T == 1024 ? 1 : 2, SS = 4;
+        const int q4 = C16 / 4, n4 = R16 * q4;
+        const int dr = T / q4, dc = T - dr * q4;
+        Walk w(tid, q4);
+        for (int jb = 0; jb * T < n4; jb += JV) {
             float4 v[JV];
             int ri[JV], ci[JV];
             bool ok[JV];
+            const float *src[JV];
 #pragma unroll
             for (int j = 0; j < JV; ++j) {
-                const int i = tid + kProjThreads * (jb + j);
-                ri[j] = i / q4;
-                ci[j] = (i - ri[j] * q4) * 4;
-                ok[j] = i < n4 && ri[j] < nr && ci[j] < nc;
+                ri[j] = w.r;
+                ci[j] = 4 * w.c;
+                ok[j] = ri[j] < nr && ci[j] < nc;
+                src[j] = etile + (ok[j] ? int64_t(ri[j]) * a.cols + ci[j] : 0);
                 v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+                w.step(q4, dr, dc);
             }
             for (int s0 = 0; s0 < a.nin; s0 += SS) {
                 float4 x[SS][JV];
 #pragma unroll
-                for (int ss = 0; ss < SS; ++ss)
+                for (int ss = 0; ss < SS; ++ss) {
+                    const int64_t so = int64_t(min(s0 + ss, a.nin - 1)) * a.in_stride;
 #pragma unroll
-                    for (int j = 0; j < JV; ++j)
-                        x[ss][j] = (ok[j] && s0 + ss < a.nin)
-                                       ? *reinterpret_cast<const float4 *>(a.En + (s0 + ss) * a.in_stride +
-                                                                           (r0 + ri[j]) * a.cols + c0 + ci[j])
-                                       : make_float4(0.f, 0.f, 0.f, 0.f);
+                    for (int j = 0; j < JV; ++j) x[ss][j] = *reinterpret_cast<const float4 *>(src[j] + so);
+                }
 #pragma unroll
-                for (int ss = 0; ss < SS; ++ss)
+                for (int ss = 0; ss < SS; ++ss) {
+                    if (s0 + ss >= a.nin) break;
 #pragma unroll
                     for (int j = 0; j < JV; ++j) {
                         v[j].x += x[ss][j].x;
@@ -108,189 +185,136 @@ __global__ __launch_bounds__(kProjThreads, kProjThreads == 1024 ? 8 : 1) void pr
                         v[j].z += x[ss][j].z;
                         v[j].w += x[ss][j].w;
                     }
+                }
             }
 #pragma unroll
             for (int j = 0; j < JV; ++j) {
-                const int i = tid + kProjThreads * (jb + j);
-                if (i < n4) *reinterpret_cast<float4 *>(En_s + ri[j] * pe + ci[j]) = v[j];
+                if (ri[j] >= R16) break;
+                *reinterpret_cast<float4 *>(En_s + ri[j] * pe + ci[j]) =
+                    ok[j] ? v[j] : make_float4(0.f, 0.f, 0.f, 0.f);
             }
         }
     } else {
-        for (int i = tid; i < RT * CT4; i += kProjThreads) {
-            const int r = i / CT4, c = i - r * CT4;
+        Walk w(tid, C16);
+        const int dr = T / C16, dc = T - dr * C16;
+        for (; w.r < R16; w.step(C16, dr, dc)) {
+            const bool ok = w.r < nr && w.c < nc;
+            const float *src = etile + (ok ? int64_t(w.r) * a.cols + w.c : 0);
             float v = 0.f;
-            if (r < nr && c < nc)
-                for (int s = 0; s < a.nin; ++s) v += a.En[s * a.in_stride + (r0 + r) * a.cols + c0 + c];
-            En_s[r * pe + c] = v;
+            for (int s = 0; s < a.nin; ++s) v += src[s * a.in_stride];
+            En_s[w.r * pe + w.c] = ok ? v : 0.f;
         }
     }
     // core and left-chain slices: every thread issues its loads before its
     // stores; the core slice as float4 where the E tile is (nc is then a
     // multiple of 4)
     if (a.Gc && vec && (reinterpret_cast<uintptr_t>(a.Gc) % 16 == 0)) {
-        const int q4 = CT4 / 4, n = A4 * q4;
-        for (int i0 = tid; i0 < n; i0 += kProjThreads * 4) {
+        const int q4 = C16 / 4;
+        const int dr = T / q4, dc = T - dr * q4;
+        Walk w(tid, q4);
+        const float *gtile = a.Gc + c0;
+        while (w.r < A16) {
             float4 v[4];
+            int ro[4], co[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int i = i0 + u * kProjThreads;
-                const int al = i / q4, c = (i - al * q4) * 4;
-                v[u] = (i < n && al < A && c < nc)
-                           ? *reinterpret_cast<const float4 *>(a.Gc + int64_t(al) * a.cols + c0 + c)
-                           : make_float4(0.f, 0.f, 0.f, 0.f);
+                ro[u] = w.r;
+                co[u] = 4 * w.c;
+                const bool ok = ro[u] < A && co[u] < nc;
+                v[u] = *reinterpret_cast<const float4 *>(gtile + (ok ? int64_t(ro[u]) * a.cols + co[u] : 0));
+                if (!ok) v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+                w.step(q4, dr, dc);
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int i = i0 + u * kProjThreads;
-                const int al = i / q4, c = (i - al * q4) * 4;
-                if (i < n) *reinterpret_cast<float4 *>(Gc_s + al * pe + c) = v[u];
-            }
+            for (int u = 0; u < 4; ++u)
+                if (ro[u] < A16) *reinterpret_cast<float4 *>(Gc_s + ro[u] * pe + co[u]) = v[u];
         }
     } else if (a.Gc) {
-        for (int i0 = tid; i0 < A4 * CT4; i0 += kProjThreads * 4) {
+        const int dr = T / C16, dc = T - dr * C16;
+        Walk w(tid, C16);
+        const float *gtile = a.Gc + c0;
+        while (w.r < A16) {
             float v[4];
+            int ro[4], co[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int i = i0 + u * kProjThreads;
-                const int al = i / CT4, c = i - al * CT4;
-                v[u] = (i < A4 * CT4 && al < A && c < nc) ? a.Gc[int64_t(al) * a.cols + c0 + c] : 0.f;
+                ro[u] = w.r;
+                co[u] = w.c;
+                const bool ok = ro[u] < A && co[u] < nc;
+                v[u] = gtile[ok ? int64_t(ro[u]) * a.cols + co[u] : 0];
+                if (!ok) v[u] = 0.f;
+                w.step(C16, dr, dc);
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int i = i0 + u * kProjThreads;
-                const int al = i / CT4, c = i - al * CT4;
-                if (i < A4 * CT4) Gc_s[al * pe + c] = v[u];
-            }
+            for (int u = 0; u < 4; ++u)
+                if (ro[u] < A16) Gc_s[ro[u] * pe + co[u]] = v[u];
         }
     }
-    if (a.P)
-        for (int i0 = tid; i0 < RT * A4; i0 += kProjThreads * 4) {
+    if (a.P) {
+        // P_k [r][a] read along a, stored transposed
+        const int dr = T / A16, dc = T - dr * A16;
+        Walk w(tid, A16);
+        const float *ptile = a.P + r0 * A;
+        while (w.r < R16) {
             float v[4];
+            int ro[4], co[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int i = i0 + u * kProjThreads;
-                const int r = i / A4, al = i - r * A4;
-                v[u] = (i < RT * A4 && r < nr && al < A) ? a.P[(r0 + r) * A + al] : 0.f;
+                ro[u] = w.r;
+                co[u] = w.c;
+                const bool ok = ro[u] < nr && co[u] < A;
+                v[u] = ptile[ok ? ro[u] * A + co[u] : 0];
+                if (!ok) v[u] = 0.f;
+                w.step(A16, dr, dc);
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int i = i0 + u * kProjThreads;
-                const int r = i / A4, al = i - r * A4;
-                if (i < RT * A4) P_s[r * pp + al] = v[u];
-            }
+            for (int u = 0; u < 4; ++u)
+                if (ro[u] < R16) Pt_s[co[u] * pt + ro[u]] = v[u];
         }
+    }
     __syncthreads();
 
-    // Both products on MFMA (v_mfma_f32_32x32x2f32) in 32 x 32 output tiles:
-    //   adjoint tiles (rows x a), K = the CT4 columns,
-    //   meet tiles    (a x columns), K = the RT rows.
-    // Lane l supplies A[l % 32][k0 + l / 32] and B[k0 + l / 32][l % 32];
-    // accumulator v of lane l is row 8 (v / 4) + 4 (l / 32) + v % 4, column
-    // l % 32.  Tiles are dealt round-robin to the waves.
-    const int lane = tid & 63, wave = tid >> 6;
-    const int li = lane & 31, lk = lane >> 5;
-    const int ta_m = (RT + 31) / 32, ta_n = (A + 31) / 32;
+    // Both products on MFMA (v_mfma_f32_16x16x4f32) in 16 x 16 output tiles:
+    //   adjoint tiles (rows x a), K = the C16 columns,
+    //   meet tiles    (a x columns), K = the R16 rows.
+    // Lane l = 16 q + i supplies A[i][s] and B[s][i] of k slot s = q and
+    // receives rows 4 q + v (v = 0..3), column i.  In the 16-deep block g of
+    // K, product j of the block gives slot q the k index 16 g + 4 q + j, so a
+    // lane's four values along a contiguous k run are one 16-byte read.
+    // Adjoint: A = E_{k+1} rows, B = G~ rows (k = column, contiguous).  Meet:
+    // A = P_k^T rows (k = row, contiguous), B = E_{k+1} columns (k = row).
+    // Tiles are dealt round-robin to the waves.
+    // blocks per operand group: 1024-thread workgroups have 64 registers
+    constexpr int NG = T == 1024 ? 2 : 4;
+    // the wave index as a scalar: tile choice and loop bounds stay uniform
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int li = lane & 15, lq = lane >> 4;
+    const int ta_m = R16 / 16, ta_n = A16 / 16;
     const int nadj = a.Gc ? ta_m * ta_n : 0;
-    const int tm_n = (CT4 + 31) / 32;
+    const int tm_n = C16 / 16;
     const int nmeet = a.P ? ta_n * tm_n : 0;
     for (int t = wave; t < nadj + nmeet; t += kProjThreads / 64) {
-        f32x16 acc;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[v] = 0.f;
         if (t < nadj) {
             const int mt = t / ta_n, nt = t - mt * ta_n;
-            const int ra = mt * 32 + li, gb = nt * 32 + li;
-            const float *pa = En_s + min(ra, RT - 1) * pe + lk;
-            const float *pb = Gc_s + min(gb, A4 - 1) * pe + lk;
-            const bool va = ra < RT, vb = gb < A4;
-            if constexpr (kProjThreads == 1024) {
-                // 64 registers: one guarded group at a time
-                for (int k = 0; k < CT4; k += 8) {
-                    float x[4], y[4];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        x[u] = va ? pa[k + 2 * u] : 0.f;
-                        y[u] = vb ? pb[k + 2 * u] : 0.f;
-                    }
-#pragma unroll
-                    for (int u = 0; u < 4; ++u)
-                        if (k + 2 * u < CT4) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u], y[u], acc, 0, 0, 0);
-                }
-            } else {
-                // whole groups of four products without per-product branches
-                // (the scheduler can then hoist the next group's LDS reads),
-                // then the last two (CT4 is a multiple of 4)
-                int k = 0;
-#pragma unroll 2
-                for (; k + 8 <= CT4; k += 8) {
-                    float x[4], y[4];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        x[u] = va ? pa[k + 2 * u] : 0.f;
-                        y[u] = vb ? pb[k + 2 * u] : 0.f;
-                    }
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u], y[u], acc, 0, 0, 0);
-                }
-                if (k < CT4) {
-                    const float x0 = va ? pa[k] : 0.f, y0 = vb ? pb[k] : 0.f;
-                    const float x1 = va ? pa[k + 2] : 0.f, y1 = vb ? pb[k + 2] : 0.f;
-                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x0, y0, acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x1, y1, acc, 0, 0, 0);
-                }
-            }
+            const f32x4 acc = proj_tile<true, NG>(En_s + (mt * 16 + li) * pe + 4 * lq,
+                                              Gc_s + (nt * 16 + li) * pe + 4 * lq, C16 / 16, pe);
             float *dst = a.Eout + int64_t(blockIdx.x) * a.out_stride;
-            const int al = nt * 32 + li;
+            const int al = nt * 16 + li;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int r = mt * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
+            for (int v = 0; v < 4; ++v) {
+                const int r = mt * 16 + 4 * lq + v;
                 if (r < nr && al < A) dst[roff_s[r] + al] = acc[v];
             }
         } else {
             const int u0 = t - nadj;
             const int mt = u0 / tm_n, nt = u0 - mt * tm_n;
-            const int am = mt * 32 + li, cn = nt * 32 + li;
-            const bool va = am < A4, vb = cn < CT4;
-            const float *pa = P_s + lk * pp + min(am, A4 - 1);
-            const float *pb = En_s + lk * pe + min(cn, CT4 - 1);
-            if constexpr (kProjThreads == 1024) {
-                for (int r = 0; r < RT; r += 8) {
-                    float x[4], y[4];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        const int rr = min(r + 2 * u, RT - 2);
-                        x[u] = va ? pa[rr * pp] : 0.f;
-                        y[u] = vb ? pb[rr * pe] : 0.f;
-                    }
-#pragma unroll
-                    for (int u = 0; u < 4; ++u)
-                        if (r + 2 * u < RT) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u], y[u], acc, 0, 0, 0);
-                }
-            } else {
-                int r = 0;
-#pragma unroll 2
-                for (; r + 8 <= RT; r += 8) {
-                    float x[4], y[4];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        x[u] = va ? pa[(r + 2 * u) * pp] : 0.f;
-                        y[u] = vb ? pb[(r + 2 * u) * pe] : 0.f;
-                    }
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u], y[u], acc, 0, 0, 0);
-                }
-                if (r < RT) {   // RT is a multiple of 4
-                    const float x0 = va ? pa[r * pp] : 0.f, y0 = vb ? pb[r * pe] : 0.f;
-                    const float x1 = va ? pa[(r + 2) * pp] : 0.f, y1 = vb ? pb[(r + 2) * pe] : 0.f;
-                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x0, y0, acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x1, y1, acc, 0, 0, 0);
-                }
-            }
+            const f32x4 acc = proj_tile<false, NG>(Pt_s + (mt * 16 + li) * pt + 4 * lq,
+                                               En_s + (4 * lq) * pe + nt * 16 + li, R16 / 16, pe);
             float *dst = a.part + int64_t(blockIdx.y) * A * a.cols;
-            const int c = nt * 32 + li;
+            const int c = nt * 16 + li;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int al = mt * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
+            for (int v = 0; v < 4; ++v) {
+                const int al = mt * 16 + 4 * lq + v;
                 if (al < A && c < nc) dst[int64_t(al) * a.cols + c0 + c] = acc[v];
             }
         }
@@ -556,7 +580,9 @@ __global__ __launch_bounds__(256) void wtile_kernel(WBuildArgs a) {
 bool proj_supported(int A) { return A >= 1 && A <= kProjMaxA; }
 
 void proj_tiles(int64_t rows, int64_t cols, int A, int &RT, int &CT) {
-    CT = int(cols <= 256 ? cols : 128);
+    // whole column ranges up to 256; wider steps in chunks of 64 (measured
+    // faster than 128 on the 2048 x 1440 rank-45 step)
+    CT = int(cols <= 256 ? cols : 64);
     RT = 64;
     while (proj_lds_floats(RT, CT, A) * sizeof(float) > kProjLds && CT > 32) CT = (CT + 1) / 2;
     while (proj_lds_floats(RT, CT, A) * sizeof(float) > kProjLds && RT > 8) RT /= 2;
@@ -571,11 +597,11 @@ bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, int &QI, int &Q
     // more LDS than allowed
     int qi = int(std::min<int64_t>(NI, std::max(1, (32 + nx - 1) / nx)));
     int qj = int(std::min<int64_t>(NJ, std::max(1, (96 + ny - 1) / ny)));
-    while (wtile_lds_floats(A, qi, qj, nx, ny) * sizeof(float) > kProjLds && (qi > 1 || qj > 1)) {
+    while (wtile_lds_floats(A, qi, qj, nx, ny) * sizeof(float) > kWtileLds && (qi > 1 || qj > 1)) {
         if (qj >= qi && qj > 1) qj = (qj + 1) / 2;
         else qi = (qi + 1) / 2;
     }
-    if (wtile_lds_floats(A, qi, qj, nx, ny) * sizeof(float) > kProjLds) return false;
+    if (wtile_lds_floats(A, qi, qj, nx, ny) * sizeof(float) > kWtileLds) return false;
     QI = qi;
     QJ = qj;
     return true;
@@ -584,10 +610,10 @@ bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, int &QI, int &Q
 int launch_wbuild(const WBuildArgs &a, void *stream) {
     if (a.NI <= 0 || a.NJ <= 0 || (!a.out && !a.out_t)) return 0;
     const size_t lds = wtile_lds_floats(a.A, a.QI, a.QJ, a.nx, a.ny) * sizeof(float);
-    if (lds > kProjLds || a.QI < 1 || a.QJ < 1) return int(hipErrorInvalidValue);
+    if (lds > kWtileLds || a.QI < 1 || a.QJ < 1) return int(hipErrorInvalidValue);
     if (!launch_check_mode()) {
         static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(wtile_kernel),
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(kProjLds)));
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(kWtileLds)));
         if (set) return set;
     }
     const int64_t gx = (a.NJ + a.QJ - 1) / a.QJ, gy = (a.NI + a.QI - 1) / a.QI;
@@ -598,14 +624,27 @@ int launch_wbuild(const WBuildArgs &a, void *stream) {
 
 int launch_proj(const ProjArgs &a, void *stream) {
     if (a.rows <= 0 || a.cols <= 0) return 0;
-    if (!proj_supported(a.A) || a.RT % 4 || a.CT < 1) return int(hipErrorInvalidValue);
+    if (!proj_supported(a.A) || a.RT % 4 || a.CT < 1 || a.nin < 1) return int(hipErrorInvalidValue);
+    // row offsets are taken apart in 32 bits
+    if (a.Gc) {
+        if (a.rows >= (int64_t(1) << 32)) return int(hipErrorInvalidValue);
+        for (int t = 1; t < a.rmap.nd; ++t)
+            if (a.rmap.radix[t] < 1 || a.rmap.radix[t] >= (int64_t(1) << 32)) return int(hipErrorInvalidValue);
+    }
     const size_t lds = proj_lds_floats(a.RT, a.CT, a.A) * sizeof(float);
     if (lds > kProjLds) return int(hipErrorInvalidValue);
     dim3 grid(unsigned((a.cols + a.CT - 1) / a.CT), unsigned((a.rows + a.RT - 1) / a.RT));
     // 1024 threads when the tile load is large (many loads in flight per CU),
     // else 256 (several workgroups per CU)
+    if (!launch_check_mode()) {
+        static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(proj_kernel<kProjThreadsMax>),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(kProjLds))) |
+                               int(hipFuncSetAttribute(reinterpret_cast<const void *>(proj_kernel<256>),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(kProjLds)));
+        if (set) return set;
+    }
     const int64_t loads4 = int64_t(a.RT) * ((a.CT + 3) / 4) * std::max(1, a.nin);
-    if (loads4 > 4096)
+    if (loads4 >= 4096)
         COMERA_LAUNCH((proj_kernel<kProjThreadsMax>), grid, dim3(kProjThreadsMax), lds, hipStream_t(stream), a);
     else
         COMERA_LAUNCH((proj_kernel<256>), grid, dim3(256), lds, hipStream_t(stream), a);
