@@ -91,17 +91,22 @@ __global__ __launch_bounds__(kFoldThreads) void fold_kernel(FoldArgs a) {
     }
 }
 
-// Workgroup of 256 threads = (256 / G) outputs x G split groups (G = 1 .. 8
-// per core, about eight splits per group): group g sums the splits
-// [g S / G, (g + 1) S / G) in order, then group 0 adds the G group sums in
-// order.  One flattened grid covers all cores (a.blk0[k] = first block of
-// core k).  The result does not depend on the launch shape other than G.
-__global__ __launch_bounds__(256) void expand_kernel(ExpandArgs a) {
-    __shared__ float red[8][257];
+// Workgroup of NT threads = (NT / G) outputs x G split groups (G = 1 .. 8
+// per core, about eight splits per group; up to 64 for a core in more than
+// 512 partials, so that a thread still waits for only a few rounds of loads):
+// group g sums the splits [g S / G, (g + 1) S / G) in order, then group 0
+// adds the G group sums in order.  One flattened grid covers all cores
+// (a.blk0[k] = first block of core k).  The result does not depend on the
+// launch shape other than G.  NT = 256 while every core has G <= 8, else
+// 1024 (the many-split cores then still get a few hundred workgroups).
+constexpr int kExpandMaxGroups = 64;
+template <int NT>
+__global__ __launch_bounds__(NT) void expand_kernel(ExpandArgs a) {
+    __shared__ float red[NT + kExpandMaxGroups];   // [G][no + 1]
     int k = 0;
     while (k + 1 < a.d && int(blockIdx.x) >= a.blk0[k + 1]) ++k;
     if (!a.dG[k]) return;
-    const int G = a.groups[k], no = 256 / G;
+    const int G = a.groups[k], no = NT / G;
     const int rl = a.r[k], rr = a.r[k + 1], m = a.m[k], n = a.n[k];
     const int crl = a.rc[k], crr = a.rc[k + 1];
     const int tot32 = rl * m * n * rr;     // core sizes are far below 2^31 (host checks)
@@ -142,11 +147,11 @@ __global__ __launch_bounds__(256) void expand_kernel(ExpandArgs a) {
         }
         for (; s < s1; ++s) v += part[s * csize + ci];
     }
-    red[g][lo] = v;
+    red[g * (no + 1) + lo] = v;
     __syncthreads();
     if (g == 0 && o < tot32) {
-        float t = red[0][lo];
-        for (int gg = 1; gg < G; ++gg) t += red[gg][lo];
+        float t = red[lo];
+        for (int gg = 1; gg < G; ++gg) t += red[gg * (no + 1) + lo];
         if (ci < 0) t = 0.f;
         else if (D) t *= D[o % rr];
         a.dG[k][o] = t;
@@ -300,18 +305,30 @@ int launch_fold(const FoldArgs &a, void *stream) {
 
 int launch_expand(const ExpandArgs &a_in, void *stream) {
     ExpandArgs a = a_in;
+    int gmax = 1;
+    for (int k = 0; k < a.d; ++k) {
+        // up to 8 groups; up to 64 for cores in more than 512 partials
+        // (measured: 8 groups of 256 threads are faster up to 256 partials)
+        const int gcap = a.splits[k] > 512 ? kExpandMaxGroups : 8;
+        int G = 1;
+        while (G < gcap && G * 8 < a.splits[k]) G *= 2;
+        a.groups[k] = G;
+        if (a.dG[k]) gmax = std::max(gmax, G);
+    }
+    const int nt = gmax <= 8 ? 256 : 1024;
     int blocks = 0;
     for (int k = 0; k < a.d; ++k) {
-        int G = 1;
-        while (G < 8 && G * 8 < a.splits[k]) G *= 2;
-        a.groups[k] = G;
         a.blk0[k] = blocks;
         const int64_t total = a.dG[k] ? int64_t(a.r[k]) * a.m[k] * a.n[k] * a.r[k + 1] : 0;
-        blocks += int((total + 256 / G - 1) / (256 / G));
+        const int no = nt / a.groups[k];
+        blocks += int((total + no - 1) / no);
     }
     for (int k = a.d; k < kMaxCores; ++k) a.blk0[k] = blocks;
     if (blocks == 0) return 0;
-    COMERA_LAUNCH(expand_kernel, dim3(unsigned(blocks)), dim3(256), 0, hipStream_t(stream), a);
+    if (nt == 256)
+        COMERA_LAUNCH_NAMED("expand_kernel", expand_kernel<256>, dim3(unsigned(blocks)), dim3(256), 0, hipStream_t(stream), a);
+    else
+        COMERA_LAUNCH_NAMED("expand_kernel", expand_kernel<1024>, dim3(unsigned(blocks)), dim3(1024), 0, hipStream_t(stream), a);
     return launch_status();
 }
 
