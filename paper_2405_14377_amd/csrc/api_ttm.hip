@@ -89,8 +89,23 @@ int build_chain(const comera_ttm_plan_s *sp, void *ws, DenseBuild &bd, int want,
         const bool last = k == d - 1;
         if (!last) {
             void *out = at(ws, L.p[k + 1]);
-            int e = chain_gemm(bd.P[k], bd.gc[k], out, false, Il, Jl, int(sp->rho[k]), int(sp->s.n[k]),
+            int e = 0;
+            if (lchain_supported(int(sp->rho[k]))) {
+                LChainArgs la;
+                la.P = bd.P[k];
+                la.G = bd.gc[k];
+                la.out = reinterpret_cast<float *>(out);
+                la.NI = Il;
+                la.NJ = Jl;
+                la.A = int(sp->rho[k]);
+                la.nx = int(sp->s.n[k]);
+                la.ny = int(sp->s.m[k]);
+                la.C = int(sp->rho[k + 1]);
+                e = launch_lchain(la, stream);
+            } else {
+                e = chain_gemm(bd.P[k], bd.gc[k], out, false, Il, Jl, int(sp->rho[k]), int(sp->s.n[k]),
                                int(sp->s.m[k]), int(sp->rho[k + 1]), stream, kChainNormal);
+            }
             if (e) return note_hip(e, "chain GEMM");
             bd.P[k + 1] = reinterpret_cast<float *>(out);
             Il *= sp->s.n[k];

@@ -328,6 +328,19 @@ struct WBuildArgs {
 bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, int &QI, int &QJ);
 int launch_wbuild(const WBuildArgs &a, void *stream);
 
+// One inner step of the chain (proj.hip), fp32, ranks A up to 64: with the
+// left chain P [NI][NJ][A] and the folded core G [A][nx][ny][C],
+//   out[(I x)][(J y)][c] = sum_a P[I][J][a] G[a][x][y][c]
+struct LChainArgs {
+    const float *P;
+    const float *G;
+    float *out;
+    int64_t NI, NJ;
+    int A, nx, ny, C;
+};
+bool lchain_supported(int A);
+int launch_lchain(const LChainArgs &a, void *stream);
+
 
 // operand type code of FP8 (OCP E4M3) GEMM operands, beside COMERA_F32 / COMERA_BF16
 constexpr int kDtypeFp8 = 2;

@@ -321,6 +321,115 @@ __global__ __launch_bounds__(kProjThreads, kProjThreads == 1024 ? 8 : 1) void pr
     }
 }
 
+// ---------------------------------------------------------------- chain step
+// One inner step of the batch-free chain (eq. TTM, read left to right): with
+// the left chain P = P_k [I][J][a] and the folded core G [a][x][y][c],
+//   P_{k+1}[(I x)][(J y)][c] = sum_a P[I][J][a] G[a][x][y][c],
+// a product with rows (I, J), columns (x, y, c) and the rank as its short
+// contraction.  A workgroup owns 64 rows x 64 columns: the P rows and the
+// G columns (transposed) are staged in LDS zero-padded to 16-deep blocks of
+// the rank, and each wave forms one 16-row block across the four 16-column
+// blocks on v_mfma_f32_16x16x4f32, one 16-byte read per operand and block
+// (the k order of the projection kernel).  The interleaved output offsets
+// of the tile's rows and columns are taken apart once, into LDS.
+constexpr int kLcRows = 64, kLcCols = 64;
+
+__global__ __launch_bounds__(256) void lchain_kernel(LChainArgs a) {
+    __shared__ __attribute__((aligned(16))) float Ps[kLcRows * (kProjMaxA + 4)];
+    __shared__ __attribute__((aligned(16))) float Gt[kLcCols * (kProjMaxA + 4)];
+    __shared__ int64_t roff[kLcRows], coff[kLcCols];
+    const int A = a.A, A16 = round16(A), pa = A16 + 4;
+    const int64_t rows = a.NI * a.NJ, cols = int64_t(a.nx) * a.ny * a.C;
+    const int64_t r0 = int64_t(blockIdx.y) * kLcRows, c0 = int64_t(blockIdx.x) * kLcCols;
+    const int nr = int(min<int64_t>(kLcRows, rows - r0)), nc = int(min<int64_t>(kLcCols, cols - c0));
+    const int tid = threadIdx.x;
+    const int64_t orow = int64_t(a.nx) * a.NJ * a.ny * a.C;   // stride of I in the output
+    const int64_t ox = a.NJ * a.ny * a.C;                     // stride of x
+    if (tid < kLcRows) {
+        // rows below 2^32 (launch_lchain checks)
+        const uint32_t r = uint32_t(r0 + tid), nj = uint32_t(a.NJ);
+        const uint32_t I = r / nj, J = r - I * nj;
+        roff[tid] = int64_t(I) * orow + int64_t(J) * a.ny * a.C;
+    } else if (tid < kLcRows + kLcCols) {
+        const int t = tid - kLcRows;
+        const uint32_t col = uint32_t(c0 + t), C = uint32_t(a.C), ny = uint32_t(a.ny);
+        const uint32_t q = col / C, c = col - q * C;
+        const uint32_t x = q / ny, y = q - x * ny;
+        coff[t] = int64_t(x) * ox + int64_t(y) * a.C + c;
+    }
+    // P rows (contiguous: 64 A floats from row r0) and G columns, loads
+    // from in-bounds addresses then zero outside
+    {
+        const float *pt = a.P + r0 * A;
+        const int dr = 256 / A16, dc = 256 - dr * A16;
+        Walk w(tid, A16);
+        while (w.r < kLcRows) {
+            float v[4];
+            int ro[4], co[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                ro[u] = w.r;
+                co[u] = w.c;
+                const bool ok = ro[u] < nr && co[u] < A;
+                v[u] = pt[ok ? ro[u] * A + co[u] : 0];
+                if (!ok) v[u] = 0.f;
+                w.step(A16, dr, dc);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (ro[u] < kLcRows) Ps[ro[u] * pa + co[u]] = v[u];
+        }
+    }
+    {
+        const float *gt = a.G + c0;
+        constexpr int dr = 256 / kLcCols, dc = 0;
+        Walk w(tid, kLcCols);
+        while (w.r < A16) {
+            float v[4];
+            int ro[4], co[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                ro[u] = w.r;
+                co[u] = w.c;
+                const bool ok = ro[u] < A && co[u] < nc;
+                v[u] = gt[ok ? int64_t(ro[u]) * cols + co[u] : 0];
+                if (!ok) v[u] = 0.f;
+                w.step(kLcCols, dr, dc);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (ro[u] < A16) Gt[co[u] * pa + ro[u]] = v[u];
+        }
+    }
+    __syncthreads();
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int li = lane & 15, lq = lane >> 4;
+    f32x4 acc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const float *pa_ = Ps + (wave * 16 + li) * pa + 4 * lq;
+    const float *pb_ = Gt + li * pa + 4 * lq;
+    for (int g = 0; g < A16 / 16; ++g) {
+        const f32x4 x = *reinterpret_cast<const f32x4 *>(pa_ + 16 * g);
+        f32x4 y[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) y[t] = *reinterpret_cast<const f32x4 *>(pb_ + t * 16 * pa + 16 * g);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(x[j], y[t][j], acc[t], 0, 0, 0);
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const int col = t * 16 + li;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int row = wave * 16 + 4 * lq + v;
+            if (row < nr && col < nc) a.out[roff[row] + coff[col]] = acc[t][v];
+        }
+    }
+}
+
 // ---------------------------------------------------------------- W build
 // Last step of the batch-free chain (eq. TTM): with the left chain
 // P = P_{d-1} [I][J][a] and the folded last core G [a][x][y] (x = i_{d-1},
@@ -648,6 +757,19 @@ int launch_proj(const ProjArgs &a, void *stream) {
         COMERA_LAUNCH((proj_kernel<kProjThreadsMax>), grid, dim3(kProjThreadsMax), lds, hipStream_t(stream), a);
     else
         COMERA_LAUNCH((proj_kernel<256>), grid, dim3(256), lds, hipStream_t(stream), a);
+    return launch_status();
+}
+
+bool lchain_supported(int A) { return A >= 1 && A <= kProjMaxA; }
+
+int launch_lchain(const LChainArgs &a, void *stream) {
+    const int64_t rows = a.NI * a.NJ, cols = int64_t(a.nx) * a.ny * a.C;
+    if (rows <= 0 || cols <= 0) return 0;
+    if (!lchain_supported(a.A) || rows >= (int64_t(1) << 32) || cols >= (int64_t(1) << 32))
+        return int(hipErrorInvalidValue);
+    const int64_t gx = (cols + kLcCols - 1) / kLcCols, gy = (rows + kLcRows - 1) / kLcRows;
+    if (gx >= (int64_t(1) << 31) || gy > 65535) return int(hipErrorInvalidValue);
+    COMERA_LAUNCH(lchain_kernel, dim3(unsigned(gx), unsigned(gy)), dim3(256), 0, hipStream_t(stream), a);
     return launch_status();
 }
 
