@@ -692,11 +692,16 @@ void proj_tiles(int64_t rows, int64_t cols, int A, int &RT, int &CT) {
     // whole column ranges up to 256; wider steps in chunks of 64 (measured
     // faster than 128 on the 2048 x 1440 rank-45 step)
     CT = int(cols <= 256 ? cols : 64);
-    RT = 64;
+    // 128-row tiles where they still give 256 workgroups (fewer meet
+    // partials; measured faster on the 65536-row step of the 1024<->4096
+    // pair), else 64; halved while the grid holds fewer than 160 workgroups
+    // (a tile over many dW slices is a long load: 192 workgroups of 32 rows
+    // beat 384 of 16 on the 6144-row, 26-slice step of the 768x768 layer)
+    RT = (rows >= 256 * 128 && proj_lds_floats(128, CT, A) * sizeof(float) <= kProjLds) ? 128 : 64;
     while (proj_lds_floats(RT, CT, A) * sizeof(float) > kProjLds && CT > 32) CT = (CT + 1) / 2;
     while (proj_lds_floats(RT, CT, A) * sizeof(float) > kProjLds && RT > 8) RT /= 2;
     const int64_t nct = (cols + CT - 1) / CT;
-    while (RT > 8 && ((rows + RT - 1) / RT) * nct < 256) RT /= 2;
+    while (RT > 8 && ((rows + RT - 1) / RT) * nct < 160) RT /= 2;
 }
 
 bool wbuild_tiles(int64_t NI, int64_t NJ, int A, int nx, int ny, int &QI, int &QJ) {
