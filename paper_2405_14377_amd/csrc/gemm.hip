@@ -787,7 +787,8 @@ dim3 tile_grid(const GemmArgs &g, int bm, int bn, GemmParams &q) {
 // ---------------------------------------------------------------- DMA path
 // bf16 products whose operands are both K-contiguous (KC: forward, dX) or
 // both M/N-contiguous (MN: dW = X^T dY), 256 x 256 tiles of eight waves
-// (128 x 64 each), K stages of 64 in two LDS slots.  The operand tiles go
+// (128 x 64 each; KC also 256 x 192 tiles of waves of 64 x 96), K stages of
+// 64 in two LDS slots.  The operand tiles go
 // from global memory straight into LDS (global_load_lds_dwordx4: lane l of a
 // wave writes 16 bytes at the instruction's LDS base + 16 l), so they take no
 // registers and no LDS store instructions, and the loads of stage kt + 1 fly
@@ -827,18 +828,28 @@ constexpr size_t dma_main_lds() {
 // tile.  KC: row 8 (4 w + j) + l / 8, position l % 8.  MN: k row
 // 2 (4 w + j) + l / 32, position l % 32.  Rows / columns past the operand
 // are clamped (their results are never stored).
-template <bool MN>
+template <bool MN, int IPB = 4>
 __device__ __forceinline__ void dma_offsets(const GemmParams &p, int64_t m0, int64_t n0, int wave, int lane,
-                                            uint32_t (&aoffs)[4], uint32_t (&boffs)[4]) {
+                                            uint32_t (&aoffs)[4], uint32_t (&boffs)[IPB]) {
     constexpr int ESZ = int(sizeof(uint16_t));
+    static_assert(!MN || IPB == 4, "the dW tile is 256 wide");
+    if constexpr (!MN) {
+        // B tiles of 64 IPB rows (256 or 192): IPB instructions per wave
+#pragma unroll
+        for (int j = 0; j < IPB; ++j) {
+            const int row = (wave * IPB + j) * 8 + (lane >> 3);
+            const int c = (lane & 7) ^ ((row >> 1) & 7);
+            const int64_t gb = min(n0 + row, p.N - 1);
+            boffs[j] = uint32_t((gb * p.ldb + c * 8) * ESZ);
+        }
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         if constexpr (!MN) {
             const int row = (wave * 4 + j) * 8 + (lane >> 3);
             const int c = (lane & 7) ^ ((row >> 1) & 7);
-            const int64_t ga = min(m0 + row, p.M - 1), gb = min(n0 + row, p.N - 1);
+            const int64_t ga = min(m0 + row, p.M - 1);
             aoffs[j] = uint32_t((ga * p.lda + c * 8) * ESZ);
-            boffs[j] = uint32_t((gb * p.ldb + c * 8) * ESZ);
         } else {
             const int kr = (wave * 4 + j) * 2 + (lane >> 5);
             const int c = (lane & 31) ^ (4 * (kr & 3));
@@ -849,16 +860,18 @@ __device__ __forceinline__ void dma_offsets(const GemmParams &p, int64_t m0, int
     }
 }
 
-__device__ __forceinline__ void dma_issue(char *sa, const char *ga, const char *gb, const uint32_t (&aoffs)[4],
-                                          const uint32_t (&boffs)[4], int wave) {
-    sa += wave * 4 * 1024;
-    char *sb = sa + kDmaOpB;
+template <int IPB = 4>
+__device__ __forceinline__ void dma_issue(char *st, const char *ga, const char *gb, const uint32_t (&aoffs)[4],
+                                          const uint32_t (&boffs)[IPB], int wave) {
+    char *sa = st + wave * 4 * 1024;
+    char *sb = st + kDmaOpB + wave * IPB * 1024;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(ga + aoffs[j]), (lds_void_t *)(sa + j * 1024),
                                          16, 0, 0);
-        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(gb + boffs[j]), (lds_void_t *)(sb + j * 1024),
-                                         16, 0, 0);
+        if (j < IPB)
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(gb + boffs[j]),
+                                             (lds_void_t *)(sb + j * 1024), 16, 0, 0);
     }
 }
 
@@ -894,17 +907,19 @@ __device__ __forceinline__ void dma_mma(f32x16 (&acc)[TM][TN], const char *st, c
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[j], av[i], acc[i][j], 0, 0, 0);
     }
     // the operands of step ks + 1 are read between the products of step ks
-    __builtin_amdgcn_sched_group_barrier(0x100, 6 * RPS, 0);
+    constexpr int NR = TM + TN, NM = TM * TN;
+    static_assert(NM >= NR, "more products than operand reads per k step");
+    __builtin_amdgcn_sched_group_barrier(0x100, NR * RPS, 0);
 #pragma unroll
     for (int r = 0; r < kDmaKT / 16 - 1; ++r) {
 #pragma unroll
-        for (int t = 0; t < 6; ++t) {
+        for (int t = 0; t < NR; ++t) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, RPS, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
     __builtin_amdgcn_s_setprio(0);
 }
 
@@ -918,9 +933,13 @@ __device__ __forceinline__ void dma_stage_barrier() {
     asm volatile("s_barrier" ::: "memory");
 }
 
-template <bool OUT_BF16>
+// BN = 256: waves of 128 x 64; BN = 192 (products whose 256 x 256 tiles
+// would leave CUs idle, e.g. N = 768): waves of 64 x 96, B tiles of 192 rows
+template <bool OUT_BF16, int BN = 256>
 __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
-    constexpr int BM = 256, BN = 256, WM = 128, WN = 64, NT = 512, KT = kDmaKT;
+    static_assert(BN == 256 || BN == 192, "tile width");
+    constexpr int BM = 256, WM = BN == 256 ? 128 : 64, WN = BN == 256 ? 64 : 96, NT = 512, KT = kDmaKT;
+    constexpr int IPB = BN / 64;   // B-operand load instructions per wave
     constexpr int TM = WM / 32, TN = WN / 32, WAVES_N = BN / WN;
     constexpr int ESZ = int(sizeof(uint16_t));
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -934,8 +953,8 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     const char *abase = reinterpret_cast<const char *>(p.A);
     const char *bbase = reinterpret_cast<const char *>(p.B);
     constexpr int64_t kstep = KT * ESZ;
-    uint32_t aoffs[4], boffs[4];
-    dma_offsets<false>(p, m0, n0, wave, lane, aoffs, boffs);
+    uint32_t aoffs[4], boffs[IPB];
+    dma_offsets<false, IPB>(p, m0, n0, wave, lane, aoffs, boffs);
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -945,7 +964,7 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    if (ntiles > 0) dma_issue(smem, abase, bbase, aoffs, boffs, wave);
+    if (ntiles > 0) dma_issue<IPB>(smem, abase, bbase, aoffs, boffs, wave);
     for (int i = tid; i < BM; i += NT) roff[i] = m0 + i < p.M ? remap(p.rmap, m0 + i) : int64_t(-1);
     for (int i = tid; i < BN; i += NT) coff[i] = n0 + i < p.N ? remap(p.cmap, n0 + i) : int64_t(-1);
 
@@ -963,7 +982,7 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     for (int kt = 0; kt < ntiles; ++kt) {
         dma_stage_barrier();
         if (kt + 1 < ntiles)
-            dma_issue(smem + ((kt + 1) & 1) * kDmaStageB, abase + (kt + 1) * kstep, bbase + (kt + 1) * kstep, aoffs,
+            dma_issue<IPB>(smem + ((kt + 1) & 1) * kDmaStageB, abase + (kt + 1) * kstep, bbase + (kt + 1) * kstep, aoffs,
                       boffs, wave);
         dma_mma<false, TM, TN>(acc, smem + (kt & 1) * kDmaStageB, aaddr, baddr, kpos);
     }
@@ -1010,7 +1029,7 @@ __global__ __launch_bounds__(512) void gemm_dma_mn_kernel(GemmParams p) {
     const char *bbase = reinterpret_cast<const char *>(p.B) + kbeg * p.ldb * ESZ;
     const int64_t astep = KT * p.lda * ESZ, bstep = KT * p.ldb * ESZ;
     uint32_t aoffs[4], boffs[4];
-    dma_offsets<true>(p, m0, n0, wave, lane, aoffs, boffs);
+    dma_offsets<true, 4>(p, m0, n0, wave, lane, aoffs, boffs);
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -1020,7 +1039,7 @@ __global__ __launch_bounds__(512) void gemm_dma_mn_kernel(GemmParams p) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    if (ntiles > 0) dma_issue(slot0, abase, bbase, aoffs, boffs, wave);
+    if (ntiles > 0) dma_issue<4>(slot0, abase, bbase, aoffs, boffs, wave);
     for (int i = tid; i < BM; i += NT) roff[i] = m0 + i < p.M ? remap(p.rmap, m0 + i) : int64_t(-1);
     for (int i = tid; i < BN; i += NT) coff[i] = n0 + i < p.N ? remap(p.cmap, n0 + i) : int64_t(-1);
 
@@ -1041,11 +1060,11 @@ __global__ __launch_bounds__(512) void gemm_dma_mn_kernel(GemmParams p) {
 
     for (int kt = 0; kt < ntiles; kt += 2) {
         dma_stage_barrier();
-        if (kt + 1 < ntiles) dma_issue(slot1, abase + (kt + 1) * astep, bbase + (kt + 1) * bstep, aoffs, boffs, wave);
+        if (kt + 1 < ntiles) dma_issue<4>(slot1, abase + (kt + 1) * astep, bbase + (kt + 1) * bstep, aoffs, boffs, wave);
         dma_mma<true, TM, TN>(acc, slot0, aaddr, baddr, kpos);
         if (kt + 1 >= ntiles) break;
         dma_stage_barrier();
-        if (kt + 2 < ntiles) dma_issue(slot0, abase + (kt + 2) * astep, bbase + (kt + 2) * bstep, aoffs, boffs, wave);
+        if (kt + 2 < ntiles) dma_issue<4>(slot0, abase + (kt + 2) * astep, bbase + (kt + 2) * bstep, aoffs, boffs, wave);
         dma_mma<true, TM, TN>(acc, slot1, aaddr, baddr, kpos);
     }
     __syncthreads();   // every wave is done with the operand slots
@@ -1103,20 +1122,21 @@ __global__ __launch_bounds__(512) void gemm_dma_mn_kernel(GemmParams p) {
     }
 }
 
-template <bool OB, bool MN>
+template <bool OB, bool MN, int BN = 256>
 int launch_dma(const GemmArgs &g, const GemmParams &p, void *stream) {
+    static_assert(!MN || BN == 256, "the dW tile is 256 wide");
     constexpr size_t lds = MN ? 0 : dma_main_lds<OB>() + size_t(512) * sizeof(int64_t);
     static_assert(lds <= kLdsPerCu, "LDS of one workgroup");
-    auto kern = MN ? gemm_dma_mn_kernel<OB> : gemm_dma_kernel<OB>;
+    auto kern = MN ? gemm_dma_mn_kernel<OB> : gemm_dma_kernel<OB, BN>;
     if (!MN && !launch_check_mode()) {
         static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
         if (set) return set;
     }
     GemmParams q = p;
-    const dim3 grid = tile_grid(g, 256, 256, q);
+    const dim3 grid = tile_grid(g, 256, BN, q);
     if (!grid.x) return int(hipErrorInvalidConfiguration);
-    q.gw = choose_gw(g, 256, 256, g.splits);
+    q.gw = choose_gw(g, 256, BN, g.splits);
     COMERA_LAUNCH_NAMED("gemm_dma_kernel", kern, grid, dim3(512), lds, hipStream_t(stream), q);
     return launch_status();
 }
@@ -1169,8 +1189,10 @@ enum FastId {
     // per stage would not fit the registers of a wave beside its
     // accumulators)
     F256x256_64w8,
-    // bf16, K-contiguous operands, straight-to-LDS loads (gemm_dma_kernel)
-    F256x256_dma
+    // bf16, straight-to-LDS loads (gemm_dma_kernel, gemm_dma_mn_kernel)
+    F256x256_dma,
+    // bf16, K-contiguous operands, straight-to-LDS loads, 256 x 192 tiles
+    F256x192_dma
 };
 
 template <typename T, bool AK, bool BK, bool OB, int BM, int BN, int WM, int WN, int KTB, int NT = 256, int PF = 1>
@@ -1238,7 +1260,17 @@ int pick_fast(const GemmArgs &g, int splits) {
     // tiles fill more CUs), M/N-contiguous ones (dW) from an eighth: their
     // transposing loads are what the DMA form saves (measured on the layer
     // shapes)
-    if (g.dtype == COMERA_BF16 && g.a_kc && g.b_kc && splits == 1 && t256 >= 128) return F256x256_dma;
+    if (g.dtype == COMERA_BF16 && g.a_kc && g.b_kc && splits == 1 && t256 >= 128) {
+        // 256 x 192 tiles where 256 x 256 ones leave CUs idle in the last
+        // round: rounds of 256 tiles, the narrower tile doing 3/4 of the
+        // work (and measured about 10 % slower per flop); e.g. N = 768
+        // fills the chip once with 192-wide tiles (16384 x 768 x 768:
+        // 26.8 -> 23.9 us), not with 256-wide ones
+        const int64_t t192 = ceil_div(g.M, 256) * ceil_div(g.N, 192);
+        const int64_t r256 = ceil_div(t256, 256), r192 = ceil_div(t192, 256);
+        if (double(r192) * 0.75 * 1.1 < double(r256)) return F256x192_dma;
+        return F256x256_dma;
+    }
     if (g.dtype == COMERA_BF16 && !g.a_kc && !g.b_kc && t256 >= 32) return F256x256_dma;
     if ((g.dtype == COMERA_BF16 || g.dtype == kDtypeFp8) && g.a_kc == g.b_kc && t256 >= (g.a_kc ? 512 : 128))
         return F256x256_128w8;
@@ -1385,6 +1417,10 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     if (g.a_kc == AK && g.b_kc == BK && g.out_bf16 == OB) {                                \
         if (fast >= 0) return launch_fast<T, AK, BK, OB>(gg, pf, fast, stream);           \
         return launch_t<T, AK, BK, OB>(gg, p, tile, stream);                               \
+    }
+    if (fast == F256x192_dma) {
+        if (g.dtype != COMERA_BF16 || !g.a_kc || !g.b_kc) return int(hipErrorInvalidValue);
+        return g.out_bf16 ? launch_dma<true, false, 192>(gg, pf, stream) : launch_dma<false, false, 192>(gg, pf, stream);
     }
     if (fast == F256x256_dma) {
         if (g.dtype != COMERA_BF16 || g.a_kc != g.b_kc) return int(hipErrorInvalidValue);
