@@ -31,7 +31,7 @@ namespace {
 constexpr int kMaxEs = 16;          // columns of the last core per register pass
 constexpr int kBlk = 1024;          // keys per radix workgroup (256 threads x 4)
 constexpr int kSub = kBlk / 256;
-constexpr int kGlVp = 8;            // prefixes per dG_last workgroup (= partial)
+constexpr int kGlVp = 4;            // prefixes per dG_last workgroup (= partial)
 constexpr size_t kEmbLds = 64 * 1024;
 
 __device__ __forceinline__ uint64_t lanemask_lt() {
