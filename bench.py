@@ -31,6 +31,7 @@ PEAK = {"f32": 157.3e12, "bf16": 2.5e15}
 HBM_PEAK = 8.0e12
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2405_14377_amd", "csrc", f) for f in ("gemm.hip", "api_ttm.hip")]
+EMBED_SRCS = [os.path.join(ROOT, "paper_2405_14377_amd", "csrc", f) for f in ("embed_kernels.hip", "api_embed.hip")]
 HEADLINE_WID = 4              # the 1024 <-> 4096 d4 r64 pair, 65536 tokens, bf16
 COPY_BYTES = 1 << 28          # plain device copy used to scale the HBM byte counters
 
@@ -147,23 +148,28 @@ def dense_step_fn(sh, X, dY):
 
 
 # ------------------------------------------------------------------ roofline
-def source_sha():
+def source_sha(files=None):
     h = hashlib.sha256()
-    for f in KERNEL_SRCS:
+    for f in (KERNEL_SRCS if files is None else files):
         h.update(open(f, "rb").read())
     return h.hexdigest()[:16]
 
 
 def traffic_from_profile(kernel_tag, act):
     """HBM bytes per launch from a committed counter summary, if it was taken
-    on the current kernel source; else None."""
+    on the current kernel sources (the GEMM sources, or the files the summary
+    lists); else None."""
     path = os.path.join(PROFILES, f"traffic_{kernel_tag}_{act}.md")
     if not os.path.exists(path):
         return None
     txt = open(path).read()
     m_sha = re.search(r"source_sha256_16:\s*([0-9a-f]+)", txt)
     m_b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
-    if not m_sha or not m_b or m_sha.group(1) != source_sha():
+    m_src = re.search(r"^sources:\s*(.+)$", txt, re.M)
+    files = [os.path.join(ROOT, f) for f in m_src.group(1).split()] if m_src else None
+    if files and not all(os.path.exists(f) for f in files):
+        return None
+    if not m_sha or not m_b or m_sha.group(1) != source_sha(files):
         return None
     return float(m_b.group(1))
 
@@ -231,7 +237,7 @@ def kernel_stats_summary(prof_dir, out_path, command, top=25):
     open(out_path, "w").write("\n".join(lines) + "\n")
 
 
-def traffic_summary(fetch_dir, write_dir, kernel, grid, tag, act, out_path, commands):
+def traffic_summary(fetch_dir, write_dir, kernel, grid, tag, act, out_path, commands, sources=None):
     """HBM bytes per launch of one kernel from two counter passes (FETCH_SIZE,
     WRITE_SIZE, KiB per dispatch), each scaled by what the same counter reads
     for a plain device copy of COPY_BYTES."""
@@ -250,8 +256,9 @@ def traffic_summary(fetch_dir, write_dir, kernel, grid, tag, act, out_path, comm
     hbm = kf * 1024 * sf + kw * 1024 * sw
     lines = ["# HBM traffic per launch", "",
              f"kernel: `{kernel}`" + (f" (grid size {grid} work-items)" if grid else ""),
-             f"tag: {tag} ({act})",
-             f"source_sha256_16: {source_sha()}",
+             f"tag: {tag} ({act})"] + \
+            ([f"sources: {' '.join(os.path.relpath(f, ROOT) for f in sources)}"] if sources else []) + [
+             f"source_sha256_16: {source_sha(sources)}",
              f"fetch_kib_per_dispatch: {kf:.1f} (mean of {nf})",
              f"write_kib_per_dispatch: {kw:.1f} (mean of {nw})",
              f"copy_{COPY_BYTES}_bytes_fetch_kib: {cf:.1f} -> scale {sf:.4f}",
@@ -416,8 +423,10 @@ def other_workloads(steps, warmup):
                  "dense_ms_per_step": round(dms, 4), "speedup_vs_dense": round(dms / ms, 3),
                  "graph": graph_entry(gms, gerr, dgms, dgerr)}
         if wid == 2:
-            roofs = [kernel_roofline(l, max(2, k // 2), act)[1] for l in layers]
-            entry["kernels_ms"] = [{t: round(v["avg_ms"], 4) for t, v in r.items()} for r in roofs]
+            rr = [kernel_roofline(l, max(2, k // 2), act, f"encoder layer {i}") for i, l in enumerate(layers)]
+            entry["kernels_ms"] = [{t: round(v["avg_ms"], 4) for t, v in r.items()} for _, r in rr]
+            # the step's dominant product (longest mean launch) and its roofline
+            entry["roofline"] = max((r for r, _ in rr), key=lambda r: r["avg_ms"])
         entry["orders"] = [l.plan.order_info(l.plan.chosen)["desc"] for l in layers]
         res[f"w{wid}_{act}"] = entry
         del layers, dense
@@ -458,12 +467,19 @@ def other_workloads(steps, warmup):
         dms, _ = time_loop(dense, steps, warmup)
         gms, gerr = graph_loop(step, steps, warmup)
         byt = 2.0 * n * E * 4            # output write + dY read (algorithmic floor)
+        # the row kernel (the forward's dominant launch): HBM bytes per launch
+        # from its counter summary (mean over the Zipf and uniform runs)
+        Vp, Ep = int(np.prod(w.v[:-1])), int(np.prod(w.e[:-1]))
+        rows_tag = f"embed_rows_{V}x{E}_b{n}"
+        rows = {"hbm_bytes": traffic_from_profile(rows_tag, "f32"),
+                "algorithmic_bytes": float(n * E * 4 + Vp * Ep * w.r[-2] * 4),
+                "traffic_profile": f"profiles/traffic_{rows_tag}_f32.md"}
         res[f"w3_{dist}"] = {"workload": w.name, "dtype": "f32", "tokens": n, "ms_per_step": round(ms, 4),
                              "fwd_ms": round(fms, 4), "tokens_per_s": round(n / (ms * 1e-3), 1),
                              "gbps_floor_bytes": round(byt / (ms * 1e-3) / 1e9, 1),
                              "hbm_frac": round(byt / (ms * 1e-3) / HBM_PEAK, 4),
                              "dense_ms_per_step": round(dms, 4), "speedup_vs_dense": round(dms / ms, 3),
-                             "graph": graph_entry(gms, gerr, None, None)}
+                             "rows_kernel": rows, "graph": graph_entry(gms, gerr, None, None)}
     return res
 
 
@@ -614,6 +630,8 @@ def main():
     ap.add_argument("--traffic-summary", nargs=5, metavar=("FETCH_DIR", "WRITE_DIR", "KERNEL", "GRID", "TAG"),
                     help="write profiles/traffic_<TAG>_<dtype>.md from two counter runs (no GPU); GRID 0 = any")
     ap.add_argument("--commands", nargs="*", default=[], help="commands recorded in a summary")
+    ap.add_argument("--sources", nargs="*", default=None,
+                    help="source files (repository paths) a traffic summary is keyed to (default: the GEMM sources)")
     ap.add_argument("--fp8-only", action="store_true", help="only the mixed-precision (FP8) figures")
     ap.add_argument("--orders", type=int, nargs="*", default=None, metavar="WORKLOAD",
                     help="time every contraction order of these workloads (default 0 1 5) and exit")
@@ -623,8 +641,9 @@ def main():
         return
     if args.traffic_summary:
         fd, wd, kern, grid, tag = args.traffic_summary
+        srcs = [os.path.join(ROOT, f) for f in args.sources] if args.sources else None
         hbm = traffic_summary(fd, wd, kern, int(grid) or None, tag, args.dtype,
-                              os.path.join(PROFILES, f"traffic_{tag}_{args.dtype}.md"), args.commands)
+                              os.path.join(PROFILES, f"traffic_{tag}_{args.dtype}.md"), args.commands, srcs)
         print(f"hbm bytes per launch: {hbm:.4e}")
         return
     ws = int(os.environ.get("WORLD_SIZE", "1"))
