@@ -353,6 +353,44 @@ int build_dense(const comera_ttm_plan_s *p, const float *const *G, const float *
     dense_ptrs(p, ws, bd);
     CoreStrides st[kMaxCores];
     dense_strides(p, st);
+    if (p->d == 3 && (want & (kWantW | kWantWT))) {
+        Build3Args ba;
+        std::memset(&ba, 0, sizeof(ba));
+        int n[3], m[3];
+        for (int k = 0; k < 3; ++k) {
+            n[k] = int(p->s.n[k]);
+            m[k] = int(p->s.m[k]);
+        }
+        if (build3_tiles(n, m, int(p->rho[1]), int(p->rho[2]), ba.SX, ba.SY, ba.PX, ba.PY) &&
+            (!p->compacted || (p->s.r[1] <= 256 && p->s.r[2] <= 256))) {
+            const bool bf = p->s.act == COMERA_BF16 && !p->fp8;
+            for (int k = 0; k < 3; ++k) {
+                ba.G[k] = G[k];
+                ba.Gc[k] = bd.gc[k];
+                ba.st[k] = st[k];
+                ba.n[k] = n[k];
+                ba.m[k] = m[k];
+            }
+            ba.D[0] = D ? D[0] : nullptr;
+            ba.D[1] = D ? D[1] : nullptr;
+            ba.P2 = reinterpret_cast<float *>(at(ws, p->dense.p[2]));
+            bd.P[1] = bd.gc[0];
+            bd.P[2] = ba.P2;
+            bd.w = at(ws, p->dense.w);
+            bd.wt = at(ws, p->dense.wt);
+            ba.w = (want & kWantW) ? bd.w : nullptr;
+            ba.wt = (want & kWantWT) ? bd.wt : nullptr;
+            ba.act1 = p->act[1];
+            ba.act2 = p->act[2];
+            ba.r1 = int(p->s.r[1]);
+            ba.r2 = int(p->s.r[2]);
+            ba.A = int(p->rho[1]);
+            ba.C = int(p->rho[2]);
+            ba.compacted = p->compacted ? 1 : 0;
+            ba.out_bf16 = bf ? 1 : 0;
+            return note_hip(launch_build3(ba, stream), "W build (three cores)");
+        }
+    }
     if (int e = fold_cores(p, G, D, bd.gc, st, stream)) return e;
     return build_chain(p, ws, bd, want, stream);
 }

@@ -341,6 +341,33 @@ struct LChainArgs {
 bool lchain_supported(int A);
 int launch_lchain(const LChainArgs &a, void *stream);
 
+// Whole batch-free build of a three-core layer in one launch (build3.hip):
+// from the raw cores G_k [r_k][m_k][n_k][r_{k+1}] and the masks of bonds 1
+// and 2 (D[k] scales core k's right bond; null = ones), the folded copies
+// Gc[k] (placed by st[k]), the left chain P_2 [(x0 x1)][(y0 y1)][C] and W
+// [N_in][N_out] (w) and / or W^T [N_out][N_in] (wt).  A, C: compacted ranks
+// of bonds 1 and 2 (at most 64); r1, r2 full ranks; tiles of SX x SY middle
+// slices and PX x PY pairs from build3_tiles.
+struct Build3Args {
+    const float *G[3];
+    const float *D[2];
+    float *Gc[3];
+    CoreStrides st[3];
+    float *P2;
+    void *w, *wt;
+    BondBits act1, act2;
+    int r1, r2;
+    int A, C;
+    int n[3], m[3];
+    int compacted;
+    int out_bf16;
+    int SX, SY, PX, PY;
+    uint8_t map1[64], map2[64];   // compacted -> full entry of bonds 1 and 2 (set by launch_build3)
+    int vec_w, vec_t;             // set by launch_build3
+};
+bool build3_tiles(const int *n, const int *m, int A, int C, int &SX, int &SY, int &PX, int &PY);
+int launch_build3(const Build3Args &a, void *stream);
+
 
 // operand type code of FP8 (OCP E4M3) GEMM operands, beside COMERA_F32 / COMERA_BF16
 constexpr int kDtypeFp8 = 2;
