@@ -217,7 +217,7 @@ __global__ __launch_bounds__(kB3Threads) void build3_kernel(Build3Args a) {
     const int gq = tid & 255, gh = tid >> 8;
     const bool gin = gq < NC;
     float gv[KH];
-    {
+    if (gq < NC16) {    // whole waves past the last row skip the loads
         const float *G2 = a.G[2] + (gin ? gq : 0);
 #pragma unroll
         for (int j = 0; j < KH; ++j) {
