@@ -1122,6 +1122,117 @@ __global__ __launch_bounds__(512) void gemm_dma_mn_kernel(GemmParams p) {
     }
 }
 
+// fp32 dW = X^T dY (operands M/N-contiguous) on the straight-to-LDS path:
+// 128 x 128 tiles of four waves (64 x 64 each, v_mfma_f32_32x32x2f32), K
+// stages of 32 k rows in two LDS slots of 32 KB (two workgroups per CU),
+// split over K by the grid (split z covers k in [z kchunk, (z + 1) kchunk)).
+// A k row of a tile is 128 m (512 bytes) loaded as 16-byte chunks, chunk c at
+// position c ^ (8 (k & 1)), so that the two k rows one MFMA reads (the two
+// lane halves) fall on different banks; lane (lr, lh) reads element m = lr of
+// k row 2 s + lh, no transposition needed for 4-byte elements.  Columns past
+// M / N are clamped (their results are never stored).  Measured against the
+// register-staged 128 x 128 fp32 tile: 197 against 210 us on 768 x 3072 x
+// 4096 (its register transposes are what this saves); the K-contiguous form
+// of the same kernel was slower than the register-staged tile (192 against
+// 181 us on 4096 x 3072 x 768) and is not kept.
+constexpr int kD32KT = 32;                  // k per stage
+constexpr int kD32Op = 128 * kD32KT * 4;    // one operand tile (16 KB)
+constexpr int kD32Stage = 2 * kD32Op;       // A and B of one stage
+
+__global__ __launch_bounds__(256) void gemm_dma32_kernel(GemmParams p) {
+    constexpr int BM = 128, BN = 128, WM = 64, WN = 64, TM = 2, TN = 2, NT = 256;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    int64_t *roff = reinterpret_cast<int64_t *>(smem + 2 * kD32Stage);
+    int64_t *coff = roff + BM;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const TileIdx ti = tile_of(p);
+    const int64_t m0 = ti.row * BM, n0 = ti.col * BN;
+    const int64_t k0 = ti.z * p.kchunk, k1 = min(p.K, k0 + p.kchunk);
+    const int ntiles = k1 > k0 ? int((k1 - k0) / kD32KT) : 0;
+    const char *abase = reinterpret_cast<const char *>(p.A);
+    const char *bbase = reinterpret_cast<const char *>(p.B);
+    // byte offsets of this thread's four chunks of A and of B in one stage
+    uint32_t aoffs[4], boffs[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int kr = (wave * 4 + j) * 2 + (lane >> 5);
+        const int c = (lane & 31) ^ (8 * (kr & 1));
+        const int64_t ga = min(m0 + 4 * c, p.M - 4), gb = min(n0 + 4 * c, p.N - 4);
+        aoffs[j] = uint32_t((kr * p.lda + ga) * 4);
+        boffs[j] = uint32_t((kr * p.ldb + gb) * 4);
+    }
+    abase += k0 * p.lda * 4;
+    bbase += k0 * p.ldb * 4;
+    const int64_t astep = int64_t(kD32KT) * p.lda * 4, bstep = int64_t(kD32KT) * p.ldb * 4;
+    auto issue = [&](char *st, int kt) {
+        char *sa = st + wave * 4 * 1024, *sb = st + kD32Op + wave * 4 * 1024;
+        const char *ga = abase + kt * astep, *gb = bbase + kt * bstep;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(ga + aoffs[j]),
+                                             (lds_void_t *)(sa + j * 1024), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(gb + boffs[j]),
+                                             (lds_void_t *)(sb + j * 1024), 16, 0, 0);
+        }
+    };
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    if (ntiles > 0) issue(smem, 0);
+    for (int i = tid; i < BM; i += NT) roff[i] = m0 + i < p.M ? remap(p.rmap, m0 + i) : int64_t(-1);
+    for (int i = tid; i < BN; i += NT) coff[i] = n0 + i < p.N ? remap(p.cmap, n0 + i) : int64_t(-1);
+
+    const int lr = lane & 31, lh = lane >> 5;
+    for (int kt = 0; kt < ntiles; ++kt) {
+        dma_stage_barrier();
+        if (kt + 1 < ntiles) issue(smem + ((kt + 1) & 1) * kD32Stage, kt + 1);
+        const char *st = smem + (kt & 1) * kD32Stage;
+        // k rows of 512 bytes; lane (lr, lh) reads m = lr of k row 2 s + lh
+        const float *fa = reinterpret_cast<const float *>(st), *fb = reinterpret_cast<const float *>(st + kD32Op);
+#pragma unroll
+        for (int s = 0; s < kD32KT / 2; ++s) {
+            const int kr = 2 * s + lh, sw = 32 * (kr & 1);
+            f32x2_t av, bv;   // (block 0, block 1)
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int ma = wm * WM + i * 32 + lr, nb = wn * WN + i * 32 + lr;
+                av[i] = fa[kr * 128 + (ma ^ sw)];
+                bv[i] = fb[kr * 128 + (nb ^ sw)];
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(bv[j], av[i], acc[i][j], 0, 0, 0);
+        }
+    }
+    epilogue<false, TM, TN, WM, WN, true>(p, acc, roff, coff, wm, wn, lr, lh);
+}
+
+int launch_dma32(const GemmArgs &g, const GemmParams &p, void *stream) {
+    constexpr size_t lds = size_t(2) * kD32Stage + size_t(256) * sizeof(int64_t);
+    static_assert(lds <= kLdsPerCu, "LDS of one workgroup");
+    auto kern = gemm_dma32_kernel;
+    if (!launch_check_mode()) {
+        static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
+        if (set) return set;
+    }
+    GemmParams q = p;
+    const dim3 grid = tile_grid(g, 128, 128, q);
+    if (!grid.x) return int(hipErrorInvalidConfiguration);
+    q.gw = choose_gw(g, 128, 128, g.splits);
+    COMERA_LAUNCH_NAMED("gemm_dma32_kernel", kern, grid, dim3(256), lds, hipStream_t(stream), q);
+    return launch_status();
+}
+
 template <bool OB, bool MN, int BN = 256>
 int launch_dma(const GemmArgs &g, const GemmParams &p, void *stream) {
     static_assert(!MN || BN == 256, "the dW tile is 256 wide");
@@ -1192,7 +1303,10 @@ enum FastId {
     // bf16, straight-to-LDS loads (gemm_dma_kernel, gemm_dma_mn_kernel)
     F256x256_dma,
     // bf16, K-contiguous operands, straight-to-LDS loads, 256 x 192 tiles
-    F256x192_dma
+    F256x192_dma,
+    // fp32, M/N-contiguous operands, straight-to-LDS loads (gemm_dma32_kernel),
+    // 128 x 128 tiles
+    F128x128_dma32
 };
 
 template <typename T, bool AK, bool BK, bool OB, int BM, int BN, int WM, int WN, int KTB, int NT = 256, int PF = 1>
@@ -1283,6 +1397,7 @@ int pick_fast(const GemmArgs &g, int splits) {
         return -1;
     }
     if (!g.a_kc && !g.b_kc) {
+        if (g.dtype == COMERA_F32 && t128 >= 240) return F128x128_dma32;
         if (ceil_div(g.M, 256) * ceil_div(g.N, 128) * splits >= 480) return F256x128_64;
         return t128 >= 240 ? F128x128_64 : -1;
     }
@@ -1395,16 +1510,27 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     // fewer tiles or none; an empty split writes zeros)
     int fast = g.fast >= 0 ? g.fast : (g.fast == -1 && g.tile < 0 ? pick_fast(gg, gg.splits) : -1);
     GemmParams pf = p;
+    // the fp32 straight-to-LDS tile writes fp32 results of M/N-contiguous
+    // operands only (otherwise: the register-staged tile)
+    if (fast == F128x128_dma32 && (g.out_bf16 || g.a_kc || g.b_kc)) fast = F128x128_64;
+    if (fast == F128x128_dma32 && (g.dtype != COMERA_F32 || g.oscale)) fast = -1;
     if (fast >= 0) {
         const int ktb = (fast == F128x128_64 || fast == F256x128_64 || fast == F256x256_64w8) ? 64 : 128;
-        if (fast >= F256x256_128w8 && g.dtype == COMERA_F32) fast = -1;
+        if (fast >= F256x256_128w8 && fast != F128x128_dma32 && g.dtype == COMERA_F32) fast = -1;
 
         const int64_t kt = ktb / esz;
         pf.kchunk = ceil_div(p.kchunk, kt) * kt;
         if (!fast_ok(gg, pf.kchunk, ktb)) {
             // a K that is a multiple of the 64-byte K row but not of the
             // 128-byte one keeps a fast 128 x 128 tile on 64-byte rows
+            const bool was32 = fast == F128x128_dma32;
             fast = -1;
+            // fp32: the register-staged 128 x 128 tile on 64-byte rows
+            if (was32 && fast_ok_k(gg, p.kchunk, 64)) {
+                fast = F128x128_64;
+                pf.kchunk = ceil_div(p.kchunk, 16) * 16;
+                if (!fast_ok(gg, pf.kchunk, 64)) fast = -1;
+            }
             if (ktb == 128 && g.dtype != COMERA_F32 && (fast_ok_k(gg, p.kchunk, 64))) {
                 fast = F128x128_64;
                 pf.kchunk = ceil_div(p.kchunk, 64 / esz) * (64 / esz);
@@ -1418,6 +1544,7 @@ int launch_gemm(const GemmArgs &g, void *stream) {
         if (fast >= 0) return launch_fast<T, AK, BK, OB>(gg, pf, fast, stream);           \
         return launch_t<T, AK, BK, OB>(gg, p, tile, stream);                               \
     }
+    if (fast == F128x128_dma32) return launch_dma32(gg, pf, stream);
     if (fast == F256x192_dma) {
         if (g.dtype != COMERA_BF16 || !g.a_kc || !g.b_kc) return int(hipErrorInvalidValue);
         return g.out_bf16 ? launch_dma<true, false, 192>(gg, pf, stream) : launch_dma<false, false, 192>(gg, pf, stream);
