@@ -828,11 +828,10 @@ constexpr size_t dma_main_lds() {
 // tile.  KC: row 8 (4 w + j) + l / 8, position l % 8.  MN: k row
 // 2 (4 w + j) + l / 32, position l % 32.  Rows / columns past the operand
 // are clamped (their results are never stored).
-template <bool MN, int IPB = 4>
+template <bool MN, int IPB = 4, int ESZ = 2>
 __device__ __forceinline__ void dma_offsets(const GemmParams &p, int64_t m0, int64_t n0, int wave, int lane,
                                             uint32_t (&aoffs)[4], uint32_t (&boffs)[IPB]) {
-    constexpr int ESZ = int(sizeof(uint16_t));
-    static_assert(!MN || IPB == 4, "the dW tile is 256 wide");
+    static_assert(!MN || (IPB == 4 && ESZ == 2), "the dW tile is 256 wide, bf16");
     if constexpr (!MN) {
         // B tiles of 64 IPB rows (256 or 192): IPB instructions per wave
 #pragma unroll
@@ -840,7 +839,7 @@ __device__ __forceinline__ void dma_offsets(const GemmParams &p, int64_t m0, int
             const int row = (wave * IPB + j) * 8 + (lane >> 3);
             const int c = (lane & 7) ^ ((row >> 1) & 7);
             const int64_t gb = min(n0 + row, p.N - 1);
-            boffs[j] = uint32_t((gb * p.ldb + c * 8) * ESZ);
+            boffs[j] = uint32_t(gb * p.ldb * ESZ + c * 16);
         }
     }
 #pragma unroll
@@ -849,7 +848,7 @@ __device__ __forceinline__ void dma_offsets(const GemmParams &p, int64_t m0, int
             const int row = (wave * 4 + j) * 8 + (lane >> 3);
             const int c = (lane & 7) ^ ((row >> 1) & 7);
             const int64_t ga = min(m0 + row, p.M - 1);
-            aoffs[j] = uint32_t((ga * p.lda + c * 8) * ESZ);
+            aoffs[j] = uint32_t(ga * p.lda * ESZ + c * 16);
         } else {
             const int kr = (wave * 4 + j) * 2 + (lane >> 5);
             const int c = (lane & 31) ^ (4 * (kr & 3));
@@ -878,9 +877,48 @@ __device__ __forceinline__ void dma_issue(char *st, const char *ga, const char *
 // acc += the products of one stage in LDS slot st.  KC: lane (lr, lh) of k
 // step ks takes logical chunk 2 ks + lh of its row (kpos).  MN: per 32-row
 // block, two transposed 8-byte reads (k rows 16 ks + 8 lh + j / 4 and + 4).
-template <bool MN, int TM, int TN>
+template <bool MN, int TM, int TN, bool FP8 = false>
 __device__ __forceinline__ void dma_mma(f32x16 (&acc)[TM][TN], const char *st, const uint32_t (&aaddr)[TM],
                                         const uint32_t (&baddr)[TN], const uint32_t (&kpos)[4]) {
+    if constexpr (FP8) {
+        // FP8 E4M3 (KC, 128 k per 128-byte row): k step ks of 64 takes
+        // chunks 4 ks + lh and 4 ks + 2 + lh of the lane's row (positions
+        // kpos[2 ks], kpos[2 ks + 1]), the k slots of the register-staged FP8
+        // tile; unit block scales (127 = 2^0), the tensor scales applied in
+        // the epilogue
+        auto read8 = [&](uint32_t addr, int ks) -> i32x8 {
+            const u32x4 lo = *reinterpret_cast<const u32x4 *>(st + addr + kpos[2 * ks]);
+            const u32x4 hi = *reinterpret_cast<const u32x4 *>(st + addr + kpos[2 * ks + 1]);
+            return __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        };
+        __builtin_amdgcn_s_setprio(3);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            i32x8 av[TM], bv[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) av[i] = read8(aaddr[i], ks);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) bv[j] = read8(baddr[j], ks);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bv[j], av[i], acc[i][j], 0, 0, 0, 127,
+                                                                                0, 127);
+        }
+        // the operands of step 1 are read between the products of step 0
+        constexpr int NR = TM + TN, NM = TM * TN;
+        __builtin_amdgcn_sched_group_barrier(0x100, NR * 2, 0);
+#pragma unroll
+        for (int t = 0; t < NR; ++t) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+        __builtin_amdgcn_s_setprio(0);
+        return;
+    }
     constexpr int RPS = MN ? 2 : 1;   // LDS reads per operand block and k step
     auto read_op = [&](uint32_t addr, int ks) -> bf16x8 {
         if constexpr (!MN) {
@@ -934,14 +972,15 @@ __device__ __forceinline__ void dma_stage_barrier() {
 }
 
 // BN = 256: waves of 128 x 64; BN = 192 (products whose 256 x 256 tiles
-// would leave CUs idle, e.g. N = 768): waves of 64 x 96, B tiles of 192 rows
-template <bool OUT_BF16, int BN = 256>
+// would leave CUs idle, e.g. N = 768): waves of 64 x 96, B tiles of 192 rows.
+// FP8: E4M3 codes, the same 128-byte K rows (128 k per stage).
+template <bool OUT_BF16, int BN = 256, bool FP8 = false>
 __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     static_assert(BN == 256 || BN == 192, "tile width");
-    constexpr int BM = 256, WM = BN == 256 ? 128 : 64, WN = BN == 256 ? 64 : 96, NT = 512, KT = kDmaKT;
+    constexpr int ESZ = FP8 ? 1 : 2;
+    constexpr int BM = 256, WM = BN == 256 ? 128 : 64, WN = BN == 256 ? 64 : 96, NT = 512, KT = 128 / ESZ;
     constexpr int IPB = BN / 64;   // B-operand load instructions per wave
     constexpr int TM = WM / 32, TN = WN / 32, WAVES_N = BN / WN;
-    constexpr int ESZ = int(sizeof(uint16_t));
     extern __shared__ __attribute__((aligned(16))) char smem[];
     int64_t *roff = reinterpret_cast<int64_t *>(smem + dma_main_lds<OUT_BF16>());
     int64_t *coff = roff + BM;
@@ -949,12 +988,14 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     const TileIdx ti = tile_of(p);
     const int64_t m0 = ti.row * BM, n0 = ti.col * BN;
-    const int ntiles = int(p.K / KT);
-    const char *abase = reinterpret_cast<const char *>(p.A);
-    const char *bbase = reinterpret_cast<const char *>(p.B);
+    // split z covers k in [z kchunk, (z + 1) kchunk) (whole stages)
+    const int64_t k0 = ti.z * p.kchunk, k1 = min(p.K, k0 + p.kchunk);
+    const int ntiles = k1 > k0 ? int((k1 - k0) / KT) : 0;
+    const char *abase = reinterpret_cast<const char *>(p.A) + k0 * ESZ;
+    const char *bbase = reinterpret_cast<const char *>(p.B) + k0 * ESZ;
     constexpr int64_t kstep = KT * ESZ;
     uint32_t aoffs[4], boffs[IPB];
-    dma_offsets<false, IPB>(p, m0, n0, wave, lane, aoffs, boffs);
+    dma_offsets<false, IPB, ESZ>(p, m0, n0, wave, lane, aoffs, boffs);
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -984,7 +1025,7 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
         if (kt + 1 < ntiles)
             dma_issue<IPB>(smem + ((kt + 1) & 1) * kDmaStageB, abase + (kt + 1) * kstep, bbase + (kt + 1) * kstep, aoffs,
                       boffs, wave);
-        dma_mma<false, TM, TN>(acc, smem + (kt & 1) * kDmaStageB, aaddr, baddr, kpos);
+        dma_mma<false, TM, TN, FP8>(acc, smem + (kt & 1) * kDmaStageB, aaddr, baddr, kpos);
     }
     __syncthreads();   // every wave is done with the operand slots
     if (p.oscale) {
@@ -1233,12 +1274,12 @@ int launch_dma32(const GemmArgs &g, const GemmParams &p, void *stream) {
     return launch_status();
 }
 
-template <bool OB, bool MN, int BN = 256>
+template <bool OB, bool MN, int BN = 256, bool FP8 = false>
 int launch_dma(const GemmArgs &g, const GemmParams &p, void *stream) {
-    static_assert(!MN || BN == 256, "the dW tile is 256 wide");
+    static_assert(!MN || (BN == 256 && !FP8), "the dW tile is 256 wide, bf16");
     constexpr size_t lds = MN ? 0 : dma_main_lds<OB>() + size_t(512) * sizeof(int64_t);
     static_assert(lds <= kLdsPerCu, "LDS of one workgroup");
-    auto kern = MN ? gemm_dma_mn_kernel<OB> : gemm_dma_kernel<OB, BN>;
+    auto kern = MN ? gemm_dma_mn_kernel<OB> : gemm_dma_kernel<OB, BN, FP8>;
     if (!MN && !launch_check_mode()) {
         static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
@@ -1368,6 +1409,9 @@ int pick_fast(const GemmArgs &g, int splits) {
     // bf16: 256 x 256 tiles of eight waves once they give two or more
     // workgroups per CU (transposed operands, split over K: half a wave of
     // workgroups is enough)
+    // FP8 codes (always K-contiguous) on the straight-to-LDS tile from half a
+    // wave of tiles
+    if (g.dtype == kDtypeFp8 && g.a_kc && g.b_kc && t256 >= 128) return F256x256_dma;
     if (g.dtype == kDtypeFp8 && t256 >= 512) return F256x256_64w8;
     // bf16 256 x 256 tiles with straight-to-LDS operand loads: K-contiguous
     // unsplit products from half a wave of tiles (below that the smaller
@@ -1548,6 +1592,11 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     if (fast == F256x192_dma) {
         if (g.dtype != COMERA_BF16 || !g.a_kc || !g.b_kc) return int(hipErrorInvalidValue);
         return g.out_bf16 ? launch_dma<true, false, 192>(gg, pf, stream) : launch_dma<false, false, 192>(gg, pf, stream);
+    }
+    if (fast == F256x256_dma && g.dtype == kDtypeFp8) {
+        if (!g.a_kc || !g.b_kc) return int(hipErrorInvalidValue);
+        return g.out_bf16 ? launch_dma<true, false, 256, true>(gg, pf, stream)
+                          : launch_dma<false, false, 256, true>(gg, pf, stream);
     }
     if (fast == F256x256_dma) {
         if (g.dtype != COMERA_BF16 || g.a_kc != g.b_kc) return int(hipErrorInvalidValue);
