@@ -8,15 +8,18 @@
 // as W [N_in][N_out] and / or W^T [N_out][N_in], fp32 or bf16 (x_k runs over
 // the input factor n_k, y_k over the output factor m_k).
 //
-// A workgroup owns SX x SY slices (x1, y1) of the middle core and PX x PY
-// pairs (x0, y0) of the first: R = SX SY PX PY <= 64 rows (slice, pair) of
-// P_2.  Each thread takes (slice, c) items: it loads the slice's column c of
-// G~_1 once (rank A values, straight from the raw core through the bond
-// maps, the mask applied) and contracts it with the PP pair rows of G~_0
-// staged in LDS, so the middle core, the largest of the three, is read once
-// per pair block and never staged.  The R x C rows of P_2 then meet the last
-// core (C x n2 m2, staged transposed) on v_mfma_f32_16x16x4f32, one 16-row
-// block per wave; the tile goes through LDS and out as runs of SY m2
+// A workgroup of eight waves owns SX x SY slices (x1, y1) of the middle core
+// and PX x PY pairs (x0, y0) of the first: R = SX SY PX PY <= 64 rows
+// (slice, pair) of P_2.  Every global load of the workgroup is issued before
+// any is used (the bond maps come as kernel arguments for uniform indices
+// and from the active bits per lane, so no address waits on LDS): the last
+// core, the pair rows of G~_0, and per thread one (slice, c) item, the
+// slice's column c of G~_1 (rank A values straight from the raw core, the
+// mask applied) that it contracts with the PP pair rows, so the middle core,
+// the largest of the three, is read once per pair block and never staged.
+// The R x C rows of P_2 then meet the last core (C x n2 m2, staged
+// transposed) on v_mfma_f32_16x16x4f32, each 16-row block split over two
+// waves by columns; the tile goes through LDS and out as runs of SY m2
 // consecutive entries of W rows and SX n2 of W^T rows, four entries per
 // store where the factors allow it.  Tiles divide the factors exactly.
 //
