@@ -20,7 +20,8 @@ def test_launch_sizing_over_degenerate_shapes():
     assert not out["bad_status"], out["bad_status"]
     assert not out["bad_launches"], out["bad_launches"]
     assert out["calls"] > 10000 and out["launches"] > out["calls"]
-    for k in ("gemm_fast_kernel", "gemm_kernel", "wtile_kernel", "fold_kernel", "build3_kernel", "gemm_dma32_kernel", "expand_kernel",
+    for k in ("gemm_fast_kernel", "gemm_kernel", "wtile_kernel", "fold_kernel", "build3_kernel", "gemm_dma32_kernel", "gemm_dma_pers_kernel",
+              "expand_kernel",
               "radix_hist_kernel",
               "embed_segsum_kernel", "quant_vec_kernel<8>", "reg_core_kernel"):
         assert k in out["kernels"], k
