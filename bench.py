@@ -237,25 +237,41 @@ def kernel_stats_summary(prof_dir, out_path, command, top=25):
     open(out_path, "w").write("\n".join(lines) + "\n")
 
 
-def traffic_summary(fetch_dir, write_dir, kernel, grid, tag, act, out_path, commands, sources=None):
+def traffic_summary(fetch_dir, write_dir, kernel, grid, tag, act, out_path, commands, sources=None, out_bytes=None):
     """HBM bytes per launch of one kernel from two counter passes (FETCH_SIZE,
     WRITE_SIZE, KiB per dispatch), each scaled by what the same counter reads
-    for a plain device copy of COPY_BYTES."""
-    def per_dispatch(d, counter):
+    for a plain device copy of COPY_BYTES.  out_bytes: products that share
+    one kernel and grid are told apart by their output size, the launches
+    whose scaled write counter lies within 2 % of it; the fetch counter is
+    read for the same dispatch ids (the two passes run one deterministic
+    launch sequence)."""
+    def rows_of(d, counter):
         rows = [r for r in _read_csv(_find(d, "counter_collection.csv")) if r["Counter_Name"] == counter]
-        k = [float(r["Counter_Value"]) for r in rows
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        k = [(int(r["Dispatch_Id"]), float(r["Counter_Value"])) for r in rows
              if kernel in r["Kernel_Name"] and (grid is None or int(r["Grid_Size"]) == grid)]
         c = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
         if not k or not c:
             raise RuntimeError(f"{counter}: {len(k)} kernel dispatches, {len(c)} copy dispatches")
-        return sum(k) / len(k), len(k), max(c)
-    kf, nf, cf = per_dispatch(fetch_dir, "FETCH_SIZE")
-    kw, nw, cw = per_dispatch(write_dir, "WRITE_SIZE")
+        return k, max(c)
+    kfr, cf = rows_of(fetch_dir, "FETCH_SIZE")
+    kwr, cw = rows_of(write_dir, "WRITE_SIZE")
+    if out_bytes:
+        if [i for i, _ in kfr] != [i for i, _ in kwr]:
+            raise RuntimeError("the two counter passes dispatched the kernel under different ids")
+        keep = {i for i, v in kwr if abs(v * 1024 * (COPY_BYTES / 1024.0 / cw) - out_bytes) <= 0.02 * out_bytes}
+        kfr = [(i, v) for i, v in kfr if i in keep]
+        kwr = [(i, v) for i, v in kwr if i in keep]
+        if not kwr:
+            raise RuntimeError(f"no dispatch writes {out_bytes} bytes")
+    kf, nf = sum(v for _, v in kfr) / len(kfr), len(kfr)
+    kw, nw = sum(v for _, v in kwr) / len(kwr), len(kwr)
     sf = COPY_BYTES / 1024.0 / cf
     sw = COPY_BYTES / 1024.0 / cw
     hbm = kf * 1024 * sf + kw * 1024 * sw
     lines = ["# HBM traffic per launch", "",
-             f"kernel: `{kernel}`" + (f" (grid size {grid} work-items)" if grid else ""),
+             f"kernel: `{kernel}`" + (f" (grid size {grid} work-items)" if grid else "") +
+             (f", the dispatches that write {int(out_bytes)} bytes" if out_bytes else ""),
              f"tag: {tag} ({act})"] + \
             ([f"sources: {' '.join(os.path.relpath(f, ROOT) for f in sources)}"] if sources else []) + [
              f"source_sha256_16: {source_sha(sources)}",
@@ -632,6 +648,8 @@ def main():
     ap.add_argument("--commands", nargs="*", default=[], help="commands recorded in a summary")
     ap.add_argument("--sources", nargs="*", default=None,
                     help="source files (repository paths) a traffic summary is keyed to (default: the GEMM sources)")
+    ap.add_argument("--out-bytes", type=float, default=None,
+                    help="traffic summary: only the dispatches whose output (write counter) is this many bytes")
     ap.add_argument("--fp8-only", action="store_true", help="only the mixed-precision (FP8) figures")
     ap.add_argument("--orders", type=int, nargs="*", default=None, metavar="WORKLOAD",
                     help="time every contraction order of these workloads (default 0 1 5) and exit")
@@ -643,7 +661,8 @@ def main():
         fd, wd, kern, grid, tag = args.traffic_summary
         srcs = [os.path.join(ROOT, f) for f in args.sources] if args.sources else None
         hbm = traffic_summary(fd, wd, kern, int(grid) or None, tag, args.dtype,
-                              os.path.join(PROFILES, f"traffic_{tag}_{args.dtype}.md"), args.commands, srcs)
+                              os.path.join(PROFILES, f"traffic_{tag}_{args.dtype}.md"), args.commands, srcs,
+                              args.out_bytes)
         print(f"hbm bytes per launch: {hbm:.4e}")
         return
     ws = int(os.environ.get("WORLD_SIZE", "1"))
