@@ -1046,8 +1046,8 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
     epilogue<OUT_BF16, TM, TN, WM, WN, true>(p, acc, roff, coff, wm, wn, lr, lh);
 }
 
-// Persistent form of the K-contiguous bf16 product for plain row-major bf16
-// outputs C[m * ldc + n]: one workgroup per CU walks its tiles, the loads of
+// Persistent form of the K-contiguous bf16 (and FP8) product for plain
+// row-major bf16 outputs C[m * ldc + n]: one workgroup per CU walks its tiles, the loads of
 // a tile's first stage fly while the previous tile's last stage is
 // multiplied, and the finished tile leaves through per-wave staging in the
 // slot of that last stage (rows of 128 bytes, 16-byte chunks XOR-swizzled by
@@ -1056,9 +1056,14 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
 // stage over the first stages of the next tile, after that stage's loads.
 // Vector memory operations of a wave complete in issue order (gfx9 counts
 // loads and stores on one counter), so the wait for a stage's loads names
-// the number of stores issued after them and does not wait for those.
-constexpr int kPersHold = 4;   // 16-byte pieces per lane held into the next tile
-constexpr int kPersNow = 16 - kPersHold;   // stored at the end of the tile
+// the number of stores issued after them and does not wait for those.  The
+// FP8 form holds no pieces: its MFMA operands take the registers (it would
+// spill).
+constexpr int kPersHold = 4;   // bf16: 16-byte pieces per lane held into the next tile
+template <bool FP8>
+constexpr int pers_hold() {
+    return FP8 ? 0 : kPersHold;
+}
 
 __device__ __forceinline__ void pers_tile(const GemmParams &p, uint32_t id, int64_t &row, int64_t &col) {
     const uint32_t nx = p.tx, ny = p.ty;
@@ -1069,17 +1074,24 @@ __device__ __forceinline__ void pers_tile(const GemmParams &p, uint32_t id, int6
     col = g * gw + r % w;
 }
 
+// vmcnt(n) for the n used here (0, 1, NOW), no wait on the other counters,
+// then the workgroup barrier
+template <int NOW>
 __device__ __forceinline__ void pers_wait(int n) {
-    // vmcnt(n) for the n used here (0, 1, kPersHold), no wait on the others
+    static_assert(NOW > 1 && NOW < 64, "vmcnt range");
     if (n == 0) __builtin_amdgcn_s_waitcnt(0x0F70);
     else if (n == 1) __builtin_amdgcn_s_waitcnt(0x0F71);
-    else __builtin_amdgcn_s_waitcnt(0x0F70 | kPersNow);
+    else __builtin_amdgcn_s_waitcnt(0x0F70 | (NOW & 15) | ((NOW >> 4) << 14));
     asm volatile("s_barrier" ::: "memory");
 }
 
+// FP8: E4M3 codes in the same 128-byte K rows (128 k per stage), the
+// tensor scales applied before the bf16 conversion.
+template <bool FP8>
 __global__ __launch_bounds__(512) void gemm_dma_pers_kernel(GemmParams p) {
-    static_assert(kPersNow < 16 && kPersHold <= 8, "vmcnt immediates, pieces of the second half");
-    constexpr int ESZ = 2, BM = 256, BN = 256, WM = 128, WN = 64, KT = 64, IPB = 4;
+    constexpr int kPersHold = pers_hold<FP8>(), kPersNow = 16 - kPersHold;
+    static_assert(kPersHold <= 8, "held pieces come from the second half");
+    constexpr int ESZ = FP8 ? 1 : 2, OESZ = 2, BM = 256, BN = 256, WM = 128, WN = 64, KT = 128 / ESZ, IPB = 4;
     constexpr int TM = WM / 32, TN = WN / 32, WAVES_N = BN / WN;
     constexpr int64_t kstep = KT * ESZ;
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -1116,12 +1128,12 @@ __global__ __launch_bounds__(512) void gemm_dma_pers_kernel(GemmParams p) {
     int after0 = 0;           // stores issued after the current tile's stage-0 loads (0 or kPersNow)
     bool held = false;        // pieces of the previous tile waiting in hv
     bool held_full = false;   // ... all of them inside the output
-    u32x4 hv[kPersHold];
+    u32x4 hv[kPersHold > 0 ? kPersHold : 1];
     char *hbase = C0;         // the lane's first held piece
     int64_t hm = 0, hn = 0;   // its row and column
     // lane's piece q of a half block: row 8 q + lane / 8, columns 8 (lane % 8) .. + 7
     const int prow = lane >> 3, pcol = 8 * (lane & 7);
-    const int64_t rstep = 8 * ldc * ESZ;   // bytes between pieces q and q + 1
+    const int64_t rstep = 8 * ldc * OESZ;   // bytes between pieces q and q + 1
     for (;;) {
         f32x16 acc[TM][TN];
 #pragma unroll
@@ -1138,16 +1150,16 @@ __global__ __launch_bounds__(512) void gemm_dma_pers_kernel(GemmParams p) {
         // the first stages store the held pieces, one per stage after its loads
 #pragma unroll
         for (int kt = 0; kt < kPersHold; ++kt) {
-            pers_wait(kt == 0 ? after0 : hone);
+            pers_wait<kPersNow>(kt == 0 ? after0 : hone);
             const int sl = (s0 + kt) & 1;
             dma_issue<IPB>(smem + (sl ^ 1) * kDmaStageB, A0 + (kt + 1) * kstep, B0 + (kt + 1) * kstep, aoffs, boffs,
                            wave);
             if (held && (held_full || (hm + 8 * kt < p.M && hn < p.N)))
                 *reinterpret_cast<u32x4 *>(hbase + kt * rstep) = hv[kt];
-            dma_mma<false, TM, TN, false>(acc, smem + sl * kDmaStageB, aaddr, baddr, kpos);
+            dma_mma<false, TM, TN, FP8>(acc, smem + sl * kDmaStageB, aaddr, baddr, kpos);
         }
         for (int kt = kPersHold; kt < nst; ++kt) {
-            pers_wait(kt == kPersHold ? hone : 0);
+            pers_wait<kPersNow>(kt == 0 ? after0 : kt == kPersHold ? hone : 0);
             const int sl = (s0 + kt) & 1;
             if (kt + 1 < nst) {
                 dma_issue<IPB>(smem + (sl ^ 1) * kDmaStageB, A0 + (kt + 1) * kstep, B0 + (kt + 1) * kstep, aoffs,
@@ -1156,7 +1168,16 @@ __global__ __launch_bounds__(512) void gemm_dma_pers_kernel(GemmParams p) {
                 dma_offsets<false, IPB, ESZ>(p, nrow * BM, ncol * BN, wave, lane, aoffs, boffs);
                 dma_issue<IPB>(smem + (sl ^ 1) * kDmaStageB, A0, B0, aoffs, boffs, wave);
             }
-            dma_mma<false, TM, TN, false>(acc, smem + sl * kDmaStageB, aaddr, baddr, kpos);
+            dma_mma<false, TM, TN, FP8>(acc, smem + sl * kDmaStageB, aaddr, baddr, kpos);
+        }
+        if (FP8 && p.oscale) {
+            const float sc = *p.oscale;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) acc[i][j][v] *= sc;
         }
         // every wave is done with the last stage's slot: it becomes the
         // staging area (no wait for the next tile's loads in flight)
@@ -1166,7 +1187,7 @@ __global__ __launch_bounds__(512) void gemm_dma_pers_kernel(GemmParams p) {
         char *st = smem + ls * kDmaStageB + wave * 8192;
         const int64_t m0 = row * BM + wm * WM + prow, n0 = col * BN + wn * WN + pcol;
         const bool full = row * BM + BM <= p.M && col * BN + BN <= p.N;
-        char *cb = C0 + (m0 * ldc + n0) * ESZ;
+        char *cb = C0 + (m0 * ldc + n0) * OESZ;
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
 #pragma unroll
@@ -1474,20 +1495,25 @@ int launch_dma(const GemmArgs &g, const GemmParams &p, void *stream) {
 // multiple of 64 with more stages than held pieces, output bf16 C[m * ldc + n]
 // (16-byte pieces aligned), no output scale.
 bool pers_ok(const GemmArgs &g) {
-    if (g.dtype != COMERA_BF16 || !g.a_kc || !g.b_kc || !g.out_bf16 || g.splits != 1 || g.oscale) return false;
-    if (g.K % 64 != 0 || g.K / 64 <= kPersHold) return false;
+    const bool fp8 = g.dtype == kDtypeFp8;
+    if ((g.dtype != COMERA_BF16 && !fp8) || !g.a_kc || !g.b_kc || !g.out_bf16 || g.splits != 1) return false;
+    if (g.oscale && !fp8) return false;
+    const int64_t kt = fp8 ? 128 : 64;   // k per stage
+    if (g.K % kt != 0 || g.K / kt <= (fp8 ? 1 : kPersHold)) return false;
     if (g.rmap.nd != 1 || g.cmap.nd != 1 || g.cmap.stride[0] != 1) return false;
     if (g.N % 8 != 0 || g.rmap.stride[0] % 8 != 0 || reinterpret_cast<uintptr_t>(g.C) % 16 != 0) return false;
     if (reinterpret_cast<uintptr_t>(g.A) % 16 != 0 || reinterpret_cast<uintptr_t>(g.B) % 16 != 0) return false;
-    if (g.lda % 8 != 0 || g.ldb % 8 != 0) return false;
+    const int64_t e16 = fp8 ? 16 : 8;   // elements per 16-byte chunk
+    if (g.lda % e16 != 0 || g.ldb % e16 != 0) return false;
     return true;
 }
 
+template <bool FP8>
 int launch_dma_pers(const GemmArgs &g, const GemmParams &p, void *stream) {
     constexpr size_t lds = size_t(2) * kDmaStageB;
     static_assert(lds <= kLdsPerCu, "LDS of one workgroup");
     if (!launch_check_mode()) {
-        static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(gemm_dma_pers_kernel),
+        static const int set = int(hipFuncSetAttribute(reinterpret_cast<const void *>(gemm_dma_pers_kernel<FP8>),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)));
         if (set) return set;
     }
@@ -1497,7 +1523,8 @@ int launch_dma_pers(const GemmArgs &g, const GemmParams &p, void *stream) {
     if (tiles.x < 256) return int(hipErrorInvalidValue);   // whole rounds of 256 workgroups, 32 per XCD
     q.gw = choose_gw(g, 256, 256, 1);
     const unsigned grid = 256;
-    COMERA_LAUNCH_NAMED("gemm_dma_pers_kernel", gemm_dma_pers_kernel, dim3(grid), dim3(512), lds, hipStream_t(stream), q);
+    COMERA_LAUNCH_NAMED("gemm_dma_pers_kernel", gemm_dma_pers_kernel<FP8>, dim3(grid), dim3(512), lds,
+                        hipStream_t(stream), q);
     return launch_status();
 }
 
@@ -1556,8 +1583,8 @@ enum FastId {
     // fp32, M/N-contiguous operands, straight-to-LDS loads (gemm_dma32_kernel),
     // 128 x 128 tiles
     F128x128_dma32,
-    // bf16, K-contiguous operands, plain bf16 output: the persistent form of
-    // F256x256_dma (gemm_dma_pers_kernel)
+    // bf16 or FP8, K-contiguous operands, plain bf16 output: the persistent
+    // form of F256x256_dma (gemm_dma_pers_kernel)
     F256x256_pers
 };
 
@@ -1622,6 +1649,7 @@ int pick_fast(const GemmArgs &g, int splits) {
     // workgroups is enough)
     // FP8 codes (always K-contiguous) on the straight-to-LDS tile from half a
     // wave of tiles
+    if (g.dtype == kDtypeFp8 && g.a_kc && g.b_kc && t256 >= 256 && splits == 1 && pers_ok(g)) return F256x256_pers;
     if (g.dtype == kDtypeFp8 && g.a_kc && g.b_kc && t256 >= 128) return F256x256_dma;
     if (g.dtype == kDtypeFp8 && t256 >= 512) return F256x256_64w8;
     // bf16 256 x 256 tiles with straight-to-LDS operand loads: K-contiguous
@@ -1806,7 +1834,7 @@ int launch_gemm(const GemmArgs &g, void *stream) {
     }
     if (fast == F256x256_pers) {
         if (!pers_ok(gg)) return int(hipErrorInvalidValue);
-        return launch_dma_pers(gg, pf, stream);
+        return g.dtype == kDtypeFp8 ? launch_dma_pers<true>(gg, pf, stream) : launch_dma_pers<false>(gg, pf, stream);
     }
     if (fast == F128x128_dma32) return launch_dma32(gg, pf, stream);
     if (fast == F256x192_dma) {

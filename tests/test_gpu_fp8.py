@@ -227,11 +227,14 @@ def test_fp8_smaller_batch_and_empty():
     assert run.forward(to_dev(np.zeros((1, 768))), 0).shape[0] == 0
 
 
+@pytest.mark.parametrize("b", [8192, 8100])
 @pytest.mark.parametrize("act", ["f32", "bf16"])
-def test_integer_layer_large_tiles(act):
-    """8192 tokens through 1024 -> 4096: the forward and dX products are large
-    enough for the eight-wave 256 x 256 FP8 tiles; still bit-exact."""
-    n, m, r, b = (4, 8, 4, 8), (8, 8, 8, 8), (1, 16, 16, 16, 1), 8192
+def test_integer_layer_large_tiles(act, b):
+    """8192 and 8100 tokens through 1024 -> 4096: the forward and dX products
+    are large enough for the eight-wave 256 x 256 FP8 tiles (the bf16
+    forward, 512 tiles, on the persistent kernel; 8100 tokens leave a ragged
+    last row of tiles); still bit-exact."""
+    n, m, r = (4, 8, 4, 8), (8, 8, 8, 8), (1, 16, 16, 16, 1)
     rng = np.random.default_rng(15)
     cores = wl.integer_bond_diagonal_cores(rng, n, m, r)
     run = TTMRun(n, m, r, cores, None, b, act, force_order=0, reuse=True, fp8=True)
