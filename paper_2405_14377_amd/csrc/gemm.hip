@@ -1047,18 +1047,19 @@ __global__ __launch_bounds__(512) void gemm_dma_kernel(GemmParams p) {
 }
 
 // Persistent form of the K-contiguous bf16 (and FP8) product for plain
-// row-major bf16 outputs C[m * ldc + n]: one workgroup per CU walks its tiles, the loads of
-// a tile's first stage fly while the previous tile's last stage is
-// multiplied, and the finished tile leaves through per-wave staging in the
-// slot of that last stage (rows of 128 bytes, 16-byte chunks XOR-swizzled by
-// row): the upper half of each wave's 128 x 64 block is stored at once, the
-// lower half is held in registers and stored one 16-byte piece per lane per
-// stage over the first stages of the next tile, after that stage's loads.
-// Vector memory operations of a wave complete in issue order (gfx9 counts
-// loads and stores on one counter), so the wait for a stage's loads names
-// the number of stores issued after them and does not wait for those.  The
-// FP8 form holds no pieces: its MFMA operands take the registers (it would
-// spill).
+// row-major bf16 outputs C[m * ldc + n]: one workgroup per CU walks its
+// tiles, the loads of a tile's first stage fly while the previous tile's
+// last stage is multiplied, and the finished tile leaves through per-wave
+// staging in the slot of that last stage (8 KB per wave: 64 rows of 128
+// bytes, 16-byte chunks XOR-swizzled by row, written and read back in two
+// halves of the wave's 128 x 64 block).  Of the 16 sixteen-byte pieces a
+// lane then owns, 12 are stored at once and the last 4 are held in
+// registers and stored one per stage during the next tile's first four
+// stages, each after that stage's loads.  Vector memory operations of a
+// wave complete in issue order (gfx9 counts loads and stores on one
+// counter), so the wait for a stage's loads names the number of stores
+// issued after them and does not wait for those.  The FP8 form stores all
+// 16 at once: its MFMA operands take the registers (holding would spill).
 constexpr int kPersHold = 4;   // bf16: 16-byte pieces per lane held into the next tile
 template <bool FP8>
 constexpr int pers_hold() {
@@ -1491,9 +1492,10 @@ int launch_dma(const GemmArgs &g, const GemmParams &p, void *stream) {
     return launch_status();
 }
 
-// The persistent product: bf16 K-contiguous operands, one split, K a
-// multiple of 64 with more stages than held pieces, output bf16 C[m * ldc + n]
-// (16-byte pieces aligned), no output scale.
+// The persistent product: bf16 or FP8 K-contiguous operands, one split, K a
+// whole number of stages (64 k bf16, 128 FP8) with more stages than held
+// pieces, output bf16 C[m * ldc + n] (16-byte pieces aligned), an output
+// scale only for FP8.
 bool pers_ok(const GemmArgs &g) {
     const bool fp8 = g.dtype == kDtypeFp8;
     if ((g.dtype != COMERA_BF16 && !fp8) || !g.a_kc || !g.b_kc || !g.out_bf16 || g.splits != 1) return false;
