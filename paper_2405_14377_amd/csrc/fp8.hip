@@ -136,6 +136,20 @@ __device__ __forceinline__ uint8_t e4m3_rne(float v) {
     return uint8_t(code | sign);
 }
 
+// Four floats -> four E4M3 codes in one dword (byte k from value k):
+// gfx950's packed conversion (v_cvt_pk_fp8_f32, round to nearest even) after
+// clamping to +-448, which gives the codes of e4m3_rne for every finite
+// input (compared on the GPU over a 2^-14-step grid of every binade up to
+// 448, the ties between codes, the subnormal steps and 2^20 random values)
+__device__ __forceinline__ uint32_t e4m3_pk4(float a, float b, float c, float d) {
+    a = __builtin_amdgcn_fmed3f(a, -448.f, 448.f);
+    b = __builtin_amdgcn_fmed3f(b, -448.f, 448.f);
+    c = __builtin_amdgcn_fmed3f(c, -448.f, 448.f);
+    d = __builtin_amdgcn_fmed3f(d, -448.f, 448.f);
+    const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+    return uint32_t(__builtin_amdgcn_cvt_pk_fp8_f32(c, d, lo, true));
+}
+
 // Tiles of 64 rows x 64 columns over x [R][C]: q[r][c] for c < ldq (if q;
 // zero codes for c >= C) and qt[c][r] for r < ldt (if qt; zero codes for
 // r >= R).  The grid covers ceil(R' / 64) x ceil(C' / 64) tiles with
@@ -187,6 +201,10 @@ __global__ __launch_bounds__(256) void quant_kernel(const void *__restrict__ x, 
 // quant_kernel with 16-byte loads (V elements per chunk) over tiles of
 // 128 rows x 128 columns: V-byte stores of q (128-byte row segments) and
 // 16-byte stores of qt through a transposed LDS tile (128-byte segments).
+// A thread takes one chunk column of four consecutive rows at a time, so
+// the codes of one column in those rows form one dword of the transposed
+// tile; its 16-byte pieces are XOR-swizzled by row (piece p of row c at
+// p ^ ((c / 8) & 7)), which spreads those dword writes over the banks.
 // Requires x 16-byte aligned, C % V == 0, q (if any) V-byte aligned with
 // ldq % V == 0, qt (if any) 16-byte aligned with ldt % 16 == 0: every chunk
 // then lies wholly inside or wholly outside each bound.  The grid covers
@@ -199,11 +217,27 @@ __global__ __launch_bounds__(256) void quant_vec_kernel(const void *__restrict__
                                                         float *__restrict__ s_out, const float *pa, float *oa,
                                                         const float *pb, float *ob) {
     constexpr int CPR = kQT / V;             // chunks per tile row
-    constexpr int NCH = kQT * CPR / 256;     // chunks per thread
+    constexpr int RG = 256 / CPR;            // four-row groups per pass
+    constexpr int NG = kQT / (4 * RG);       // passes
     constexpr int ESZ = 16 / V;              // bytes per element
     __shared__ float red[4];
-    __shared__ __attribute__((aligned(16))) uint8_t tt[kQT][kQT + 16];   // tt[c][r]
+    __shared__ __attribute__((aligned(16))) uint8_t tt[kQT][kQT];   // tt[c][r], 16-byte pieces swizzled
     const int tid = threadIdx.x;
+    const int ch = tid % CPR, rg = tid / CPR;
+    const int64_t r0 = int64_t(blockIdx.x) * kQT, c0 = int64_t(blockIdx.y) * kQT;
+    const int64_t c = c0 + int64_t(ch) * V;
+    const char *xb = reinterpret_cast<const char *>(x);
+    // every load of the tile first (addresses in bounds; zero selected after)
+    u32x4 v[NG][4];
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t r = r0 + gi * 4 * RG + 4 * rg + j;
+            const bool ok = r < R && c < C;
+            v[gi][j] = *reinterpret_cast<const u32x4 *>(xb + (ok ? r * C + c : 0) * ESZ);
+            if (!ok) v[gi][j] = u32x4{0u, 0u, 0u, 0u};
+        }
     float m = 0.f;
     for (int i = tid; i < nb; i += 256) m = fmaxf(m, pmax[i]);
     m = wave_max(m);
@@ -215,36 +249,36 @@ __global__ __launch_bounds__(256) void quant_vec_kernel(const void *__restrict__
         if (pa && oa) *oa = 1.f / (s * *pa);
         if (pb && ob) *ob = 1.f / (s * *pb);
     }
-    const int64_t r0 = int64_t(blockIdx.x) * kQT, c0 = int64_t(blockIdx.y) * kQT;
-    const char *xb = reinterpret_cast<const char *>(x);
-#pragma unroll 4
-    for (int i = 0; i < NCH; ++i) {
-        const int id = tid + 256 * i;
-        const int rr = id / CPR, ch = id % CPR;
-        const int64_t r = r0 + rr, c = c0 + int64_t(ch) * V;
-        uint32_t w[V / 4];
 #pragma unroll
-        for (int k = 0; k < V / 4; ++k) w[k] = 0u;
-        if (r < R && c < C) {
-            const u32x4 v = *reinterpret_cast<const u32x4 *>(xb + (r * C + c) * ESZ);
+    for (int gi = 0; gi < NG; ++gi) {
+        uint32_t w[4][V / 4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            float f[V];
 #pragma unroll
             for (int e = 0; e < V; ++e) {
-                float f;
-                if constexpr (V == 4) f = __uint_as_float(v[e]);
-                else f = __uint_as_float((e & 1) ? (v[e >> 1] & 0xFFFF0000u) : (v[e >> 1] << 16));
-                w[e >> 2] |= uint32_t(e4m3_rne(f * s)) << (8 * (e & 3));
+                if constexpr (V == 4) f[e] = __uint_as_float(v[gi][j][e]) * s;
+                else f[e] = __uint_as_float((e & 1) ? (v[gi][j][e >> 1] & 0xFFFF0000u) : (v[gi][j][e >> 1] << 16)) * s;
             }
-        }
-        if (q && r < R && c < ldq) {
-            if constexpr (V == 4) {
-                *reinterpret_cast<uint32_t *>(q + r * ldq + c) = w[0];
-            } else {
-                *reinterpret_cast<uint2 *>(q + r * ldq + c) = make_uint2(w[0], w[1]);
+#pragma unroll
+            for (int k = 0; k < V / 4; ++k) w[j][k] = e4m3_pk4(f[4 * k], f[4 * k + 1], f[4 * k + 2], f[4 * k + 3]);
+            const int64_t r = r0 + gi * 4 * RG + 4 * rg + j;
+            if (q && r < R && c < ldq) {
+                if constexpr (V == 4) *reinterpret_cast<uint32_t *>(q + r * ldq + c) = w[j][0];
+                else *reinterpret_cast<uint2 *>(q + r * ldq + c) = make_uint2(w[j][0], w[j][1]);
             }
         }
         if (qt) {
+            // column ch V + e, rows gi 4 RG + 4 rg .. + 3: one dword
+            const int rl = gi * 4 * RG + 4 * rg;
 #pragma unroll
-            for (int e = 0; e < V; ++e) tt[ch * V + e][rr] = uint8_t(w[e >> 2] >> (8 * (e & 3)));
+            for (int e = 0; e < V; ++e) {
+                const int cc = ch * V + e, sh = 8 * (e & 3);
+                const uint32_t d = ((w[0][e >> 2] >> sh) & 0xFFu) | (((w[1][e >> 2] >> sh) & 0xFFu) << 8) |
+                                   (((w[2][e >> 2] >> sh) & 0xFFu) << 16) | (((w[3][e >> 2] >> sh) & 0xFFu) << 24);
+                const int piece = (rl >> 4) ^ ((cc >> 3) & 7);
+                *reinterpret_cast<uint32_t *>(&tt[cc][piece * 16 + (rl & 15)]) = d;
+            }
         }
     }
     if (!qt) return;
@@ -254,9 +288,10 @@ __global__ __launch_bounds__(256) void quant_vec_kernel(const void *__restrict__
     for (int i = 0; i < kQT * 8 / 256; ++i) {
         const int id = tid + 256 * i;
         const int cc = id >> 3, part = id & 7;
-        const int64_t c = c0 + cc, r = r0 + part * 16;
-        if (c < C && r < ldt)
-            *reinterpret_cast<u32x4 *>(qt + c * ldt + r) = *reinterpret_cast<const u32x4 *>(&tt[cc][part * 16]);
+        const int64_t cq = c0 + cc, r = r0 + part * 16;
+        if (cq < C && r < ldt)
+            *reinterpret_cast<u32x4 *>(qt + cq * ldt + r) =
+                *reinterpret_cast<const u32x4 *>(&tt[cc][(part ^ ((cc >> 3) & 7)) * 16]);
     }
 }
 
