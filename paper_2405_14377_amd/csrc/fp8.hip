@@ -79,15 +79,20 @@ __global__ __launch_bounds__(kAmaxThreads) void amax_vec_kernel(const void *__re
     __shared__ float red[kAmaxThreads / 64];
     const u32x4 *xv = reinterpret_cast<const u32x4 *>(x);
     const int64_t nv = n / V;
-    const int64_t stride = int64_t(gridDim.x) * kAmaxThreads;
-    int64_t i = int64_t(blockIdx.x) * kAmaxThreads + threadIdx.x;
+    // one contiguous range of 16-byte chunks per workgroup, walked with
+    // eight loads in flight per thread
+    const int64_t per = (nv + gridDim.x - 1) / gridDim.x;
+    const int64_t b1 = min(nv, (int64_t(blockIdx.x) + 1) * per);
+    int64_t i = int64_t(blockIdx.x) * per + threadIdx.x;
     float m = 0.f;
-    for (; i + 3 * stride < nv; i += 4 * stride) {
-        const u32x4 a = xv[i], b = xv[i + stride], c = xv[i + 2 * stride], d = xv[i + 3 * stride];
-        m = fmaxf(fmaxf(m, fmaxf(chunk_absmax<V>(a), chunk_absmax<V>(b))),
-                  fmaxf(chunk_absmax<V>(c), chunk_absmax<V>(d)));
+    for (; i + 7 * kAmaxThreads < b1; i += 8 * kAmaxThreads) {
+        u32x4 a[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) a[u] = xv[i + u * kAmaxThreads];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) m = fmaxf(m, chunk_absmax<V>(a[u]));
     }
-    for (; i < nv; i += stride) m = fmaxf(m, chunk_absmax<V>(xv[i]));
+    for (; i < b1; i += kAmaxThreads) m = fmaxf(m, chunk_absmax<V>(xv[i]));
     if (blockIdx.x == 0)
         for (int64_t j = nv * V + threadIdx.x; j < n; j += kAmaxThreads) m = fmaxf(m, fabsf(load_act(x, dtype, j)));
     m = wave_max(m);
