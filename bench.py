@@ -237,6 +237,39 @@ def kernel_stats_summary(prof_dir, out_path, command, top=25):
     open(out_path, "w").write("\n".join(lines) + "\n")
 
 
+def headline_products(prof_dir, out_path):
+    """Append to a kernel-statistics summary of the headline run the mean
+    duration of each of its two K-contiguous products, which share one
+    kernel and grid: in the kernel trace every layer's step starts with its
+    fold launch (the up layer's fold grid is the first one seen) and its
+    first two persistent-kernel launches after it are the forward and dX
+    (up layer: 65536 x 4096 x 1024, then 65536 x 1024 x 4096; down layer
+    the other way round)."""
+    rows = sorted(_read_csv(_find(prof_dir, "kernel_trace.csv")), key=lambda r: int(r["Start_Timestamp"]))
+    up_grid = None
+    dur = {"65536x4096x1024": [], "65536x1024x4096": []}
+    layer, seen = None, 0
+    for r in rows:
+        name = r["Kernel_Name"]
+        if "fold_kernel" in name:
+            g = (r["Grid_Size_X"], r["Grid_Size_Y"])
+            up_grid = up_grid or g
+            layer, seen = ("up" if g == up_grid else "down"), 0
+        elif "gemm_dma_pers_kernel<false>" in name and layer and seen < 2:
+            first = (layer == "up") == (seen == 0)
+            dur["65536x4096x1024" if first else "65536x1024x4096"].append(
+                (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+            seen += 1
+    lines = ["", "Per product of `gemm_dma_pers_kernel<false>` (kernel trace of the same run; each layer's two",
+             "launches after its fold are its forward and dX):", "",
+             "| product | calls | avg us |", "|---|---:|---:|"]
+    for k, v in dur.items():
+        if v:
+            lines.append(f"| {k.replace('x', ' x ')} K-contiguous | {len(v)} | {sum(v) / len(v):.2f} |")
+    open(out_path, "a").write("\n".join(lines) + "\n")
+    return {k: (len(v), sum(v) / len(v) if v else 0.0) for k, v in dur.items()}
+
+
 def traffic_summary(fetch_dir, write_dir, kernel, grid, tag, act, out_path, commands, sources=None, out_bytes=None):
     """HBM bytes per launch of one kernel from two counter passes (FETCH_SIZE,
     WRITE_SIZE, KiB per dispatch), each scaled by what the same counter reads
@@ -648,6 +681,8 @@ def main():
     ap.add_argument("--commands", nargs="*", default=[], help="commands recorded in a summary")
     ap.add_argument("--sources", nargs="*", default=None,
                     help="source files (repository paths) a traffic summary is keyed to (default: the GEMM sources)")
+    ap.add_argument("--headline-products", nargs=2, metavar=("PROF_DIR", "OUT_MD"),
+                    help="append the per-product means of the headline's persistent GEMM to a summary (no GPU)")
     ap.add_argument("--out-bytes", type=float, default=None,
                     help="traffic summary: only the dispatches whose output (write counter) is this many bytes")
     ap.add_argument("--fp8-only", action="store_true", help="only the mixed-precision (FP8) figures")
@@ -656,6 +691,9 @@ def main():
     args = ap.parse_args()
     if args.stats_summary:
         kernel_stats_summary(*args.stats_summary)
+        return
+    if args.headline_products:
+        print(headline_products(*args.headline_products))
         return
     if args.traffic_summary:
         fd, wd, kern, grid, tag = args.traffic_summary
