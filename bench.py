@@ -261,7 +261,9 @@ def headline_products(prof_dir, out_path):
                 (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
             seen += 1
     lines = ["", "Per product of `gemm_dma_pers_kernel<false>` (kernel trace of the same run; each layer's two",
-             "launches after its fold are its forward and dX):", "",
+             "launches after its fold are its forward and dX; "
+             f"`python3 bench.py --headline-products {os.path.relpath(prof_dir, ROOT)} {os.path.relpath(out_path, ROOT)}`,",
+             "no GPU needed for this step):", "",
              "| product | calls | avg us |", "|---|---:|---:|"]
     for k, v in dur.items():
         if v:
