@@ -707,8 +707,8 @@ def main():
         return
     ws = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or ws != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path (the layer shards by tokens with "
-              "one all-reduce of the core gradients; see the design notes). Use --gpus 1.", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library has no multi-GPU path (a layer would shard by tokens, "
+              "with one all-reduce of the core gradients per step). Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
     import torch
     if not torch.cuda.is_available():

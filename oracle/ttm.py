@@ -1,6 +1,6 @@
 """fp64 oracle for one TTM linear layer Y = X W (test infrastructure only).
 
-Conventions (fixed by the paper and the readings listed in the design notes):
+Conventions (the paper's, and the readings taken where it leaves a choice):
 
 * Core k (0-based here, k = 0..d-1) is G_k[r_k, m_k, n_k, r_{k+1}] with
   r_0 = r_d = 1: ``m`` is the output factor, ``n`` the input factor (the TTM
